@@ -208,7 +208,10 @@ def run_points(model: dict, traces, points: dict, *, per_request=False, iter_cap
         pts[i] = _point(points, i)
     out = np.zeros(max(n_points, 1), dtype=POINT_OUT_DTYPE)
     max_n = max([len(t["arrival_ns"]) for t in traces] + [1])
-    req = np.zeros((n_points, max_n), dtype=REQ_DTYPE) if per_request else None
+    req = None
+    if per_request:  # rows of shorter traces are padded with pending records
+        req = np.zeros((n_points, max_n), dtype=REQ_DTYPE)
+        req["admit_ns"] = req["first_token_ns"] = req["finish_ns"] = -1
     opt = _options(iter_cap, slo_ttft_ns, slo_tpot_ns, n_threads, 0)
     rc = lib().tso_run_points(C.byref(_model(model)), keep.structs, len(traces), pts, n_points,
                               C.byref(opt), out.ctypes.data,

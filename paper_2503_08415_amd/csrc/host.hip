@@ -1,0 +1,528 @@
+// host.hip -- C ABI of the serving-simulation sweep (see include/ts_sweep.h).
+//
+// ts_sweep_create validates every input on the host, derives each design
+// point's block budget and reciprocals, checks that every cost-model integer
+// stays exact in fp64, orders the points longest-expected-first and uploads
+// traces and points.  ts_sweep_run enqueues the simulation kernels (one
+// per register-chunk class, on forked streams so their tails overlap) and
+// the statistics kernel.  ts_sweep_results copies the results back.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <numeric>
+#include <vector>
+
+#include "sweep_internal.h"
+
+namespace tsw {
+template <int NCH>
+__global__ void sim_kernel(SimArgs A);
+__global__ void stats_kernel(const int64_t* e2e, const int64_t* ttft, ts_point_result* res,
+                             int max_n, int n_points);
+__global__ void fill_pending_kernel(ts_req_result* r, size_t n);
+__global__ void reset_counters_kernel(unsigned int* c, int n);
+}  // namespace tsw
+
+using namespace tsw;
+
+namespace {
+
+thread_local char g_err[256];
+
+constexpr int kClasses = 3;                 // register chunks per lane: 1, 2, 4
+constexpr int kClassChunks[kClasses] = {1, 2, 4};
+
+int class_of(int max_batch) { return max_batch <= 64 ? 0 : (max_batch <= 128 ? 1 : 2); }
+
+int device_error(hipError_t e, const char* what) {
+  snprintf(g_err, sizeof g_err, "%s: %s", what, hipGetErrorString(e));
+  return TS_ERR_DEVICE;
+}
+
+bool model_ok(const ts_model* m) {
+  if (!m) return false;
+  if (m->n_layers < 1 || m->n_layers > 4096) return false;
+  if (m->d_model < 1 || m->d_model > 131072) return false;
+  if (m->n_heads < 1 || m->n_kv_heads < 1) return false;
+  if (m->d_model % m->n_heads != 0 || m->n_heads % m->n_kv_heads != 0) return false;
+  if (m->ffn_dim < 1 || m->ffn_dim > 524288) return false;
+  if (m->ffn_gated != 0 && m->ffn_gated != 1) return false;
+  if (m->vocab < 1 || m->vocab > 4194304) return false;
+  if (m->w_bytes < 1 || m->w_bytes > 16 || m->kv_bytes < 1 || m->kv_bytes > 16) return false;
+  if (m->weights_in_capacity != 0 && m->weights_in_capacity != 1) return false;
+  return true;
+}
+
+struct TraceStats {
+  int64_t max_po = 0;     // largest prompt + output
+  double mean_p = 0, mean_o = 0, span_s = 0;
+};
+
+struct Shape {
+  int64_t L, d, dkv, f, g, V, e, ekv;
+};
+
+Shape shape_of(const ts_model* m) {
+  Shape s;
+  s.L = m->n_layers;
+  s.d = m->d_model;
+  s.dkv = (int64_t)m->n_kv_heads * (m->d_model / m->n_heads);
+  s.f = m->ffn_dim;
+  s.g = 1 + m->ffn_gated;
+  s.V = m->vocab;
+  s.e = m->w_bytes;
+  s.ekv = m->kv_bytes;
+  return s;
+}
+
+CostCoef make_coef(const Shape& s) {
+  CostCoef c;
+  c.f_qkv = 2 * s.d * (s.d + 2 * s.dkv);
+  c.b_qkv0 = s.e * s.d * (s.d + 2 * s.dkv);
+  c.b_qkv = s.e * s.d + s.ekv * 2 * s.dkv + s.e * s.d;
+  c.f_attp = 4 * s.d;
+  c.b_attp_c = s.ekv * 2 * s.dkv;
+  c.b_attp_t = 2 * s.e * s.d;
+  c.f_attd = 4 * s.d;
+  c.b_attd_c = s.ekv * 2 * s.dkv;
+  c.b_attd_n = 2 * s.e * s.d;
+  c.f_out = 2 * s.d * s.d;
+  c.b_out0 = s.e * s.d * s.d;
+  c.b_out = 2 * s.e * s.d;
+  c.f_up = 2 * s.g * s.d * s.f;
+  c.b_up0 = s.e * s.g * s.d * s.f;
+  c.b_up = s.e * (s.d + s.g * s.f);
+  c.f_dn = 2 * s.f * s.d;
+  c.b_dn0 = s.e * s.f * s.d;
+  c.b_dn = s.e * (s.f + s.d);
+  c.f_lm = 2 * s.d * s.V;
+  c.b_lm0 = s.e * s.d * s.V;
+  c.b_lm = s.e * (s.d + s.V);
+  c.n_layers = (double)s.L;
+  return c;
+}
+
+// Upper bounds of every FLOP / byte count and of the iteration time for a
+// point whose requests hold at most max_po tokens.
+bool exact_and_bounded(const CostCoef& c, int64_t max_po, int M, int K, double iF, double iB) {
+  const double po = (double)max_po;
+  const double T = K > 0 ? (double)K : (double)M * po;   // tokens per iteration
+  const double AP = T * po;                             // sum q*(c0+q) >= causal pairs
+  const double CP = (double)M * po, CD = (double)M * po, nD = M, R = M;
+  const double lim = 9007199254740992.0;                 // 2^53
+  const double F[7] = {c.f_qkv * T, c.f_attp * AP, c.f_attd * CD, c.f_out * T, c.f_up * T,
+                       c.f_dn * T, c.f_lm * R};
+  const double Bv[7] = {c.b_qkv0 + c.b_qkv * T, c.b_attp_c * CP + c.b_attp_t * T,
+                        c.b_attd_c * CD + c.b_attd_n * nD, c.b_out0 + c.b_out * T,
+                        c.b_up0 + c.b_up * T, c.b_dn0 + c.b_dn * T, c.b_lm0 + c.b_lm * R};
+  double tmax = 0;
+  for (int i = 0; i < 7; ++i) {
+    if (!(F[i] < lim) || !(Bv[i] < lim)) return false;
+    const double t = std::max(F[i] * iF, Bv[i] * iB);
+    tmax += i < 6 ? c.n_layers * t : t;
+  }
+  // per-lane int32 partial sums (tokens, keys) must not overflow either
+  if (T * 4 > 2147483647.0 || CD * 4 > 2147483647.0) return false;
+  return tmax < 1125899906842624.0;  // 2^50 ns per iteration
+}
+
+// Longest-expected-first ordering key: a rough count of iterations.  Under
+// light load each request runs about prefill + output iterations on its own;
+// under load the running set shares iterations.  Only the order of the
+// points depends on it, never a result.
+double work_estimate(const TraceStats& ts, int64_t n, int M, int K, double peak, double bw,
+                     double weight_bytes) {
+  const double chunks = K > 0 ? std::ceil(ts.mean_p / K) : 1.0;
+  const double per_req = ts.mean_o + chunks;
+  const double rate = ts.span_s > 0 ? (double)n / ts.span_s : 1.0;
+  const double t_dec = weight_bytes / bw;
+  const double t_pre = 2.0 * weight_bytes / 2.0 * ts.mean_p / peak;
+  const double busy = rate * (t_pre + ts.mean_o * t_dec);  // mean concurrency
+  const double conc = std::min((double)M, std::max(1.0, busy));
+  return (double)n * per_req / conc;
+}
+
+}  // namespace
+
+struct ts_sweep {
+  int device = 0;
+  int32_t n_points = 0, max_n = 0;
+  uint32_t flags = 0;
+  int64_t iter_cap = 0, slo_ttft = 0, slo_tpot = 0, time_limit_ms = 0;
+  CostCoef coef{};
+  TraceRec* d_recs = nullptr;
+  DevPoint* d_points = nullptr;
+  int32_t* d_order = nullptr;       // all classes, concatenated
+  unsigned int* d_counter = nullptr;
+  QEntry* d_queue[kClasses] = {nullptr, nullptr, nullptr};
+  ts_point_result* d_res = nullptr;
+  ts_req_result* d_req = nullptr;
+  int64_t* d_e2e = nullptr;
+  int64_t* d_ttft = nullptr;
+  int class_off[kClasses] = {0, 0, 0}, class_n[kClasses] = {0, 0, 0};
+  int grid[kClasses] = {0, 0, 0};
+  int stats_grid = 0;
+  hipStream_t side[kClasses] = {nullptr, nullptr, nullptr};
+  hipEvent_t ev_fork = nullptr, ev_join[kClasses] = {nullptr, nullptr, nullptr};
+  hipEvent_t ev_t0 = nullptr, ev_t1 = nullptr, ev_t2 = nullptr;
+  hipStream_t last_stream = nullptr;
+  bool ran = false;
+};
+
+namespace {
+
+void release(ts_sweep* h) {
+  if (!h) return;
+  (void)hipFree(h->d_recs);
+  (void)hipFree(h->d_points);
+  (void)hipFree(h->d_order);
+  (void)hipFree(h->d_counter);
+  for (int c = 0; c < kClasses; ++c) (void)hipFree(h->d_queue[c]);
+  (void)hipFree(h->d_res);
+  (void)hipFree(h->d_req);
+  (void)hipFree(h->d_e2e);
+  (void)hipFree(h->d_ttft);
+  for (int c = 0; c < kClasses; ++c) {
+    if (h->side[c]) (void)hipStreamDestroy(h->side[c]);
+    if (h->ev_join[c]) (void)hipEventDestroy(h->ev_join[c]);
+  }
+  if (h->ev_fork) (void)hipEventDestroy(h->ev_fork);
+  if (h->ev_t0) (void)hipEventDestroy(h->ev_t0);
+  if (h->ev_t1) (void)hipEventDestroy(h->ev_t1);
+  if (h->ev_t2) (void)hipEventDestroy(h->ev_t2);
+  delete h;
+}
+
+template <typename T>
+hipError_t dev_alloc(T** p, size_t count) {
+  *p = nullptr;
+  if (count == 0) count = 1;
+  return hipMalloc((void**)p, count * sizeof(T));
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* ts_status_str(int status) {
+  switch (status) {
+    case TS_OK: return "ok";
+    case TS_ERR_ARG: return "invalid argument";
+    case TS_ERR_UNSUPPORTED: return "unsupported input (batch cap, policy, or exact-fp64 range)";
+    case TS_ERR_OOM: return "out of memory";
+    case TS_ERR_DEVICE: return g_err[0] ? g_err : "HIP device error";
+    case TS_ERR_STATE: return "call out of order";
+    default: return "unknown status";
+  }
+}
+
+int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_traces,
+                    const ts_point* points, int32_t n_points, const ts_options* opt,
+                    ts_sweep** out) {
+  if (!out) return TS_ERR_ARG;
+  *out = nullptr;
+  g_err[0] = 0;
+  // ---------------------------------------------------------- validation
+  if (!model_ok(model)) return TS_ERR_ARG;
+  if (!traces || n_traces < 1 || !points || n_points < 0) return TS_ERR_ARG;
+  int first = 0, count = n_points;
+  uint32_t flags = 0;
+  int64_t iter_cap = (int64_t)1 << 40, slo_ttft = 15000000000LL, slo_tpot = 300000000LL;
+  int64_t time_limit_ms = 0;
+  if (opt) {
+    if (opt->flags & ~TS_F_PER_REQUEST) return TS_ERR_ARG;
+    flags = opt->flags;
+    if (opt->first_point < 0 || opt->n_points < 0) return TS_ERR_ARG;
+    first = opt->first_point;
+    if (first > n_points) return TS_ERR_ARG;
+    count = opt->n_points == 0 ? n_points - first : opt->n_points;
+    if ((int64_t)first + count > n_points) return TS_ERR_ARG;
+    if (opt->iter_cap < 0 || opt->slo_ttft_ns < 0 || opt->slo_tpot_ns < 0) return TS_ERR_ARG;
+    if (opt->iter_cap > 0) iter_cap = opt->iter_cap;
+    if (opt->slo_ttft_ns > 0) slo_ttft = opt->slo_ttft_ns;
+    if (opt->slo_tpot_ns > 0) slo_tpot = opt->slo_tpot_ns;
+    if (opt->point_time_limit_ms < 0) return TS_ERR_ARG;
+    time_limit_ms = opt->point_time_limit_ms;
+  }
+  std::vector<TraceStats> tstats((size_t)n_traces);
+  std::vector<int64_t> toff((size_t)n_traces);
+  int64_t total_recs = 0, max_n = 0;
+  for (int k = 0; k < n_traces; ++k) {
+    const ts_trace& tr = traces[k];
+    if (tr.n < 0) return TS_ERR_ARG;
+    if (tr.n > 0 && (!tr.arrival_ns || !tr.prompt_len || !tr.output_len)) return TS_ERR_ARG;
+    TraceStats& s = tstats[(size_t)k];
+    double sp = 0, so = 0;
+    for (int i = 0; i < tr.n; ++i) {
+      const int64_t a = tr.arrival_ns[i];
+      const int32_t p = tr.prompt_len[i], o = tr.output_len[i];
+      if (a < 0 || (i > 0 && a < tr.arrival_ns[i - 1])) return TS_ERR_ARG;
+      if (p < 1 || o < 1 || p > TS_MAX_TOKENS || o > TS_MAX_TOKENS) return TS_ERR_ARG;
+      s.max_po = std::max<int64_t>(s.max_po, (int64_t)p + o);
+      sp += p;
+      so += o;
+    }
+    if (tr.n > 0) {
+      s.mean_p = sp / tr.n;
+      s.mean_o = so / tr.n;
+      s.span_s = (double)(tr.arrival_ns[tr.n - 1] - tr.arrival_ns[0]) * 1e-9;
+    }
+    toff[(size_t)k] = total_recs;
+    total_recs += tr.n;
+    max_n = std::max<int64_t>(max_n, tr.n);
+  }
+  if (total_recs > INT32_MAX) return TS_ERR_UNSUPPORTED;
+  const Shape sh = shape_of(model);
+  const CostCoef coef = make_coef(sh);
+  const int64_t kv_tok = 2 * sh.L * sh.dkv * sh.ekv;
+  const int64_t weights =
+      sh.e * (sh.L * (sh.d * (sh.d + 2 * sh.dkv) + sh.d * sh.d + (sh.g + 1) * sh.d * sh.f) +
+              2 * sh.V * sh.d);
+
+  std::vector<DevPoint> dp((size_t)count);
+  std::vector<double> est((size_t)count);
+  for (int i = 0; i < count; ++i) {
+    const ts_point& p = points[first + i];
+    if (!std::isfinite(p.peak_flops) || !(p.peak_flops > 0) || !std::isfinite(p.mem_bw) ||
+        !(p.mem_bw > 0))
+      return TS_ERR_ARG;
+    if (p.capacity_bytes <= 0 || p.mem_util_permille < 1 || p.mem_util_permille > 1000)
+      return TS_ERR_ARG;
+    if (p.block_size < 1 || p.block_size > 65536) return TS_ERR_ARG;
+    if (p.max_batch < 1) return TS_ERR_ARG;
+    if (p.max_batch > TS_MAX_BATCH) return TS_ERR_UNSUPPORTED;
+    if (p.chunk_size != 0 && (p.chunk_size < p.max_batch || p.chunk_size > TS_MAX_TOKENS))
+      return TS_ERR_ARG;
+    if (p.trace_id < 0 || p.trace_id >= n_traces) return TS_ERR_ARG;
+    if (p.policy != 0) return TS_ERR_UNSUPPORTED;
+    // KV block budget: floor(capacity * util / 1000), minus the weights when
+    // they share the memory, in whole blocks of block_size tokens
+    const __int128 usable = ((__int128)p.capacity_bytes * p.mem_util_permille) / 1000;
+    const __int128 budget = usable - (model->weights_in_capacity ? weights : 0);
+    const __int128 per_block = (__int128)p.block_size * kv_tok;
+    const __int128 nb = budget > 0 ? budget / per_block : 0;
+    if (nb > ((__int128)1 << 30)) return TS_ERR_UNSUPPORTED;
+    const TraceStats& ts = tstats[(size_t)p.trace_id];
+    DevPoint& d = dp[(size_t)i];
+    d.inv_flops_ns = 1e9 / p.peak_flops;
+    d.inv_bw_ns = 1e9 / p.mem_bw;
+    d.num_blocks = (int32_t)nb;
+    d.block = p.block_size;
+    d.cap_tokens = (int64_t)nb * p.block_size;
+    d.max_batch = p.max_batch;
+    d.chunk = p.chunk_size;
+    d.trace_off = (int32_t)toff[(size_t)p.trace_id];
+    d.n = traces[p.trace_id].n;
+    d.out_index = i;
+    d.may_reject = ts.max_po > d.cap_tokens ? 1 : 0;
+    if (!exact_and_bounded(coef, ts.max_po, p.max_batch, p.chunk_size, d.inv_flops_ns,
+                           d.inv_bw_ns))
+      return TS_ERR_UNSUPPORTED;
+    est[(size_t)i] = work_estimate(ts, d.n, p.max_batch, p.chunk_size, p.peak_flops, p.mem_bw,
+                                   (double)weights);
+  }
+
+  // ---------------------------------------------------------- classes + order
+  std::vector<int32_t> order;
+  order.reserve((size_t)count);
+  ts_sweep* h = new (std::nothrow) ts_sweep();
+  if (!h) return TS_ERR_OOM;
+  for (int c = 0; c < kClasses; ++c) {
+    std::vector<int32_t> cls;
+    for (int i = 0; i < count; ++i)
+      if (class_of(dp[(size_t)i].max_batch) == c) cls.push_back(i);
+    std::stable_sort(cls.begin(), cls.end(),
+                     [&](int32_t a, int32_t b) { return est[(size_t)a] > est[(size_t)b]; });
+    h->class_off[c] = (int)order.size();
+    h->class_n[c] = (int)cls.size();
+    order.insert(order.end(), cls.begin(), cls.end());
+  }
+  h->n_points = count;
+  h->max_n = (int32_t)std::max<int64_t>(max_n, 1);
+  h->flags = flags;
+  h->iter_cap = iter_cap;
+  h->slo_ttft = slo_ttft;
+  h->slo_tpot = slo_tpot;
+  h->time_limit_ms = time_limit_ms;
+  h->coef = coef;
+
+  // ---------------------------------------------------------- device
+  hipError_t e = hipGetDevice(&h->device);
+  if (e != hipSuccess) { release(h); return device_error(e, "hipGetDevice"); }
+  hipDeviceProp_t prop;
+  e = hipGetDeviceProperties(&prop, h->device);
+  if (e != hipSuccess) { release(h); return device_error(e, "hipGetDeviceProperties"); }
+  const int n_cu = prop.multiProcessorCount;
+  for (int c = 0; c < kClasses; ++c) {
+    if (h->class_n[c] == 0) continue;
+    int per_cu = 0;
+    const void* fn = c == 0 ? (const void*)sim_kernel<1>
+                     : c == 1 ? (const void*)sim_kernel<2> : (const void*)sim_kernel<4>;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, 64, 0);
+    if (e != hipSuccess) { release(h); return device_error(e, "occupancy query"); }
+    per_cu = std::max(per_cu, 1);
+    h->grid[c] = std::min(h->class_n[c], n_cu * per_cu);
+  }
+  h->stats_grid = std::max(1, std::min(count, n_cu * 8));
+
+  std::vector<TraceRec> recs((size_t)std::max<int64_t>(total_recs, 1));
+  for (int k = 0; k < n_traces; ++k) {
+    const ts_trace& tr = traces[k];
+    for (int i = 0; i < tr.n; ++i) {
+      TraceRec& r = recs[(size_t)(toff[(size_t)k] + i)];
+      r.arrival_ns = tr.arrival_ns[i];
+      r.prompt = tr.prompt_len[i];
+      r.output = tr.output_len[i];
+    }
+  }
+  const size_t per_point = (size_t)h->max_n;
+  hipError_t ae = hipSuccess;
+  if (ae == hipSuccess) ae = dev_alloc(&h->d_recs, recs.size());
+  if (ae == hipSuccess) ae = dev_alloc(&h->d_points, dp.size());
+  if (ae == hipSuccess) ae = dev_alloc(&h->d_order, order.size());
+  if (ae == hipSuccess) ae = dev_alloc(&h->d_counter, (size_t)kClasses);
+  for (int c = 0; c < kClasses && ae == hipSuccess; ++c)
+    if (h->grid[c] > 0) ae = dev_alloc(&h->d_queue[c], (size_t)h->grid[c] * kQueueCap);
+  if (ae == hipSuccess) ae = dev_alloc(&h->d_res, (size_t)count);
+  if (ae == hipSuccess) ae = dev_alloc(&h->d_e2e, (size_t)count * per_point);
+  if (ae == hipSuccess) ae = dev_alloc(&h->d_ttft, (size_t)count * per_point);
+  if (ae == hipSuccess && (flags & TS_F_PER_REQUEST))
+    ae = dev_alloc(&h->d_req, (size_t)count * per_point);
+  if (ae != hipSuccess) {
+    const int rc = ae == hipErrorOutOfMemory ? TS_ERR_OOM : device_error(ae, "hipMalloc");
+    if (rc == TS_ERR_OOM) snprintf(g_err, sizeof g_err, "device allocation failed");
+    release(h);
+    return rc;
+  }
+  e = hipMemcpy(h->d_recs, recs.data(), recs.size() * sizeof(TraceRec), hipMemcpyHostToDevice);
+  if (e == hipSuccess && !dp.empty())
+    e = hipMemcpy(h->d_points, dp.data(), dp.size() * sizeof(DevPoint), hipMemcpyHostToDevice);
+  if (e == hipSuccess && !order.empty())
+    e = hipMemcpy(h->d_order, order.data(), order.size() * sizeof(int32_t),
+                  hipMemcpyHostToDevice);
+  if (e != hipSuccess) { release(h); return device_error(e, "upload"); }
+  for (int c = 0; c < kClasses && e == hipSuccess; ++c) {
+    e = hipStreamCreateWithFlags(&h->side[c], hipStreamNonBlocking);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&h->ev_join[c], hipEventDisableTiming);
+  }
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&h->ev_fork, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreate(&h->ev_t0);
+  if (e == hipSuccess) e = hipEventCreate(&h->ev_t1);
+  if (e == hipSuccess) e = hipEventCreate(&h->ev_t2);
+  if (e != hipSuccess) { release(h); return device_error(e, "stream/event create"); }
+  *out = h;
+  return TS_OK;
+}
+
+int ts_sweep_run(ts_sweep* h, void* hip_stream) {
+  if (!h) return TS_ERR_ARG;
+  hipStream_t s = (hipStream_t)hip_stream;
+  hipError_t e = hipEventRecord(h->ev_t0, s);
+  if (e != hipSuccess) return device_error(e, "event record");
+  reset_counters_kernel<<<1, 64, 0, s>>>(h->d_counter, kClasses);
+  if (h->d_req) {
+    const size_t n = (size_t)h->n_points * (size_t)h->max_n;
+    const int blocks = (int)std::min<size_t>((n + 255) / 256, 65536);
+    fill_pending_kernel<<<std::max(blocks, 1), 256, 0, s>>>(h->d_req, n);
+  }
+  int used = 0;
+  for (int c = 0; c < kClasses; ++c) used += h->class_n[c] > 0;
+  if (used > 1) {
+    e = hipEventRecord(h->ev_fork, s);
+    if (e != hipSuccess) return device_error(e, "event record");
+  }
+  for (int c = 0; c < kClasses; ++c) {
+    if (h->class_n[c] == 0) continue;
+    SimArgs a;
+    a.recs = h->d_recs;
+    a.points = h->d_points;
+    a.order = h->d_order + h->class_off[c];
+    a.n_order = h->class_n[c];
+    a.max_n = h->max_n;
+    a.counter = h->d_counter + c;
+    a.queue = h->d_queue[c];
+    a.res = h->d_res;
+    a.req = h->d_req;
+    a.e2e = h->d_e2e;
+    a.ttft = h->d_ttft;
+    a.iter_cap = h->iter_cap;
+    a.slo_ttft_ns = h->slo_ttft;
+    a.slo_tpot_ns = h->slo_tpot;
+    a.time_limit_ticks = (uint64_t)h->time_limit_ms * 100000ull;  // 100 MHz clock
+    a.coef = h->coef;
+    hipStream_t ks = s;
+    if (used > 1) {
+      ks = h->side[c];
+      e = hipStreamWaitEvent(ks, h->ev_fork, 0);
+      if (e != hipSuccess) return device_error(e, "stream wait");
+    }
+    if (kClassChunks[c] == 1) sim_kernel<1><<<h->grid[c], 64, 0, ks>>>(a);
+    else if (kClassChunks[c] == 2) sim_kernel<2><<<h->grid[c], 64, 0, ks>>>(a);
+    else sim_kernel<4><<<h->grid[c], 64, 0, ks>>>(a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return device_error(e, "sim kernel launch");
+    if (used > 1) {
+      e = hipEventRecord(h->ev_join[c], ks);
+      if (e == hipSuccess) e = hipStreamWaitEvent(s, h->ev_join[c], 0);
+      if (e != hipSuccess) return device_error(e, "stream join");
+    }
+  }
+  e = hipEventRecord(h->ev_t1, s);
+  if (e != hipSuccess) return device_error(e, "event record");
+  if (h->n_points > 0)
+    stats_kernel<<<h->stats_grid, 256, 0, s>>>(h->d_e2e, h->d_ttft, h->d_res, h->max_n,
+                                                h->n_points);
+  e = hipGetLastError();
+  if (e != hipSuccess) return device_error(e, "stats kernel launch");
+  e = hipEventRecord(h->ev_t2, s);
+  if (e != hipSuccess) return device_error(e, "event record");
+  h->last_stream = s;
+  h->ran = true;
+  return TS_OK;
+}
+
+int ts_sweep_results(ts_sweep* h, ts_point_result* out_points, ts_req_result* out_requests) {
+  if (!h) return TS_ERR_ARG;
+  if (!h->ran) return TS_ERR_STATE;
+  if (out_requests && !h->d_req) return TS_ERR_STATE;
+  if (!out_points && h->n_points > 0) return TS_ERR_ARG;
+  hipError_t e = hipStreamSynchronize(h->last_stream);
+  if (e != hipSuccess) return device_error(e, "stream synchronize");
+  if (h->n_points > 0) {
+    e = hipMemcpy(out_points, h->d_res, (size_t)h->n_points * sizeof(ts_point_result),
+                  hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return device_error(e, "copy results");
+  }
+  if (out_requests && h->n_points > 0) {
+    e = hipMemcpy(out_requests, h->d_req,
+                  (size_t)h->n_points * (size_t)h->max_n * sizeof(ts_req_result),
+                  hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return device_error(e, "copy request records");
+  }
+  return TS_OK;
+}
+
+int ts_sweep_shape(const ts_sweep* h, int32_t* n_points, int32_t* max_n) {
+  if (!h || !n_points || !max_n) return TS_ERR_ARG;
+  *n_points = h->n_points;
+  *max_n = h->max_n;
+  return TS_OK;
+}
+
+int ts_sweep_timing(ts_sweep* h, float* sim_ms, float* stats_ms) {
+  if (!h || !sim_ms || !stats_ms) return TS_ERR_ARG;
+  if (!h->ran) return TS_ERR_STATE;
+  hipError_t e = hipEventSynchronize(h->ev_t2);
+  if (e == hipSuccess) e = hipEventElapsedTime(sim_ms, h->ev_t0, h->ev_t1);
+  if (e == hipSuccess) e = hipEventElapsedTime(stats_ms, h->ev_t1, h->ev_t2);
+  if (e != hipSuccess) return device_error(e, "event timing");
+  return TS_OK;
+}
+
+void ts_sweep_destroy(ts_sweep* h) { release(h); }
+
+}  // extern "C"

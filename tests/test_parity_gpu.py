@@ -1,0 +1,271 @@
+"""Parity of the HIP sweep with the CPU oracle, through the C ABI.
+
+Scheduling decisions, timestamps and every integer aggregate must match
+bit for bit; the fp64 time integral of used blocks within 1e-9 relative.
+The per-point digest hashes every finished / rejected request's record, so
+matching digests cover per-request parity for points whose records are not
+copied back.  Every GPU run carries an iteration cap derived from the
+oracle so a scheduling bug ends as a mismatch, never as a hang.
+"""
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import pytest
+
+from paper_2503_08415_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+REL_TOL = 1e-9
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def S():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    from paper_2503_08415_amd import sweep
+    sweep.lib()
+    return sweep
+
+
+def gpu_run(S, model, traces, points, per_request=False, **kw):
+    kw.setdefault("point_time_limit_ms", 60_000)  # watchdog: a stuck point ends, never hangs
+    sw = S.Sweep(model, traces, points, per_request=per_request, **kw)
+    try:
+        sw.run()
+        out, req = sw.results()
+    finally:
+        sw.close()
+    return out, req
+
+
+def compare_points(g, o, label=""):
+    assert len(g) == len(o)
+    bad = []
+    for f in o.dtype.names:
+        if f == "used_block_ns":
+            ok = np.isclose(g[f], o[f], rtol=REL_TOL, atol=0.0)
+        else:
+            ok = g[f] == o[f]
+        if not ok.all():
+            idx = np.nonzero(~ok)[0]
+            bad.append((f, int(idx.size), int(idx[0]), g[f][idx[0]], o[f][idx[0]]))
+    assert not bad, "%s point mismatches (field, count, first, gpu, oracle): %s" % (label, bad[:8])
+
+
+def compare_requests(g, o, label=""):
+    assert g.shape == o.shape
+    for f in o.dtype.names:
+        ne = g[f] != o[f]
+        if ne.any():
+            p, r = [int(x[0]) for x in np.nonzero(ne)]
+            raise AssertionError("%s request mismatch in %s at point %d request %d: gpu %s oracle %s"
+                                 % (label, f, p, r, g[p, r], o[p, r]))
+
+
+def cap_from(oracle_out):
+    return int(oracle_out["n_iters"].max()) * 2 + 1000
+
+
+def hand_sweep():
+    with open(os.path.join(GOLD, "hand_traces.json")) as f:
+        g = json.load(f)
+    traces, rows = [], []
+    for k, c in enumerate(g["cases"]):
+        r = c["requests"]
+        traces.append({"arrival_ns": np.array([x[0] for x in r], np.int64),
+                       "prompt_len": np.array([x[1] for x in r], np.int32),
+                       "output_len": np.array([x[2] for x in r], np.int32)})
+        nb, b = c["num_blocks"], c["block_size"]
+        rows.append(dict(peak_flops=1e300, mem_bw=1e300,
+                         capacity_bytes=nb * b * 16 if nb > 0 else 1, mem_util_permille=1000,
+                         block_size=b, max_batch=c["max_batch"], chunk_size=c["chunk_size"],
+                         trace_id=k))
+    pts = {k: np.array([r[k] for r in rows]) for k in rows[0]}
+    pts = {k: (v.astype(np.float64) if k in ("peak_flops", "mem_bw") else
+               v.astype(np.int64) if k == "capacity_bytes" else v.astype(np.int32))
+           for k, v in pts.items()}
+    return g["model"], traces, pts, g["cases"]
+
+
+def test_hand_traced_schedules_gpu(S, oracle):
+    model, traces, pts, cases = hand_sweep()
+    say("hand traces: %d cases" % len(cases))
+    out, req = gpu_run(S, model, traces, pts, per_request=True, iter_cap=10_000)
+    for k, c in enumerate(cases):
+        n = len(c["requests"])
+        got = [[int(x) for x in r] for r in req[k, :n].tolist()]
+        assert got == c["expect_req"], c["name"]
+        for f, v in c["expect_point"].items():
+            assert out[k][f] == v, (c["name"], f)
+    o_out, o_req = oracle.run_points(model, traces, pts, per_request=True)
+    compare_points(out, o_out, "hand")
+    compare_requests(req, o_req, "hand")
+
+
+@pytest.mark.parametrize("name", ["c1", "c2"])
+def test_full_config_per_request(S, oracle, name):
+    m, traces, pts = W.make_config(name)
+    say("%s: %d points, oracle..." % (name, len(pts["peak_flops"])))
+    t0 = time.time()
+    o_out, o_req = oracle.run_points(m, traces, pts, per_request=True)
+    say("%s: oracle %.1fs, gpu..." % (name, time.time() - t0))
+    out, req = gpu_run(S, m, traces, pts, per_request=True, iter_cap=cap_from(o_out))
+    compare_points(out, o_out, name)
+    compare_requests(req, o_req, name)
+    assert (out["status"] == 0).all()
+
+
+def _fuzz_case(rng, n_pts):
+    traces, rows = [], []
+    for k in range(n_pts):
+        n = int(rng.integers(0, 41))
+        gaps = rng.choice([0, 0, 1, 3, 50, 10_000], size=n)
+        a = np.cumsum(gaps).astype(np.int64)
+        p = rng.integers(1, 30, size=n).astype(np.int32)
+        o = rng.integers(1, 12, size=n).astype(np.int32)
+        traces.append({"arrival_ns": a, "prompt_len": p, "output_len": o})
+        M = int(rng.choice([1, 2, 3, 5, 64, 65, 100, 130, 256]))
+        b = int(rng.choice([1, 2, 3, 16]))
+        K = int(rng.choice([0, 0, M, M + int(rng.integers(0, 9))]))
+        nb = int(rng.integers(0, 21)) if M < 64 else int(rng.integers(0, 400))
+        fast = rng.random() < 0.5
+        rows.append(dict(peak_flops=1e300 if fast else float(rng.choice([1e9, 3e9])),
+                         mem_bw=1e300 if fast else float(rng.choice([1e8, 7e8])),
+                         capacity_bytes=max(1, nb * b * 16), mem_util_permille=1000,
+                         block_size=b, max_batch=M, chunk_size=K, trace_id=k))
+    pts = {
+        "peak_flops": np.array([r["peak_flops"] for r in rows], np.float64),
+        "mem_bw": np.array([r["mem_bw"] for r in rows], np.float64),
+        "capacity_bytes": np.array([r["capacity_bytes"] for r in rows], np.int64),
+        **{f: np.array([r[f] for r in rows], np.int32)
+           for f in ("mem_util_permille", "block_size", "max_batch", "chunk_size", "trace_id")}}
+    return traces, pts
+
+
+def test_fuzz_tiny_points(S, oracle):
+    """Thousands of tiny random points: sequential oracle vs the kernel's
+    prefix-scan formulation of reservation, preemption and admission."""
+    model = {"n_layers": 1, "d_model": 8, "n_heads": 2, "n_kv_heads": 1, "ffn_dim": 16,
+             "ffn_gated": 1, "vocab": 10, "w_bytes": 2, "kv_bytes": 2,
+             "weights_in_capacity": 0}
+    rng = np.random.default_rng(2024)
+    total_pre = 0
+    for rnd in range(3):
+        traces, pts = _fuzz_case(rng, 1500)
+        o_out, o_req = oracle.run_points(model, traces, pts, per_request=True)
+        say("fuzz round %d: oracle preemptions %d" % (rnd, int(o_out["n_preempt"].sum())))
+        out, req = gpu_run(S, model, traces, pts, per_request=True, iter_cap=cap_from(o_out))
+        compare_points(out, o_out, "fuzz%d" % rnd)
+        compare_requests(req, o_req, "fuzz%d" % rnd)
+        total_pre += int(o_out["n_preempt"].sum())
+    assert total_pre > 100
+
+
+def test_full_c3_points(S, oracle):
+    m, traces, pts = W.make_config("c3")
+    t0 = time.time()
+    o_out, _ = oracle.run_points(m, traces, pts)
+    say("c3: oracle %.1fs" % (time.time() - t0))
+    out, _ = gpu_run(S, m, traces, pts, iter_cap=cap_from(o_out))
+    compare_points(out, o_out, "c3")
+    # per-request records on a sub-range of points
+    sub = dict(first_point=1000, n_points=64)
+    out2, req2 = gpu_run(S, m, traces, pts, per_request=True, iter_cap=cap_from(o_out), **sub)
+    sp = W.subset_points(pts, np.arange(1000, 1064))
+    o2, oreq2 = oracle.run_points(m, traces, sp, per_request=True)
+    compare_points(out2, o2, "c3 sub-range")
+    compare_requests(req2, oreq2, "c3 sub-range")
+
+
+def test_full_c4_points(S, oracle):
+    m, traces, pts = W.make_config("c4")
+    t0 = time.time()
+    o_out, _ = oracle.run_points(m, traces, pts)
+    say("c4: oracle %.1fs, %d preemptions" % (time.time() - t0, int(o_out["n_preempt"].sum())))
+    out, _ = gpu_run(S, m, traces, pts, iter_cap=cap_from(o_out))
+    compare_points(out, o_out, "c4")
+
+
+def c5_sample_index(n_points, n_sample=96, seed=5):
+    rng = np.random.default_rng(seed)
+    return np.sort(rng.choice(n_points, size=n_sample, replace=False))
+
+
+def test_c5_full_sweep_sampled(S, oracle):
+    """The full 65536-point sweep as the benchmark launches it; the oracle
+    recomputes a seeded sample of points one by one."""
+    m, traces, pts = W.make_config("c5")
+    idx = c5_sample_index(len(pts["peak_flops"]))
+    t0 = time.time()
+    o_out, _ = oracle.run_points(m, traces, W.subset_points(pts, idx))
+    say("c5: oracle on %d sampled points %.1fs" % (len(idx), time.time() - t0))
+    out, _ = gpu_run(S, m, traces, pts, iter_cap=cap_from(o_out) * 4)
+    compare_points(out[idx], o_out, "c5 sample")
+    assert (out["status"] == 0).all()
+    # properties that hold at any size
+    n = len(traces[0]["arrival_ns"])
+    assert (out["n_done"] + out["n_rejected"] == n).all()
+    tr_o = np.array([int(t["output_len"].sum()) for t in traces])
+    assert (out["decode_tokens"] == tr_o[pts["trace_id"]]).all()
+    tr_p = np.array([int(t["prompt_len"].sum()) for t in traces])
+    assert (out["prefill_tokens"] >= tr_p[pts["trace_id"]]).all()
+    assert (out["peak_used_blocks"] <= out["num_blocks"]).all()
+
+
+def test_determinism_and_point_order(S):
+    m, traces, pts = W.make_config("c3", n_requests=300)
+    n = len(pts["peak_flops"])
+    a, _ = gpu_run(S, m, traces, pts, iter_cap=1_000_000)
+    b, _ = gpu_run(S, m, traces, pts, iter_cap=1_000_000)
+    assert a.tobytes() == b.tobytes()
+    perm = np.random.default_rng(1).permutation(n)
+    c, _ = gpu_run(S, m, traces, W.subset_points(pts, perm), iter_cap=1_000_000)
+    assert c.tobytes() == a[perm].tobytes()
+
+
+def test_edge_cases(S, oracle):
+    m = W.MODELS["llama2-7b"]
+    empty = {"arrival_ns": np.zeros(0, np.int64), "prompt_len": np.zeros(0, np.int32),
+             "output_len": np.zeros(0, np.int32)}
+    burst = {"arrival_ns": np.zeros(300, np.int64),
+             "prompt_len": np.full(300, 64, np.int32), "output_len": np.full(300, 40, np.int32)}
+    huge = {"arrival_ns": np.array([0, 5, 9], np.int64),
+            "prompt_len": np.array([10, 200000, 10], np.int32),
+            "output_len": np.array([3, 3, 3], np.int32)}
+    traces = [empty, burst, huge]
+    rows = [
+        (312e12, 2e12, 80_000_000_000, 900, 16, 32, 0, 0),     # empty trace
+        (312e12, 2e12, 80_000_000_000, 900, 16, 256, 0, 1),    # 300 at once, M = 256
+        (312e12, 2e12, 80_000_000_000, 900, 16, 256, 256, 1),  # chunk = M
+        (312e12, 2e12, 14_000_000_000, 1000, 16, 256, 0, 1),   # tight memory: preemption
+        (312e12, 2e12, 10_000_000_000, 900, 16, 8, 0, 1),      # weights > capacity: NO_KV
+        (312e12, 2e12, 20_000_000_000, 1000, 16, 8, 0, 2),     # one request rejected
+        (312e12, 2e12, 80_000_000_000, 900, 1, 130, 512, 1),   # block 1, two chunks
+    ]
+    keys = ("peak_flops", "mem_bw", "capacity_bytes", "mem_util_permille", "block_size",
+            "max_batch", "chunk_size", "trace_id")
+    pts = {k: np.array([r[i] for r in rows]) for i, k in enumerate(keys)}
+    pts = {k: (v.astype(np.float64) if k in ("peak_flops", "mem_bw") else
+               v.astype(np.int64) if k == "capacity_bytes" else v.astype(np.int32))
+           for k, v in pts.items()}
+    o_out, o_req = oracle.run_points(m, traces, pts, per_request=True)
+    assert o_out["status"][4] == 1 and o_out["n_rejected"][5] == 1 and o_out["n_preempt"][3] > 0
+    out, req = gpu_run(S, m, traces, pts, per_request=True, iter_cap=cap_from(o_out))
+    compare_points(out, o_out, "edge")
+    compare_requests(req, o_req, "edge")
+    # iteration cap: stops early, identical partial state
+    o_cap, o_rq = oracle.run_points(m, traces, pts, per_request=True, iter_cap=37)
+    g_cap, g_rq = gpu_run(S, m, traces, pts, per_request=True, iter_cap=37)
+    compare_points(g_cap, o_cap, "iter cap")
+    compare_requests(g_rq, o_rq, "iter cap")
+    assert (g_cap["status"][[1, 2, 3, 6]] == 2).all()
