@@ -1,0 +1,184 @@
+#!/usr/bin/env python3
+"""Benchmark of the serving-simulation sweep on one MI355X.
+
+One step = one whole sweep (every design point simulated to completion:
+intake, block reservation / preemption, admission, roofline pricing and
+state advance for every iteration, then the percentile statistics) with
+traces and design points already resident in HBM.  Prints one JSON line.
+
+The default workload is the largest sweep: 65536 design points x 10000
+requests (7B GQA model, chunked prefill 256..2048, long-context prompt
+mixture, bursty arrivals), generated from fixed seeds.
+
+roofline: the simulation is bound by VALU instruction issue (integer
+scheduling and a short fp64 roofline per iteration; no dense contraction,
+negligible HBM traffic).  ``achieved`` is the algorithmic instruction count
+of the dominant simulation kernel divided by its HIP-event duration:
+  per simulated iteration  U = 80 wave64 VALU instructions
+      (the roofline: 14 int->fp64 conversions, 14 fp64 multiplies, 7 maxes,
+       6 adds, 1 multiply, 1 add, 1 ceil, 1 fp64->int = 45; five batch sums
+       as 6-step wave reductions = 30; arrival compare and clock update = 5)
+  per request-iteration    S = 16/64 (16 lane operations on a 64-lane wave:
+       phase / block-boundary tests, budget share, sum contributions,
+       token / context / gap / clock updates, finish test)
+with request-iterations counted as decode tokens + one prefill iteration
+per finished request (a lower bound).  Peak = 256 CUs x 4 SIMDs x 2.4 GHz /
+4 cycles per wave64 instruction = 614.4 G instructions/s.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "simulated requests/sec across sweep on 1 MI355X; % VALU-issue peak"
+VALU_ISSUE_PEAK = 256 * 4 * 2.4e9 / 4.0   # wave64 VALU instructions per second
+U_ITER = 80.0
+S_REQ_ITER = 16.0 / 64.0
+KERNEL_NAMES = ("sim_kernel<1>", "sim_kernel<2>", "sim_kernel<4>")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def algorithmic_instructions(out):
+    ri = out["decode_tokens"].astype(np.float64) + out["n_done"].astype(np.float64)
+    return U_ITER * out["n_iters"].astype(np.float64) + S_REQ_ITER * ri
+
+
+def kernel_class(max_batch):
+    mb = np.asarray(max_batch)
+    return np.where(mb <= 64, 0, np.where(mb <= 128, 1, 2))
+
+
+def cpu_baseline(model, traces, points, target_s, seed=0):
+    """The oracle on a bounded, seeded sample of the same design points."""
+    from oracle import tso
+    from paper_2503_08415_amd import workloads
+    n_points = len(points["peak_flops"])
+    cores = min(len(os.sched_getaffinity(0)), 16)
+    rng = np.random.default_rng(seed)
+    order = rng.permutation(n_points)
+    # calibrate on a first slice, then size the sample to about target_s
+    first = order[:max(cores, 8)]
+    t0 = time.perf_counter()
+    tso.run_points(model, traces, workloads.subset_points(points, first), n_threads=cores)
+    dt = time.perf_counter() - t0
+    per_point = dt / len(first)
+    n_more = int(max(0, min(n_points - len(first), target_s / max(per_point, 1e-6))))
+    sample = order[:len(first) + n_more]
+    sub = workloads.subset_points(points, sample)
+    t0 = time.perf_counter()
+    out, _ = tso.run_points(model, traces, sub, n_threads=cores)
+    dt = time.perf_counter() - t0
+    n_req = int(sum(len(traces[int(t)]["arrival_ns"]) for t in sub["trace_id"]))
+    return {"value": n_req / dt, "unit": "simulated requests/s", "cores": cores,
+            "kind": "oracle",
+            "sample": "%d of %d design points (seeded random), %d simulated requests, %.1f s wall"
+                      % (len(sample), n_points, n_req, dt)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--config", default="c5", choices=["c1", "c2", "c3", "c4", "c5"])
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="wall time budget of the oracle baseline sample (0 = skip)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU: the sweep's design points are independent and this "
+              "build measures one GPU's share; --gpus %d is not supported" % args.gpus,
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2503_08415_amd import sweep, workloads
+
+    torch.cuda.set_device(0)
+    t0 = time.perf_counter()
+    model, traces, points = workloads.make_config(args.config)
+    n_points = len(points["peak_flops"])
+    n_req = int(sum(len(traces[int(t)]["arrival_ns"]) for t in points["trace_id"]))
+    log("workload %s: %d points, %d simulated requests (generated in %.1fs)"
+        % (args.config, n_points, n_req, time.perf_counter() - t0))
+    sw = sweep.Sweep(model, traces, points)
+    stream = torch.cuda.current_stream()
+
+    for i in range(args.warmup):
+        t0 = time.perf_counter()
+        sw.run(stream)
+        torch.cuda.synchronize()
+        log("warmup %d: %.3fs" % (i, time.perf_counter() - t0))
+
+    step_s, sim_ms, stats_ms, kms = [], [], [], []
+    torch.cuda.synchronize()
+    t_all = time.perf_counter()
+    for i in range(args.steps):
+        t0 = time.perf_counter()
+        sw.run(stream)
+        torch.cuda.synchronize()
+        step_s.append(time.perf_counter() - t0)
+        a, b = sw.timing()
+        sim_ms.append(a)
+        stats_ms.append(b)
+        kms.append([k[0] for k in sw.kernel_timing()])
+        log("step %d: %.3fs (simulation %.1f ms, statistics %.1f ms, kernels %s)"
+            % (i, step_s[-1], a, b, ["%.1f" % x for x in kms[-1]]))
+    torch.cuda.synchronize()
+    total_s = time.perf_counter() - t_all
+    t0 = time.perf_counter()
+    out, _ = sw.results()
+    results_s = time.perf_counter() - t0
+    sw.close()
+
+    ms_per_step = 1e3 * total_s / args.steps
+    value = n_req / (total_s / args.steps)
+    status = np.bincount(out["status"], minlength=4).tolist()
+
+    # roofline of the dominant simulation kernel (longest mean duration)
+    kmean = np.mean(np.array(kms), axis=0)
+    cls = kernel_class(points["max_batch"])
+    w = algorithmic_instructions(out)
+    k = int(np.argmax(kmean))
+    w_k = float(w[cls == k].sum())
+    achieved = w_k / (kmean[k] * 1e-3)
+    roofline = {"bound": "alu", "achieved": achieved / 1e9, "peak": VALU_ISSUE_PEAK / 1e9,
+                "unit": "G wave64 VALU instr/s", "frac": achieved / VALU_ISSUE_PEAK,
+                "traffic": None, "kernel": KERNEL_NAMES[k],
+                "algorithmic_instr": w_k, "kernel_ms": float(kmean[k])}
+
+    line = {
+        "metric": METRIC, "value": value, "unit": "simulated requests/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "int32/int64 + f64", "data": "synthetic",
+        "config": {"workload": "%s: %s" % (args.config, workloads.CONFIGS[args.config][2]),
+                   "design_points": n_points, "simulated_requests": n_req,
+                   "model": "none (simulated transformer shape)",
+                   "parallelism": "one wave64 workgroup per design point"},
+        "roofline": roofline,
+        "kernels_ms": {KERNEL_NAMES[i]: float(kmean[i]) for i in range(3) if kmean[i] > 0},
+        "simulation_phase_ms": float(np.mean(sim_ms)), "statistics_ms": float(np.mean(stats_ms)),
+        "results_copy_ms": 1e3 * results_s,
+        "simulated_iterations": int(out["n_iters"].sum()),
+        "point_status_counts": status,
+    }
+    if args.cpu_seconds > 0:
+        log("cpu baseline: oracle on a sample (~%.0fs)..." % args.cpu_seconds)
+        line["cpu_baseline"] = cpu_baseline(model, traces, points, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -169,6 +169,8 @@ struct ts_sweep {
   hipStream_t side[kClasses] = {nullptr, nullptr, nullptr};
   hipEvent_t ev_fork = nullptr, ev_join[kClasses] = {nullptr, nullptr, nullptr};
   hipEvent_t ev_t0 = nullptr, ev_t1 = nullptr, ev_t2 = nullptr;
+  hipEvent_t ev_k0[kClasses] = {nullptr, nullptr, nullptr};
+  hipEvent_t ev_k1[kClasses] = {nullptr, nullptr, nullptr};
   hipStream_t last_stream = nullptr;
   bool ran = false;
 };
@@ -189,6 +191,8 @@ void release(ts_sweep* h) {
   for (int c = 0; c < kClasses; ++c) {
     if (h->side[c]) (void)hipStreamDestroy(h->side[c]);
     if (h->ev_join[c]) (void)hipEventDestroy(h->ev_join[c]);
+    if (h->ev_k0[c]) (void)hipEventDestroy(h->ev_k0[c]);
+    if (h->ev_k1[c]) (void)hipEventDestroy(h->ev_k1[c]);
   }
   if (h->ev_fork) (void)hipEventDestroy(h->ev_fork);
   if (h->ev_t0) (void)hipEventDestroy(h->ev_t0);
@@ -408,6 +412,8 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
   for (int c = 0; c < kClasses && e == hipSuccess; ++c) {
     e = hipStreamCreateWithFlags(&h->side[c], hipStreamNonBlocking);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&h->ev_join[c], hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreate(&h->ev_k0[c]);
+    if (e == hipSuccess) e = hipEventCreate(&h->ev_k1[c]);
   }
   if (e == hipSuccess) e = hipEventCreateWithFlags(&h->ev_fork, hipEventDisableTiming);
   if (e == hipSuccess) e = hipEventCreate(&h->ev_t0);
@@ -460,11 +466,15 @@ int ts_sweep_run(ts_sweep* h, void* hip_stream) {
       e = hipStreamWaitEvent(ks, h->ev_fork, 0);
       if (e != hipSuccess) return device_error(e, "stream wait");
     }
+    e = hipEventRecord(h->ev_k0[c], ks);
+    if (e != hipSuccess) return device_error(e, "event record");
     if (kClassChunks[c] == 1) sim_kernel<1><<<h->grid[c], 64, 0, ks>>>(a);
     else if (kClassChunks[c] == 2) sim_kernel<2><<<h->grid[c], 64, 0, ks>>>(a);
     else sim_kernel<4><<<h->grid[c], 64, 0, ks>>>(a);
     e = hipGetLastError();
     if (e != hipSuccess) return device_error(e, "sim kernel launch");
+    e = hipEventRecord(h->ev_k1[c], ks);
+    if (e != hipSuccess) return device_error(e, "event record");
     if (used > 1) {
       e = hipEventRecord(h->ev_join[c], ks);
       if (e == hipSuccess) e = hipStreamWaitEvent(s, h->ev_join[c], 0);
@@ -519,6 +529,19 @@ int ts_sweep_timing(ts_sweep* h, float* sim_ms, float* stats_ms) {
   hipError_t e = hipEventSynchronize(h->ev_t2);
   if (e == hipSuccess) e = hipEventElapsedTime(sim_ms, h->ev_t0, h->ev_t1);
   if (e == hipSuccess) e = hipEventElapsedTime(stats_ms, h->ev_t1, h->ev_t2);
+  if (e != hipSuccess) return device_error(e, "event timing");
+  return TS_OK;
+}
+
+int ts_sweep_kernel_timing(ts_sweep* h, float* ms, int32_t* n_points) {
+  if (!h || !ms || !n_points) return TS_ERR_ARG;
+  if (!h->ran) return TS_ERR_STATE;
+  hipError_t e = hipEventSynchronize(h->ev_t2);
+  for (int c = 0; c < kClasses && e == hipSuccess; ++c) {
+    ms[c] = 0.0f;
+    n_points[c] = h->class_n[c];
+    if (h->class_n[c] > 0) e = hipEventElapsedTime(&ms[c], h->ev_k0[c], h->ev_k1[c]);
+  }
   if (e != hipSuccess) return device_error(e, "event timing");
   return TS_OK;
 }

@@ -63,7 +63,8 @@ POINT_DTYPE = np.dtype([
 
 # every entry point declared in include/ts_sweep.h
 EXPORTS = ("ts_sweep_create", "ts_sweep_run", "ts_sweep_results", "ts_sweep_shape",
-           "ts_sweep_timing", "ts_sweep_destroy", "ts_status_str")
+           "ts_sweep_timing", "ts_sweep_kernel_timing", "ts_sweep_destroy", "ts_status_str")
+N_SIM_KERNELS = 3  # register-chunk classes: max_batch <= 64, <= 128, <= 256
 
 _lib = None
 
@@ -95,6 +96,9 @@ def lib():
         L.ts_sweep_shape.restype = C.c_int
         L.ts_sweep_timing.argtypes = [C.c_void_p, C.POINTER(C.c_float), C.POINTER(C.c_float)]
         L.ts_sweep_timing.restype = C.c_int
+        L.ts_sweep_kernel_timing.argtypes = [C.c_void_p, C.POINTER(C.c_float),
+                                             C.POINTER(C.c_int32)]
+        L.ts_sweep_kernel_timing.restype = C.c_int
         L.ts_sweep_destroy.argtypes = [C.c_void_p]
         L.ts_sweep_destroy.restype = None
         L.ts_status_str.argtypes = [C.c_int]
@@ -176,6 +180,13 @@ class Sweep:
         a, b = C.c_float(), C.c_float()
         _check(lib().ts_sweep_timing(self._h, C.byref(a), C.byref(b)), "ts_sweep_timing")
         return a.value, b.value
+
+    def kernel_timing(self):
+        """Per simulation kernel: (ms, points) of the last run, from HIP events."""
+        ms = (C.c_float * N_SIM_KERNELS)()
+        n = (C.c_int32 * N_SIM_KERNELS)()
+        _check(lib().ts_sweep_kernel_timing(self._h, ms, n), "ts_sweep_kernel_timing")
+        return [(ms[k], n[k]) for k in range(N_SIM_KERNELS)]
 
     def close(self):
         if self._h:
