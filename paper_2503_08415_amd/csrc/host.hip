@@ -106,6 +106,26 @@ CostCoef make_coef(const Shape& s) {
   return c;
 }
 
+// Per-lane operator table of the device roofline (lane j prices operator j;
+// X/Y/Z are selected on the device: T for the projections and FFN, AP/CP/TP
+// for prefill attention, CD/CD/nD for decode attention, R/R for the LM head).
+LaneCoef lane_coef(const CostCoef& c) {
+  LaneCoef l;
+  for (int j = 0; j < 8; ++j) l.f[j] = l.b0[j] = l.b1[j] = l.b2[j] = 0.0;
+  const int64_t tab[7][4] = {
+      {c.f_qkv, c.b_qkv0, c.b_qkv, 0},          {c.f_attp, 0, c.b_attp_c, c.b_attp_t},
+      {c.f_attd, 0, c.b_attd_c, c.b_attd_n},    {c.f_out, c.b_out0, c.b_out, 0},
+      {c.f_up, c.b_up0, c.b_up, 0},             {c.f_dn, c.b_dn0, c.b_dn, 0},
+      {c.f_lm, c.b_lm0, c.b_lm, 0}};
+  for (int j = 0; j < 7; ++j) {
+    l.f[j] = (double)tab[j][0];   // all below 2^53: exact
+    l.b0[j] = (double)tab[j][1];
+    l.b1[j] = (double)tab[j][2];
+    l.b2[j] = (double)tab[j][3];
+  }
+  return l;
+}
+
 // Upper bounds of every FLOP / byte count and of the iteration time for a
 // point whose requests hold at most max_po tokens.
 bool exact_and_bounded(const CostCoef& c, int64_t max_po, int M, int K, double iF, double iB) {
@@ -154,6 +174,7 @@ struct ts_sweep {
   uint32_t flags = 0;
   int64_t iter_cap = 0, slo_ttft = 0, slo_tpot = 0, time_limit_ms = 0;
   CostCoef coef{};
+  LaneCoef lc{};
   TraceRec* d_recs = nullptr;
   DevPoint* d_points = nullptr;
   int32_t* d_order = nullptr;       // all classes, concatenated
@@ -353,6 +374,7 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
   h->slo_tpot = slo_tpot;
   h->time_limit_ms = time_limit_ms;
   h->coef = coef;
+  h->lc = lane_coef(coef);
 
   // ---------------------------------------------------------- device
   hipError_t e = hipGetDevice(&h->device);
@@ -459,7 +481,8 @@ int ts_sweep_run(ts_sweep* h, void* hip_stream) {
     a.slo_ttft_ns = h->slo_ttft;
     a.slo_tpot_ns = h->slo_tpot;
     a.time_limit_ticks = (uint64_t)h->time_limit_ms * 100000ull;  // 100 MHz clock
-    a.coef = h->coef;
+    a.n_layers = h->coef.n_layers;
+    a.lc = h->lc;
     hipStream_t ks = s;
     if (used > 1) {
       ks = h->side[c];

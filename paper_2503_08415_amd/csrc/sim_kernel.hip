@@ -123,60 +123,123 @@ __device__ __forceinline__ uint64_t record_hash(int64_t idx, int64_t admit, int6
 }
 
 // ------------------------------------------------------------ roofline
-// Per operator: max(FLOPs / peak, bytes / bandwidth) in ns; both counts are
-// exact integers below 2^53, so the int64 -> double conversion is exact.
-__device__ __forceinline__ double roof(int64_t flops, int64_t bytes, double iF, double iB) {
-  const double tf = (double)flops * iF;
-  const double tb = (double)bytes * iB;
-  return tf > tb ? tf : tb;
+// Lane j < 7 prices operator j of the iteration (QKV projection, prefill
+// attention, decode attention, output projection, FFN up(+gate), FFN down,
+// LM head): F = f * X, B = (b0 + b1 * Y) + b2 * Z with X, Y, Z batch sums.
+// Every F and B is an integer below 2^53 and so is every partial product
+// and sum, so fp64 evaluates them exactly: the same doubles as converting
+// exact int64 counts.  Then t = max(F / peak, B / BW) with the reciprocals
+// given in ns per FLOP / byte.  The layer sum keeps the fixed left-to-right
+// order ((((t0 + t1) + t2) + t3) + t4) + t5 through a DPP chain in which
+// lane k adds its term to lane k-1's partial sum.
+__device__ __forceinline__ double dpp_shr1_f64(double v) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, v);
+  const uint32_t lo = (uint32_t)dpp0<0x111, 0xf>((int)(uint32_t)u);
+  const uint32_t hi = (uint32_t)dpp0<0x111, 0xf>((int)(uint32_t)(u >> 32));
+  return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+__device__ __forceinline__ double rdl_f64(double v, int l) {
+  return __builtin_bit_cast(double, (uint64_t)rdl64((int64_t)__builtin_bit_cast(uint64_t, v), l));
 }
 
-__device__ __forceinline__ int64_t iteration_ns(const CostCoef& C, double iF, double iB,
-                                                int64_t T, int64_t TP, int64_t AP, int64_t CP,
-                                                int64_t nD, int64_t CD, int64_t R) {
-  const double t1 = roof(C.f_qkv * T, C.b_qkv0 + C.b_qkv * T, iF, iB);
-  const double t2 = roof(C.f_attp * AP, C.b_attp_c * CP + C.b_attp_t * TP, iF, iB);
-  const double t3 = roof(C.f_attd * CD, C.b_attd_c * CD + C.b_attd_n * nD, iF, iB);
-  const double t4 = roof(C.f_out * T, C.b_out0 + C.b_out * T, iF, iB);
-  const double t5 = roof(C.f_up * T, C.b_up0 + C.b_up * T, iF, iB);
-  const double t6 = roof(C.f_dn * T, C.b_dn0 + C.b_dn * T, iF, iB);
-  const double t7 = R > 0 ? roof(C.f_lm * R, C.b_lm0 + C.b_lm * R, iF, iB) : 0.0;
-  double layer = t1;
-  layer = layer + t2;
-  layer = layer + t3;
-  layer = layer + t4;
-  layer = layer + t5;
-  layer = layer + t6;
-  double total = C.n_layers * layer;
-  total = total + t7;
-  const int64_t ns = (int64_t)ceil(total);
-  return ns < 1 ? 1 : ns;
+struct LaneRoof {
+  double f, b0, b1, b2;  // this lane's operator coefficients (zero above lane 6)
+  bool is_attp, is_attd, is_lm;
+};
+
+// Returns max(1, ceil(L * layer_sum + lm_head)) and the same value as a double.
+__device__ __forceinline__ int64_t iteration_ns(const LaneRoof& c, double n_layers, double iF,
+                                                double iB, int T, int TP, int64_t AP, int CP,
+                                                int nD, int CD, int R, double* iter_d) {
+  const double dT = (double)T;
+  double X = dT, Y = dT, Z = 0.0;
+  X = c.is_attp ? (double)AP : X;
+  Y = c.is_attp ? (double)CP : Y;
+  Z = c.is_attp ? (double)TP : Z;
+  X = c.is_attd ? (double)CD : X;
+  Y = c.is_attd ? (double)CD : Y;
+  Z = c.is_attd ? (double)nD : Z;
+  X = c.is_lm ? (double)R : X;
+  Y = c.is_lm ? (double)R : Y;
+  const double b0 = (c.is_lm && R == 0) ? 0.0 : c.b0;  // no LM head without an emitter
+  const double F = c.f * X;
+  const double Bv = (b0 + c.b1 * Y) + c.b2 * Z;
+  const double tf = F * iF;
+  const double tb = Bv * iB;
+  const double t = tf > tb ? tf : tb;
+  double s = t;
+  s = dpp_shr1_f64(s) + t;  // lane 1: t0 + t1
+  s = dpp_shr1_f64(s) + t;  // lane 2: (t0 + t1) + t2
+  s = dpp_shr1_f64(s) + t;
+  s = dpp_shr1_f64(s) + t;
+  s = dpp_shr1_f64(s) + t;  // lane 5: the layer sum
+  const double layer = rdl_f64(s, 5);
+  const double lm = rdl_f64(t, 6);
+  double total = n_layers * layer;
+  total = total + lm;
+  double it = ceil(total);
+  it = it < 1.0 ? 1.0 : it;
+  *iter_d = it;
+  return (int64_t)it;
 }
 
 // Admission staging: one entry per admitted candidate of a window.
 struct StageSlot {
-  int32_t id, tgt, rem, npre, q, alloc, room, pad;
+  int32_t id, tgt, rem, npre, q, alloc, room, first_done;
   int64_t admit, first, last, gap;
 };
 
-// Stable compaction of one per-slot field through LDS scratch.
+// Per-workgroup LDS: the cold fields of the slots (used only at admission,
+// preemption and finish) and a staging area shared by admission and the
+// stable compaction.
+template <int NCH>
+struct SlotLds {
+  int32_t id[64 * NCH];
+  int32_t npre[64 * NCH];
+  int64_t admit[64 * NCH];
+  int64_t first[64 * NCH];
+  union {
+    StageSlot stage[64];
+    int64_t scratch[64 * NCH];
+  } u;
+};
+
+// Stable compaction of one register field through LDS scratch.
 template <int NCH, typename Tv>
-__device__ __forceinline__ void compact_field(Tv (&f)[NCH], const bool (&keep)[NCH],
-                                              const int (&pos)[NCH], Tv* scratch, int lane) {
+__device__ __forceinline__ void compact_reg(Tv (&f)[NCH], const bool (&keep)[NCH],
+                                            const int (&pos)[NCH], Tv* scratch, int lane,
+                                            int nch) {
 #pragma unroll
   for (int j = 0; j < NCH; ++j)
-    if (keep[j]) scratch[pos[j]] = f[j];
+    if (j < nch && keep[j]) scratch[pos[j]] = f[j];
   __syncthreads();
 #pragma unroll
-  for (int j = 0; j < NCH; ++j) f[j] = scratch[j * 64 + lane];
+  for (int j = 0; j < NCH; ++j)
+    if (j < nch) f[j] = scratch[j * 64 + lane];
   __syncthreads();
+}
+
+// Stable compaction of one LDS field in place (positions only move down,
+// every chunk is read before it is written).
+template <int NCH, typename Tv>
+__device__ __forceinline__ void compact_lds(Tv* f, const bool (&keep)[NCH],
+                                            const int (&pos)[NCH], int lane, int nch) {
+#pragma unroll
+  for (int j = 0; j < NCH; ++j) {
+    if (j < nch) {
+      const Tv v = f[j * 64 + lane];
+      __syncthreads();
+      if (keep[j]) f[pos[j]] = v;
+      __syncthreads();
+    }
+  }
 }
 
 // ------------------------------------------------------------ one point
 template <int NCH>
 __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
-                                               StageSlot* stage, int64_t* scratch,
-                                               QEntry* Q, const int lane) {
+                                               SlotLds<NCH>& L, QEntry* Q, const int lane,
+                                               const LaneRoof& roofc) {
   const DevPoint P = A.points[pidx];
   const TraceRec* __restrict__ rec = A.recs + P.trace_off;
   const int N = P.n, NB = P.num_blocks, B = P.block, M = P.max_batch, K = P.chunk;
@@ -233,16 +296,13 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
     w_arr = r.arrival_ns; w_p = r.prompt; w_o = r.output;
   }
 
-  int s_ctx[NCH], s_tgt[NCH], s_rem[NCH], s_room[NCH], s_alloc[NCH], s_id[NCH], s_npre[NCH];
-  int64_t s_admit[NCH], s_first[NCH], s_last[NCH], s_gap[NCH];
-  int q[NCH];
-  bool act[NCH], dec[NCH];
+  // hot slot state in registers: slot s = chunk s / 64, lane s % 64
+  int s_ctx[NCH], s_tgt[NCH], s_rem[NCH], s_room[NCH], s_alloc[NCH], s_fd[NCH], q[NCH];
+  int64_t s_last[NCH], s_gap[NCH];
 #pragma unroll
   for (int j = 0; j < NCH; ++j) {
-    s_ctx[j] = s_tgt[j] = s_rem[j] = s_room[j] = s_alloc[j] = s_id[j] = s_npre[j] = 0;
-    s_admit[j] = s_first[j] = s_last[j] = s_gap[j] = 0;
-    q[j] = 0;
-    act[j] = dec[j] = false;
+    s_ctx[j] = s_tgt[j] = s_rem[j] = s_room[j] = s_alloc[j] = s_fd[j] = q[j] = 0;
+    s_last[j] = s_gap[j] = 0;
   }
 
   const uint64_t clock0 = A.time_limit_ticks ? __builtin_amdgcn_s_memrealtime() : 0;
@@ -295,19 +355,27 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
     }
 
     // ---- 3. reserve a block for decodes crossing a block boundary
+    int nch = (nrun + 63) >> 6;  // register chunks holding running slots
+    bool act[NCH], dec[NCH];
     int nneed = 0;
 #pragma unroll
     for (int j = 0; j < NCH; ++j) {
-      act[j] = (j * 64 + lane) < nrun;
-      dec[j] = act[j] && s_ctx[j] >= s_tgt[j];
-      nneed += popc(ballot(dec[j] && s_room[j] == 0));
+      act[j] = false;
+      dec[j] = false;
+      if (j < nch) {
+        act[j] = (j * 64 + lane) < nrun;
+        dec[j] = act[j] && s_ctx[j] >= s_tgt[j];
+        nneed += popc(ballot(dec[j] && s_room[j] == 0));
+      }
     }
     bool preempted = false;
     if (nneed <= freeb) {
       freeb -= nneed;
+      if (nneed > 0) {
 #pragma unroll
-      for (int j = 0; j < NCH; ++j)
-        if (dec[j] && s_room[j] == 0) { s_alloc[j] += 1; s_room[j] += B; }
+        for (int j = 0; j < NCH; ++j)
+          if (j < nch && dec[j] && s_room[j] == 0) { s_alloc[j] += 1; s_room[j] += B; }
+      }
     } else {
       // Recompute preemption from the tail: keep the longest prefix of slots
       // whose held + needed blocks fit in the whole budget.
@@ -315,35 +383,42 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       bool keep[NCH];
 #pragma unroll
       for (int j = 0; j < NCH; ++j) {
-        const int need = (dec[j] && s_room[j] == 0) ? 1 : 0;
-        const int v = act[j] ? s_alloc[j] + need : 0;
-        const int S = scan_i32(v) + carry;
-        keep[j] = act[j] && S <= NB;
-        k += popc(ballot(keep[j]));
-        kept += wsum(keep[j] ? v : 0);
-        carry = rdl(S, 63);
+        keep[j] = false;
+        if (j < nch) {
+          const int need = (dec[j] && s_room[j] == 0) ? 1 : 0;
+          const int v = act[j] ? s_alloc[j] + need : 0;
+          const int S = scan_i32(v) + carry;
+          keep[j] = act[j] && S <= NB;
+          k += popc(ballot(keep[j]));
+          kept += wsum(keep[j] ? v : 0);
+          carry = rdl(S, 63);
+        }
       }
       freeb = NB - kept;
       const int nv = nrun - k;
       qhead = (qhead - nv) & (kQueueCap - 1);
 #pragma unroll
       for (int j = 0; j < NCH; ++j) {
-        const int s = j * 64 + lane;
-        if (keep[j]) {
-          if (dec[j] && s_room[j] == 0) { s_alloc[j] += 1; s_room[j] += B; }
-        } else if (act[j]) {
-          // victims keep admission order at the front of the waiting queue:
-          // they are older than every request still waiting
-          QEntry e;
-          e.id = s_id[j];
-          e.target = s_ctx[j] > s_tgt[j] ? s_ctx[j] : s_tgt[j];  // prompt + tokens decoded
-          e.rem = s_rem[j];
-          e.n_pre = s_npre[j] + 1;
-          e.admit = s_admit[j];
-          e.first = s_first[j];
-          e.last = s_last[j];
-          e.gap = s_gap[j];
-          Q[(qhead + s - k) & (kQueueCap - 1)] = e;
+        if (j < nch) {
+          const int s = j * 64 + lane;
+          if (keep[j]) {
+            if (dec[j] && s_room[j] == 0) { s_alloc[j] += 1; s_room[j] += B; }
+          } else if (act[j]) {
+            // victims keep admission order at the front of the waiting queue:
+            // they are older than every request still waiting
+            QEntry e;
+            e.id = L.id[s];
+            e.target = s_ctx[j] > s_tgt[j] ? s_ctx[j] : s_tgt[j];  // prompt + tokens decoded
+            e.rem = s_rem[j];
+            e.n_pre = L.npre[s] + 1;
+            e.first_done = s_fd[j];
+            e.pad0 = e.pad1 = e.pad2 = 0;
+            e.admit = L.admit[s];
+            e.first = L.first[s];
+            e.last = s_last[j];
+            e.gap = s_gap[j];
+            Q[(qhead + s - k) & (kQueueCap - 1)] = e;
+          }
         }
       }
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
@@ -352,38 +427,62 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       nrun = k;
       preempted = true;
       head_need = -1;
+      nch = (nrun + 63) >> 6;
+#pragma unroll
+      for (int j = 0; j < NCH; ++j) {
+        act[j] = j < nch && (j * 64 + lane) < nrun;
+        dec[j] = act[j] && s_ctx[j] >= s_tgt[j];
+      }
     }
 
     // ---- 4. token budget: decodes one token, running prefills share the rest
-    int R = 0;
-    {
-      int ndec = 0;
+    int nD = 0, npf = 0;
+    uint64_t pfm[NCH];
 #pragma unroll
-      for (int j = 0; j < NCH; ++j) {
-        act[j] = (j * 64 + lane) < nrun;
-        dec[j] = act[j] && s_ctx[j] >= s_tgt[j];
-        ndec += popc(ballot(dec[j]));
+    for (int j = 0; j < NCH; ++j) {
+      pfm[j] = 0;
+      if (j < nch) {
+        nD += popc(ballot(dec[j]));
+        pfm[j] = ballot(act[j] && !dec[j]);
+        npf += popc(pfm[j]);
       }
-      if (!unlimited) {
-        R = K - ndec;
+    }
+    int R = 0;
+    if (!unlimited) {
+      R = K - nD;
+      if (npf == 1) {
+        // one running prefill takes min(what it still needs, the budget)
+#pragma unroll
+        for (int j = 0; j < NCH; ++j) {
+          if (pfm[j] != 0) {
+            const int l = (int)__builtin_ctzll(pfm[j]);
+            const int left = rdl(s_tgt[j] - s_ctx[j], l);
+            const int qv = left < R ? left : R;
+            q[j] = qv;
+            R -= qv;
+          }
+        }
+      } else if (npf > 1) {
         int carry = 0;
 #pragma unroll
         for (int j = 0; j < NCH; ++j) {
-          const bool pf = act[j] && !dec[j];
-          const int left = pf ? s_tgt[j] - s_ctx[j] : 0;
-          const int S = scan_i32(left);
-          int avail = R - (S - left + carry);
-          avail = avail < 0 ? 0 : avail;
-          q[j] = dec[j] ? 1 : (pf ? (left < avail ? left : avail) : 0);
-          carry += rdl(S, 63);
+          if (j < nch) {
+            const bool pf = act[j] && !dec[j];
+            const int left = pf ? s_tgt[j] - s_ctx[j] : 0;
+            const int S = scan_i32(left);
+            int avail = R - (S - left + carry);
+            avail = avail < 0 ? 0 : avail;
+            q[j] = left < avail ? left : avail;
+            carry += rdl(S, 63);
+          }
         }
         R = R - carry;
         if (R < 0) R = 0;
-      } else {
-#pragma unroll
-        for (int j = 0; j < NCH; ++j)
-          q[j] = dec[j] ? 1 : (act[j] ? s_tgt[j] - s_ctx[j] : 0);
       }
+    } else {
+#pragma unroll
+      for (int j = 0; j < NCH; ++j)
+        if (j < nch) q[j] = s_tgt[j] - s_ctx[j];
     }
 
     // ---- 5. FCFS admission over 64-candidate windows (none after preemption)
@@ -393,7 +492,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
         if (head_need >= 0 && head_need > freeb) break;
         const bool fromq = npre > 0;
         bool valid;
-        int c_id, c_tgt, c_rem, c_npre;
+        int c_id, c_tgt, c_rem, c_npre, c_fd;
         int64_t c_admit, c_first, c_last, c_gap;
         if (fromq) {
           valid = lane < npre;
@@ -401,15 +500,16 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
           if (valid) {
             const QEntry e = Q[(qhead + lane) & (kQueueCap - 1)];
             c_id = e.id; c_tgt = e.target; c_rem = e.rem; c_npre = e.n_pre;
+            c_fd = e.first_done;
             c_admit = e.admit; c_first = e.first; c_last = e.last; c_gap = e.gap;
           } else {
-            c_id = 0; c_tgt = 1; c_rem = 1; c_npre = 0;
+            c_id = 0; c_tgt = 1; c_rem = 1; c_npre = 0; c_fd = 0;
             c_admit = -1; c_first = -1; c_last = -1; c_gap = 0;
           }
         } else {
           const int idx = next_new + lane;
           valid = idx < next;
-          c_id = idx; c_npre = 0; c_admit = -1; c_first = -1; c_last = -1; c_gap = 0;
+          c_id = idx; c_npre = 0; c_fd = 0; c_admit = -1; c_first = -1; c_last = -1; c_gap = 0;
           c_tgt = 1; c_rem = 1;
           if (valid) {
             const TraceRec r = rec[idx];
@@ -449,21 +549,21 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
         if (adm) {
           StageSlot st;
           st.id = c_id; st.tgt = c_tgt; st.rem = c_rem; st.npre = c_npre; st.q = qv;
-          st.alloc = need; st.room = need * B - c_tgt; st.pad = 0;
+          st.alloc = need; st.room = need * B - c_tgt; st.first_done = c_fd;
           st.admit = c_admit < 0 ? t : c_admit;
           st.first = c_first; st.last = c_last; st.gap = c_gap;
-          stage[rank] = st;
+          L.u.stage[rank] = st;
         }
         __syncthreads();
 #pragma unroll
         for (int j = 0; j < NCH; ++j) {
           const int s = j * 64 + lane;
           if (s >= nrun && s < nrun + a) {
-            const StageSlot st = stage[s - nrun];
-            s_id[j] = st.id; s_ctx[j] = 0; s_tgt[j] = st.tgt; s_rem[j] = st.rem;
-            s_npre[j] = st.npre; q[j] = st.q; s_alloc[j] = st.alloc; s_room[j] = st.room;
-            s_admit[j] = st.admit; s_first[j] = st.first; s_last[j] = st.last;
-            s_gap[j] = st.gap;
+            const StageSlot st = L.u.stage[s - nrun];
+            s_ctx[j] = 0; s_tgt[j] = st.tgt; s_rem[j] = st.rem; q[j] = st.q;
+            s_alloc[j] = st.alloc; s_room[j] = st.room; s_fd[j] = st.first_done;
+            s_last[j] = st.last; s_gap[j] = st.gap;
+            L.id[s] = st.id; L.npre[s] = st.npre; L.admit[s] = st.admit; L.first[s] = st.first;
           }
         }
         __syncthreads();
@@ -482,47 +582,74 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
           break;
         }
       }
+      nch = (nrun + 63) >> 6;
+#pragma unroll
+      for (int j = 0; j < NCH; ++j) act[j] = j < nch && (j * 64 + lane) < nrun;
     }
 
-    // ---- 6. batch sums (wave reductions) and the roofline iteration time
-    int l_nd = 0, l_cd = 0, l_r = 0, l_tp = 0, l_cp = 0;
-    int64_t l_ap = 0;
-    bool l_pf = false;
+    // ---- 6. batch sums and the roofline iteration time
+    // decodes: count by ballot, keys by one wave reduction
+    int l_cd = 0;
+    uint64_t pqm[NCH];
+    int npq = 0;
 #pragma unroll
     for (int j = 0; j < NCH; ++j) {
-      act[j] = (j * 64 + lane) < nrun;
-      dec[j] = act[j] && s_ctx[j] >= s_tgt[j];
-      const int c0 = s_ctx[j];
-      if (dec[j]) {
-        l_nd += 1;
-        l_cd += c0 + 1;
-        l_r += 1;
-      } else if (act[j] && q[j] > 0) {
-        const int qq = q[j];
-        l_tp += qq;
-        l_ap += (int64_t)qq * c0 + ((int64_t)qq * (qq + 1)) / 2;
-        l_cp += c0 + qq;
-        if (c0 + qq == s_tgt[j] && s_first[j] < 0) l_r += 1;  // emits its first token
-        l_pf = true;
+      pqm[j] = 0;
+      if (j < nch) {
+        if (dec[j]) l_cd += s_ctx[j] + 1;
+        pqm[j] = ballot(act[j] && !dec[j] && q[j] > 0);
+        npq += popc(pqm[j]);
       }
     }
-    const int nD = wsum(l_nd);
-    const int CD = wsum(l_cd);
-    const int Rl = wsum(l_r);
-    int TP = 0, CP = 0;
+    const int CD = nD > 0 ? wsum(l_cd) : 0;
+    int TP = 0, CP = 0, Rc = 0;
     int64_t AP = 0;
-    if (ballot(l_pf) != 0) {
+    if (npq > 0 && npq <= 2) {
+      // one or two prefills: read them out lane by lane
+#pragma unroll
+      for (int j = 0; j < NCH; ++j) {
+        uint64_t m = pqm[j];
+        while (m != 0) {
+          const int l = (int)__builtin_ctzll(m);
+          m &= m - 1;
+          const int qq = rdl(q[j], l);
+          const int c0 = rdl(s_ctx[j], l);
+          const int tg = rdl(s_tgt[j], l);
+          const int fd = rdl(s_fd[j], l);
+          TP += qq;
+          CP += c0 + qq;
+          AP += (int64_t)qq * c0 + ((int64_t)qq * (qq + 1)) / 2;
+          if (c0 + qq == tg && fd == 0) Rc += 1;  // emits its first token
+        }
+      }
+    } else if (npq > 2) {
+      int l_tp = 0, l_cp = 0;
+      int64_t l_ap = 0;
+#pragma unroll
+      for (int j = 0; j < NCH; ++j) {
+        if (j < nch) {
+          const bool pf = (pqm[j] >> lane) & 1;
+          const int qq = pf ? q[j] : 0;
+          const int c0 = s_ctx[j];
+          l_tp += qq;
+          l_cp += pf ? c0 + qq : 0;
+          l_ap += pf ? (int64_t)qq * c0 + ((int64_t)qq * (qq + 1)) / 2 : 0;
+          Rc += popc(ballot(pf && c0 + qq == s_tgt[j] && s_fd[j] == 0));
+        }
+      }
       TP = wsum(l_tp);
       CP = wsum(l_cp);
       AP = wsum64(l_ap);
     }
-    const int64_t iter_ns = iteration_ns(A.coef, iF, iB, (int64_t)nD + TP, TP, AP, CP, nD, CD, Rl);
+    double iter_d;
+    const int64_t iter_ns = iteration_ns(roofc, A.n_layers, iF, iB, nD + TP, TP, AP, CP, nD,
+                                         CD, nD + Rc, &iter_d);
 
     // ---- 7. advance the clock and every scheduled request
     const int64_t t_end = t + iter_ns;
     const int used = NB - freeb;
     if (used > peak) peak = used;
-    ubns = ubns + (double)used * (double)iter_ns;
+    ubns = ubns + (double)used * iter_d;
     ++n_iters;
     pf_tok += TP;
     dec_tok += nD;
@@ -533,54 +660,63 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
 #pragma unroll
     for (int j = 0; j < NCH; ++j) {
       fin[j] = false;
-      if (dec[j]) {
-        s_ctx[j] += 1;
-        s_rem[j] -= 1;
-        s_room[j] -= 1;
-        const int64_t g = t_end - s_last[j];
-        if (g > s_gap[j]) s_gap[j] = g;
-        s_last[j] = t_end;
-        fin[j] = s_rem[j] == 0;
-      } else if (act[j] && q[j] > 0) {
-        s_ctx[j] += q[j];
-        if (s_ctx[j] == s_tgt[j] && s_first[j] < 0) {  // the full prefill emits a token
-          s_first[j] = t_end;
+      fm[j] = 0;
+      if (j < nch) {
+        if (dec[j]) {
+          s_ctx[j] += 1;
+          s_rem[j] -= 1;
+          s_room[j] -= 1;
+          const int64_t g = t_end - s_last[j];
+          s_gap[j] = g > s_gap[j] ? g : s_gap[j];
           s_last[j] = t_end;
+          fin[j] = s_rem[j] == 0;
+        } else if ((pqm[j] >> lane) & 1) {
+          s_ctx[j] += q[j];
+          if (s_ctx[j] == s_tgt[j] && s_fd[j] == 0) {  // the full prefill emits a token
+            s_fd[j] = 1;
+            s_last[j] = t_end;
+            L.first[j * 64 + lane] = t_end;
+          }
         }
+        fm[j] = ballot(fin[j]);
+        nfin += popc(fm[j]);
       }
-      fm[j] = ballot(fin[j]);
-      nfin += popc(fm[j]);
     }
     if (nfin > 0) {
       int base = n_done;
       int l_freed = 0;
 #pragma unroll
       for (int j = 0; j < NCH; ++j) {
-        if (fin[j]) {
-          const int id = s_id[j];
-          const int64_t arr = rec[id].arrival_ns;
-          const int64_t tt = s_first[j] - arr;
-          const int64_t ee = t_end - arr;
-          acc_ttft += tt;
-          acc_e2e += ee;
-          acc_tpot += t_end - s_first[j];
-          acc_maxe2e = ee > acc_maxe2e ? ee : acc_maxe2e;
-          acc_last = t_end;
-          if (tt <= A.slo_ttft_ns && s_gap[j] <= A.slo_tpot_ns) acc_slo += 1;
-          acc_dig += record_hash(id, s_admit[j], s_first[j], t_end, s_gap[j], s_npre[j],
-                                 TS_REQ_DONE);
-          if (RR) {
-            ts_req_result o;
-            o.admit_ns = s_admit[j]; o.first_token_ns = s_first[j]; o.finish_ns = t_end;
-            o.max_gap_ns = s_gap[j]; o.n_preempt = s_npre[j]; o.status = TS_REQ_DONE;
-            RR[id] = o;
+        if (j < nch) {
+          if (fin[j]) {
+            const int s = j * 64 + lane;
+            const int id = L.id[s];
+            const int npr = L.npre[s];
+            const int64_t admit = L.admit[s];
+            const int64_t first = L.first[s];
+            const int64_t arr = rec[id].arrival_ns;
+            const int64_t tt = first - arr;
+            const int64_t ee = t_end - arr;
+            acc_ttft += tt;
+            acc_e2e += ee;
+            acc_tpot += t_end - first;
+            acc_maxe2e = ee > acc_maxe2e ? ee : acc_maxe2e;
+            acc_last = t_end;
+            if (tt <= A.slo_ttft_ns && s_gap[j] <= A.slo_tpot_ns) acc_slo += 1;
+            acc_dig += record_hash(id, admit, first, t_end, s_gap[j], npr, TS_REQ_DONE);
+            if (RR) {
+              ts_req_result o;
+              o.admit_ns = admit; o.first_token_ns = first; o.finish_ns = t_end;
+              o.max_gap_ns = s_gap[j]; o.n_preempt = npr; o.status = TS_REQ_DONE;
+              RR[id] = o;
+            }
+            const int pos = base + rank_below(fm[j]);
+            E2E[pos] = ee;
+            TTFT[pos] = tt;
+            l_freed += s_alloc[j];
           }
-          const int pos = base + rank_below(fm[j]);
-          E2E[pos] = ee;
-          TTFT[pos] = tt;
-          l_freed += s_alloc[j];
+          base += popc(fm[j]);
         }
-        base += popc(fm[j]);
       }
       freeb += wsum(l_freed);
       n_done += nfin;
@@ -590,23 +726,28 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       int off = 0;
 #pragma unroll
       for (int j = 0; j < NCH; ++j) {
-        keep[j] = act[j] && !fin[j];
-        const uint64_t km = ballot(keep[j]);
-        pos[j] = off + rank_below(km);
-        off += popc(km);
+        keep[j] = false;
+        pos[j] = 0;
+        if (j < nch) {
+          keep[j] = act[j] && !fin[j];
+          const uint64_t km = ballot(keep[j]);
+          pos[j] = off + rank_below(km);
+          off += popc(km);
+        }
       }
-      int* s32 = reinterpret_cast<int*>(scratch);
-      compact_field<NCH, int>(s_ctx, keep, pos, s32, lane);
-      compact_field<NCH, int>(s_tgt, keep, pos, s32, lane);
-      compact_field<NCH, int>(s_rem, keep, pos, s32, lane);
-      compact_field<NCH, int>(s_room, keep, pos, s32, lane);
-      compact_field<NCH, int>(s_alloc, keep, pos, s32, lane);
-      compact_field<NCH, int>(s_id, keep, pos, s32, lane);
-      compact_field<NCH, int>(s_npre, keep, pos, s32, lane);
-      compact_field<NCH, int64_t>(s_admit, keep, pos, scratch, lane);
-      compact_field<NCH, int64_t>(s_first, keep, pos, scratch, lane);
-      compact_field<NCH, int64_t>(s_last, keep, pos, scratch, lane);
-      compact_field<NCH, int64_t>(s_gap, keep, pos, scratch, lane);
+      int* s32 = reinterpret_cast<int*>(L.u.scratch);
+      compact_reg<NCH, int>(s_ctx, keep, pos, s32, lane, nch);
+      compact_reg<NCH, int>(s_tgt, keep, pos, s32, lane, nch);
+      compact_reg<NCH, int>(s_rem, keep, pos, s32, lane, nch);
+      compact_reg<NCH, int>(s_room, keep, pos, s32, lane, nch);
+      compact_reg<NCH, int>(s_alloc, keep, pos, s32, lane, nch);
+      compact_reg<NCH, int>(s_fd, keep, pos, s32, lane, nch);
+      compact_reg<NCH, int64_t>(s_last, keep, pos, L.u.scratch, lane, nch);
+      compact_reg<NCH, int64_t>(s_gap, keep, pos, L.u.scratch, lane, nch);
+      compact_lds<NCH, int>(L.id, keep, pos, lane, nch);
+      compact_lds<NCH, int>(L.npre, keep, pos, lane, nch);
+      compact_lds<NCH, int64_t>(L.admit, keep, pos, lane, nch);
+      compact_lds<NCH, int64_t>(L.first, keep, pos, lane, nch);
       nrun -= nfin;
     }
     t = t_end;
@@ -653,10 +794,18 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
 // counter until none is left.
 template <int NCH>
 __global__ __launch_bounds__(64) void sim_kernel(SimArgs A) {
-  __shared__ StageSlot stage[64];
-  __shared__ int64_t scratch[64 * NCH];
+  __shared__ SlotLds<NCH> L;
   const int lane = lane_id();
   QEntry* Q = A.queue + (size_t)blockIdx.x * kQueueCap;
+  LaneRoof roofc;
+  const int cl = lane < 8 ? lane : 7;
+  roofc.f = A.lc.f[cl];
+  roofc.b0 = A.lc.b0[cl];
+  roofc.b1 = A.lc.b1[cl];
+  roofc.b2 = A.lc.b2[cl];
+  roofc.is_attp = lane == 1;
+  roofc.is_attd = lane == 2;
+  roofc.is_lm = lane == 6;
   // A workgroup never needs more tickets than there are points.
   for (int taken = 0; taken <= A.n_order; ++taken) {
     // All lanes take part (lane 0 adds 1, the others 0) so the ticket is
@@ -664,7 +813,7 @@ __global__ __launch_bounds__(64) void sim_kernel(SimArgs A) {
     const unsigned old = atomicAdd(A.counter, lane == 0 ? 1u : 0u);
     const int tk = __builtin_amdgcn_readfirstlane((int)old);
     if (tk >= A.n_order) break;
-    simulate_point<NCH>(A, A.order[tk], stage, scratch, Q, lane);
+    simulate_point<NCH>(A, A.order[tk], L, Q, lane, roofc);
   }
 }
 

@@ -46,10 +46,16 @@ struct CostCoef {
   double n_layers;
 };
 
-// A request waiting after recompute preemption, 48 bytes.
+// A request waiting after recompute preemption, 64 bytes.
 struct __attribute__((aligned(16))) QEntry {
-  int32_t id, target, rem, n_pre;
+  int32_t id, target, rem, n_pre, first_done, pad0, pad1, pad2;
   int64_t admit, first, last, gap;
+};
+
+// Per-lane roofline coefficients (doubles holding exact integers): lane j < 7
+// prices operator j as F = f * X_j, B = (b0 + b1 * Y_j) + b2 * Z_j.
+struct LaneCoef {
+  double f[8], b0[8], b1[8], b2[8];
 };
 
 constexpr int kQueueCap = 256;  // >= max_batch: queue + running never exceed max_batch
@@ -70,7 +76,8 @@ struct SimArgs {
   int64_t slo_ttft_ns;
   int64_t slo_tpot_ns;
   uint64_t time_limit_ticks;   // 0 = none; 100 MHz device clock ticks per point
-  CostCoef coef;
+  double n_layers;
+  LaneCoef lc;
 };
 
 }  // namespace tsw
