@@ -180,6 +180,7 @@ struct ts_sweep {
   int32_t* d_order = nullptr;       // all classes, concatenated
   unsigned int* d_counter = nullptr;
   QEntry* d_queue[kClasses] = {nullptr, nullptr, nullptr};
+  ReqTimes* d_times[kClasses] = {nullptr, nullptr, nullptr};
   ts_point_result* d_res = nullptr;
   ts_req_result* d_req = nullptr;
   int64_t* d_e2e = nullptr;
@@ -205,6 +206,7 @@ void release(ts_sweep* h) {
   (void)hipFree(h->d_order);
   (void)hipFree(h->d_counter);
   for (int c = 0; c < kClasses; ++c) (void)hipFree(h->d_queue[c]);
+  for (int c = 0; c < kClasses; ++c) (void)hipFree(h->d_times[c]);
   (void)hipFree(h->d_res);
   (void)hipFree(h->d_req);
   (void)hipFree(h->d_e2e);
@@ -392,6 +394,11 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
     if (e != hipSuccess) { release(h); return device_error(e, "occupancy query"); }
     per_cu = std::max(per_cu, 1);
     h->grid[c] = std::min(h->class_n[c], n_cu * per_cu);
+    // per-workgroup request-time table: max_n entries; keep it under 1 GiB
+    const int64_t cap = std::max<int64_t>(1, ((int64_t)1 << 30) /
+                                                 ((int64_t)std::max<int64_t>(max_n, 1) *
+                                                  (int64_t)sizeof(ReqTimes)));
+    h->grid[c] = (int)std::min<int64_t>(h->grid[c], cap);
   }
   h->stats_grid = std::max(1, std::min(count, n_cu * 8));
 
@@ -411,8 +418,11 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
   if (ae == hipSuccess) ae = dev_alloc(&h->d_points, dp.size());
   if (ae == hipSuccess) ae = dev_alloc(&h->d_order, order.size());
   if (ae == hipSuccess) ae = dev_alloc(&h->d_counter, (size_t)kClasses);
-  for (int c = 0; c < kClasses && ae == hipSuccess; ++c)
-    if (h->grid[c] > 0) ae = dev_alloc(&h->d_queue[c], (size_t)h->grid[c] * kQueueCap);
+  for (int c = 0; c < kClasses && ae == hipSuccess; ++c) {
+    if (h->grid[c] == 0) continue;
+    ae = dev_alloc(&h->d_queue[c], (size_t)h->grid[c] * kQueueCap);
+    if (ae == hipSuccess) ae = dev_alloc(&h->d_times[c], (size_t)h->grid[c] * per_point);
+  }
   if (ae == hipSuccess) ae = dev_alloc(&h->d_res, (size_t)count);
   if (ae == hipSuccess) ae = dev_alloc(&h->d_e2e, (size_t)count * per_point);
   if (ae == hipSuccess) ae = dev_alloc(&h->d_ttft, (size_t)count * per_point);
@@ -473,6 +483,7 @@ int ts_sweep_run(ts_sweep* h, void* hip_stream) {
     a.max_n = h->max_n;
     a.counter = h->d_counter + c;
     a.queue = h->d_queue[c];
+    a.times = h->d_times[c];
     a.res = h->d_res;
     a.req = h->d_req;
     a.e2e = h->d_e2e;

@@ -183,63 +183,67 @@ __device__ __forceinline__ int64_t iteration_ns(const LaneRoof& c, double n_laye
   return (int64_t)it;
 }
 
-// Admission staging: one entry per admitted candidate of a window.
-struct StageSlot {
-  int32_t id, tgt, rem, npre, q, alloc, room, first_done;
-  int64_t admit, first, last, gap;
+// ------------------------------------------------------------ slot state
+// Running requests occupy slots in admission order.  Slot s lives in chunk
+// s / 64, lane s % 64: chunk 0 in registers, chunks 1.. in LDS (only points
+// with more than 64 running requests touch them).  Per slot, the hot state:
+//   ctx   KV tokens resident          tgt  prefill target (prompt + decoded)
+//   rem   decode iterations left      room free token slots in held blocks
+//   fl    FL_FIRST: first token emitted; FL_STALE: the last token is older
+//         than the previous iteration (set on re-admission after preemption)
+//   q     tokens scheduled this iteration (prefill slots)
+//   gap   largest interval between consecutive tokens so far
+// Held blocks are (max(ctx, tgt) + room) / block and are never stored.
+enum : int { FL_FIRST = 1, FL_STALE = 2 };
+
+struct Hot {
+  int ctx, tgt, rem, room, fl, q;
+  int64_t gap;
 };
 
-// Per-workgroup LDS: the cold fields of the slots (used only at admission,
-// preemption and finish) and a staging area shared by admission and the
-// stable compaction.
+// Admission staging: one entry per admitted candidate of a window.
+struct StageSlot {
+  int32_t id, tgt, rem, npre, fl, q, room, pad;
+  int64_t gap;
+};
+
 template <int NCH>
 struct SlotLds {
-  int32_t id[64 * NCH];
-  int32_t npre[64 * NCH];
-  int64_t admit[64 * NCH];
-  int64_t first[64 * NCH];
+  static constexpr int NX = NCH > 1 ? NCH - 1 : 1;  // LDS chunks (storage for one when unused)
+  int32_t x_ctx[NX * 64], x_tgt[NX * 64], x_rem[NX * 64], x_room[NX * 64], x_q[NX * 64];
+  int64_t x_gap[NX * 64];
+  int32_t x_fl[NX * 64];
+  int32_t id[NCH * 64];    // request index per slot
+  int32_t npre[NCH * 64];  // times preempted per slot
   union {
     StageSlot stage[64];
-    int64_t scratch[64 * NCH];
+    int64_t scratch[NCH * 64];
   } u;
 };
 
-// Stable compaction of one register field through LDS scratch.
-template <int NCH, typename Tv>
-__device__ __forceinline__ void compact_reg(Tv (&f)[NCH], const bool (&keep)[NCH],
-                                            const int (&pos)[NCH], Tv* scratch, int lane,
-                                            int nch) {
-#pragma unroll
-  for (int j = 0; j < NCH; ++j)
-    if (j < nch && keep[j]) scratch[pos[j]] = f[j];
-  __syncthreads();
-#pragma unroll
-  for (int j = 0; j < NCH; ++j)
-    if (j < nch) f[j] = scratch[j * 64 + lane];
-  __syncthreads();
+template <int NCH>
+__device__ __forceinline__ Hot load_chunk(const SlotLds<NCH>& L, const Hot& h0, int j, int lane) {
+  if (j == 0) return h0;
+  const int e = (j - 1) * 64 + lane;
+  Hot h;
+  h.ctx = L.x_ctx[e]; h.tgt = L.x_tgt[e]; h.rem = L.x_rem[e]; h.room = L.x_room[e];
+  h.fl = L.x_fl[e]; h.q = L.x_q[e]; h.gap = L.x_gap[e];
+  return h;
 }
-
-// Stable compaction of one LDS field in place (positions only move down,
-// every chunk is read before it is written).
-template <int NCH, typename Tv>
-__device__ __forceinline__ void compact_lds(Tv* f, const bool (&keep)[NCH],
-                                            const int (&pos)[NCH], int lane, int nch) {
-#pragma unroll
-  for (int j = 0; j < NCH; ++j) {
-    if (j < nch) {
-      const Tv v = f[j * 64 + lane];
-      __syncthreads();
-      if (keep[j]) f[pos[j]] = v;
-      __syncthreads();
-    }
-  }
+template <int NCH>
+__device__ __forceinline__ void store_chunk(SlotLds<NCH>& L, Hot& h0, int j, int lane,
+                                            const Hot& h) {
+  if (j == 0) { h0 = h; return; }
+  const int e = (j - 1) * 64 + lane;
+  L.x_ctx[e] = h.ctx; L.x_tgt[e] = h.tgt; L.x_rem[e] = h.rem; L.x_room[e] = h.room;
+  L.x_fl[e] = h.fl; L.x_q[e] = h.q; L.x_gap[e] = h.gap;
 }
 
 // ------------------------------------------------------------ one point
 template <int NCH>
 __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
-                                               SlotLds<NCH>& L, QEntry* Q, const int lane,
-                                               const LaneRoof& roofc) {
+                                               SlotLds<NCH>& L, QEntry* Q, ReqTimes* RT,
+                                               const int lane, const LaneRoof& roofc) {
   const DevPoint P = A.points[pidx];
   const TraceRec* __restrict__ rec = A.recs + P.trace_off;
   const int N = P.n, NB = P.num_blocks, B = P.block, M = P.max_batch, K = P.chunk;
@@ -253,7 +257,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
 
   // per-lane accumulators of finished / rejected requests
   int64_t acc_ttft = 0, acc_e2e = 0, acc_tpot = 0, acc_maxe2e = 0, acc_last = 0;
-  int64_t acc_slo = 0;
+  int acc_slo = 0;
   uint64_t acc_dig = 0;
   int n_rej = 0;
 
@@ -290,20 +294,15 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
 
   // arrival window: lane l holds record wbase + l
   int64_t w_arr = INT64_MAX;
-  int w_p = 0, w_o = 0;
+  int w_po = 0;
   if (lane < N) {
     const TraceRec r = rec[lane];
-    w_arr = r.arrival_ns; w_p = r.prompt; w_o = r.output;
+    w_arr = r.arrival_ns; w_po = r.prompt + r.output;
   }
 
-  // hot slot state in registers: slot s = chunk s / 64, lane s % 64
-  int s_ctx[NCH], s_tgt[NCH], s_rem[NCH], s_room[NCH], s_alloc[NCH], s_fd[NCH], q[NCH];
-  int64_t s_last[NCH], s_gap[NCH];
-#pragma unroll
-  for (int j = 0; j < NCH; ++j) {
-    s_ctx[j] = s_tgt[j] = s_rem[j] = s_room[j] = s_alloc[j] = s_fd[j] = q[j] = 0;
-    s_last[j] = s_gap[j] = 0;
-  }
+  Hot h0;  // chunk 0 in registers
+  h0.ctx = h0.tgt = h0.rem = h0.room = h0.fl = h0.q = 0;
+  h0.gap = 0;
 
   const uint64_t clock0 = A.time_limit_ticks ? __builtin_amdgcn_s_memrealtime() : 0;
   while (status == TS_POINT_OK) {
@@ -322,8 +321,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       if (nn > next) {
         int add = nn - next;
         if (P.may_reject) {
-          const bool rj = lane >= next - wbase && lane < cnt &&
-                          (int64_t)w_p + (int64_t)w_o > cap_tok;
+          const bool rj = lane >= next - wbase && lane < cnt && (int64_t)w_po > cap_tok;
           add -= popc(ballot(rj));
         }
         if (npre == 0 && nwait == 0) head_need = -1;
@@ -332,10 +330,11 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       }
       if (cnt == 64 && nn < N) {
         wbase = nn;
-        w_arr = INT64_MAX; w_p = 0; w_o = 0;
+        w_arr = INT64_MAX;
+        w_po = 0;
         if (wbase + lane < N) {
           const TraceRec r = rec[wbase + lane];
-          w_arr = r.arrival_ns; w_p = r.prompt; w_o = r.output;
+          w_arr = r.arrival_ns; w_po = r.prompt + r.output;
         }
         continue;
       }
@@ -355,71 +354,77 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
     }
 
     // ---- 3. reserve a block for decodes crossing a block boundary
-    int nch = (nrun + 63) >> 6;  // register chunks holding running slots
-    bool act[NCH], dec[NCH];
+    int nch = (nrun + 63) >> 6;
+    nch = nch < NCH ? nch : NCH;
     int nneed = 0;
-#pragma unroll
-    for (int j = 0; j < NCH; ++j) {
-      act[j] = false;
-      dec[j] = false;
-      if (j < nch) {
-        act[j] = (j * 64 + lane) < nrun;
-        dec[j] = act[j] && s_ctx[j] >= s_tgt[j];
-        nneed += popc(ballot(dec[j] && s_room[j] == 0));
-      }
+#pragma nounroll
+    for (int j = 0; j < nch; ++j) {
+      const Hot h = load_chunk<NCH>(L, h0, j, lane);
+      const bool act = (j * 64 + lane) < nrun;
+      nneed += popc(ballot(act && h.ctx >= h.tgt && h.room == 0));
     }
     bool preempted = false;
     if (nneed <= freeb) {
       freeb -= nneed;
       if (nneed > 0) {
-#pragma unroll
-        for (int j = 0; j < NCH; ++j)
-          if (j < nch && dec[j] && s_room[j] == 0) { s_alloc[j] += 1; s_room[j] += B; }
+#pragma nounroll
+        for (int j = 0; j < nch; ++j) {
+          const bool act = (j * 64 + lane) < nrun;
+          if (j == 0) {
+            if (act && h0.ctx >= h0.tgt && h0.room == 0) h0.room += B;
+          } else {
+            const int e = (j - 1) * 64 + lane;
+            if (act && L.x_ctx[e] >= L.x_tgt[e] && L.x_room[e] == 0) L.x_room[e] = B;
+          }
+        }
       }
     } else {
       // Recompute preemption from the tail: keep the longest prefix of slots
       // whose held + needed blocks fit in the whole budget.
       int carry = 0, k = 0, kept = 0;
-      bool keep[NCH];
-#pragma unroll
-      for (int j = 0; j < NCH; ++j) {
-        keep[j] = false;
-        if (j < nch) {
-          const int need = (dec[j] && s_room[j] == 0) ? 1 : 0;
-          const int v = act[j] ? s_alloc[j] + need : 0;
-          const int S = scan_i32(v) + carry;
-          keep[j] = act[j] && S <= NB;
-          k += popc(ballot(keep[j]));
-          kept += wsum(keep[j] ? v : 0);
-          carry = rdl(S, 63);
-        }
+#pragma nounroll
+      for (int j = 0; j < nch; ++j) {
+        const Hot h = load_chunk<NCH>(L, h0, j, lane);
+        const bool act = (j * 64 + lane) < nrun;
+        const int top = h.ctx > h.tgt ? h.ctx : h.tgt;
+        const int need = (h.ctx >= h.tgt && h.room == 0) ? 1 : 0;
+        const int v = act ? (top + h.room) / B + need : 0;  // held + needed blocks
+        const int S = scan_i32(v) + carry;
+        const bool keep = act && S <= NB;
+        k += popc(ballot(keep));
+        kept += wsum(keep ? v : 0);
+        carry = rdl(S, 63);
       }
       freeb = NB - kept;
       const int nv = nrun - k;
       qhead = (qhead - nv) & (kQueueCap - 1);
-#pragma unroll
-      for (int j = 0; j < NCH; ++j) {
-        if (j < nch) {
-          const int s = j * 64 + lane;
-          if (keep[j]) {
-            if (dec[j] && s_room[j] == 0) { s_alloc[j] += 1; s_room[j] += B; }
-          } else if (act[j]) {
-            // victims keep admission order at the front of the waiting queue:
-            // they are older than every request still waiting
-            QEntry e;
-            e.id = L.id[s];
-            e.target = s_ctx[j] > s_tgt[j] ? s_ctx[j] : s_tgt[j];  // prompt + tokens decoded
-            e.rem = s_rem[j];
-            e.n_pre = L.npre[s] + 1;
-            e.first_done = s_fd[j];
-            e.pad0 = e.pad1 = e.pad2 = 0;
-            e.admit = L.admit[s];
-            e.first = L.first[s];
-            e.last = s_last[j];
-            e.gap = s_gap[j];
-            Q[(qhead + s - k) & (kQueueCap - 1)] = e;
+#pragma nounroll
+      for (int j = 0; j < nch; ++j) {
+        Hot h = load_chunk<NCH>(L, h0, j, lane);
+        const int s = j * 64 + lane;
+        if (s < k) {
+          if (h.ctx >= h.tgt && h.room == 0) h.room += B;
+        } else if (s < nrun) {
+          // victims keep admission order at the front of the waiting queue:
+          // they are older than every request still waiting
+          const int id = L.id[s];
+          int fl = h.fl;
+          if ((fl & FL_FIRST) && !(fl & FL_STALE)) {
+            // the last token is the one emitted at the end of the previous iteration
+            if (h.ctx >= h.tgt) RT[id].last = t;
+            fl |= FL_STALE;
           }
+          QEntry e;
+          e.id = id;
+          e.target = h.ctx > h.tgt ? h.ctx : h.tgt;  // prompt + tokens decoded
+          e.rem = h.rem;
+          e.n_pre = L.npre[s] + 1;
+          e.flags = fl;
+          e.pad = 0;
+          e.gap = h.gap;
+          Q[(qhead + s - k) & (kQueueCap - 1)] = e;
         }
+        store_chunk<NCH>(L, h0, j, lane, h);
       }
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
       npre += nv;
@@ -428,61 +433,51 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       preempted = true;
       head_need = -1;
       nch = (nrun + 63) >> 6;
-#pragma unroll
-      for (int j = 0; j < NCH; ++j) {
-        act[j] = j < nch && (j * 64 + lane) < nrun;
-        dec[j] = act[j] && s_ctx[j] >= s_tgt[j];
-      }
+      nch = nch < NCH ? nch : NCH;
     }
 
     // ---- 4. token budget: decodes one token, running prefills share the rest
     int nD = 0, npf = 0;
-    uint64_t pfm[NCH];
-#pragma unroll
-    for (int j = 0; j < NCH; ++j) {
-      pfm[j] = 0;
-      if (j < nch) {
-        nD += popc(ballot(dec[j]));
-        pfm[j] = ballot(act[j] && !dec[j]);
-        npf += popc(pfm[j]);
-      }
+#pragma nounroll
+    for (int j = 0; j < nch; ++j) {
+      const Hot h = load_chunk<NCH>(L, h0, j, lane);
+      const bool act = (j * 64 + lane) < nrun;
+      nD += popc(ballot(act && h.ctx >= h.tgt));
+      npf += popc(ballot(act && h.ctx < h.tgt));
     }
     int R = 0;
-    if (!unlimited) {
-      R = K - nD;
-      if (npf == 1) {
-        // one running prefill takes min(what it still needs, the budget)
-#pragma unroll
-        for (int j = 0; j < NCH; ++j) {
-          if (pfm[j] != 0) {
-            const int l = (int)__builtin_ctzll(pfm[j]);
-            const int left = rdl(s_tgt[j] - s_ctx[j], l);
-            const int qv = left < R ? left : R;
-            q[j] = qv;
-            R -= qv;
-          }
-        }
-      } else if (npf > 1) {
-        int carry = 0;
-#pragma unroll
-        for (int j = 0; j < NCH; ++j) {
-          if (j < nch) {
-            const bool pf = act[j] && !dec[j];
-            const int left = pf ? s_tgt[j] - s_ctx[j] : 0;
+    if (!unlimited) R = K - nD;
+    if (npf > 0) {
+      int carry = 0;  // prefill tokens still needed by the slots before this chunk
+#pragma nounroll
+      for (int j = 0; j < nch; ++j) {
+        const Hot h = load_chunk<NCH>(L, h0, j, lane);
+        const bool pf = (j * 64 + lane) < nrun && h.ctx < h.tgt;
+        const int left = pf ? h.tgt - h.ctx : 0;
+        int qv = left;
+        if (!unlimited) {
+          if (npf == 1) {  // one running prefill: min(what it needs, the budget)
+            qv = left < R ? left : R;
+            const uint64_t pm = ballot(pf);
+            if (pm != 0) carry += rdl(left, (int)__builtin_ctzll(pm));
+          } else {
             const int S = scan_i32(left);
             int avail = R - (S - left + carry);
             avail = avail < 0 ? 0 : avail;
-            q[j] = left < avail ? left : avail;
+            qv = left < avail ? left : avail;
             carry += rdl(S, 63);
           }
         }
+        if (j == 0) {
+          if (pf) h0.q = qv;
+        } else if (pf) {
+          L.x_q[(j - 1) * 64 + lane] = qv;
+        }
+      }
+      if (!unlimited) {
         R = R - carry;
         if (R < 0) R = 0;
       }
-    } else {
-#pragma unroll
-      for (int j = 0; j < NCH; ++j)
-        if (j < nch) q[j] = s_tgt[j] - s_ctx[j];
     }
 
     // ---- 5. FCFS admission over 64-candidate windows (none after preemption)
@@ -492,25 +487,22 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
         if (head_need >= 0 && head_need > freeb) break;
         const bool fromq = npre > 0;
         bool valid;
-        int c_id, c_tgt, c_rem, c_npre, c_fd;
-        int64_t c_admit, c_first, c_last, c_gap;
+        int c_id, c_tgt, c_rem, c_npre, c_fl;
+        int64_t c_gap;
         if (fromq) {
           valid = lane < npre;
           __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
           if (valid) {
             const QEntry e = Q[(qhead + lane) & (kQueueCap - 1)];
-            c_id = e.id; c_tgt = e.target; c_rem = e.rem; c_npre = e.n_pre;
-            c_fd = e.first_done;
-            c_admit = e.admit; c_first = e.first; c_last = e.last; c_gap = e.gap;
+            c_id = e.id; c_tgt = e.target; c_rem = e.rem; c_npre = e.n_pre; c_fl = e.flags;
+            c_gap = e.gap;
           } else {
-            c_id = 0; c_tgt = 1; c_rem = 1; c_npre = 0; c_fd = 0;
-            c_admit = -1; c_first = -1; c_last = -1; c_gap = 0;
+            c_id = 0; c_tgt = 1; c_rem = 1; c_npre = 0; c_fl = 0; c_gap = 0;
           }
         } else {
           const int idx = next_new + lane;
           valid = idx < next;
-          c_id = idx; c_npre = 0; c_fd = 0; c_admit = -1; c_first = -1; c_last = -1; c_gap = 0;
-          c_tgt = 1; c_rem = 1;
+          c_id = idx; c_npre = 0; c_fl = 0; c_gap = 0; c_tgt = 1; c_rem = 1;
           if (valid) {
             const TraceRec r = rec[idx];
             c_tgt = r.prompt;
@@ -547,23 +539,24 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
         freeb -= rdl(SN, last_lane);
         if (!unlimited) R -= wsum(adm ? qv : 0);
         if (adm) {
+          if (!fromq) RT[c_id].admit = t;  // first admission
           StageSlot st;
-          st.id = c_id; st.tgt = c_tgt; st.rem = c_rem; st.npre = c_npre; st.q = qv;
-          st.alloc = need; st.room = need * B - c_tgt; st.first_done = c_fd;
-          st.admit = c_admit < 0 ? t : c_admit;
-          st.first = c_first; st.last = c_last; st.gap = c_gap;
+          st.id = c_id; st.tgt = c_tgt; st.rem = c_rem; st.npre = c_npre; st.fl = c_fl;
+          st.q = qv; st.room = need * B - c_tgt; st.pad = 0; st.gap = c_gap;
           L.u.stage[rank] = st;
         }
         __syncthreads();
-#pragma unroll
-        for (int j = 0; j < NCH; ++j) {
+#pragma nounroll
+        for (int j = nrun >> 6; j < NCH && j * 64 < nrun + a; ++j) {
           const int s = j * 64 + lane;
           if (s >= nrun && s < nrun + a) {
             const StageSlot st = L.u.stage[s - nrun];
-            s_ctx[j] = 0; s_tgt[j] = st.tgt; s_rem[j] = st.rem; q[j] = st.q;
-            s_alloc[j] = st.alloc; s_room[j] = st.room; s_fd[j] = st.first_done;
-            s_last[j] = st.last; s_gap[j] = st.gap;
-            L.id[s] = st.id; L.npre[s] = st.npre; L.admit[s] = st.admit; L.first[s] = st.first;
+            Hot h;
+            h.ctx = 0; h.tgt = st.tgt; h.rem = st.rem; h.room = st.room; h.fl = st.fl;
+            h.q = st.q; h.gap = st.gap;
+            store_chunk<NCH>(L, h0, j, lane, h);
+            L.id[s] = st.id;
+            L.npre[s] = st.npre;
           }
         }
         __syncthreads();
@@ -583,63 +576,46 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
         }
       }
       nch = (nrun + 63) >> 6;
-#pragma unroll
-      for (int j = 0; j < NCH; ++j) act[j] = j < nch && (j * 64 + lane) < nrun;
+      nch = nch < NCH ? nch : NCH;
     }
 
     // ---- 6. batch sums and the roofline iteration time
-    // decodes: count by ballot, keys by one wave reduction
-    int l_cd = 0;
-    uint64_t pqm[NCH];
-    int npq = 0;
-#pragma unroll
-    for (int j = 0; j < NCH; ++j) {
-      pqm[j] = 0;
-      if (j < nch) {
-        if (dec[j]) l_cd += s_ctx[j] + 1;
-        pqm[j] = ballot(act[j] && !dec[j] && q[j] > 0);
-        npq += popc(pqm[j]);
-      }
-    }
-    const int CD = nD > 0 ? wsum(l_cd) : 0;
-    int TP = 0, CP = 0, Rc = 0;
-    int64_t AP = 0;
-    if (npq > 0 && npq <= 2) {
-      // one or two prefills: read them out lane by lane
-#pragma unroll
-      for (int j = 0; j < NCH; ++j) {
-        uint64_t m = pqm[j];
-        while (m != 0) {
+    int l_cd = 0, l_tp = 0, l_cp = 0, TP = 0, CP = 0, Rc = 0;
+    int64_t l_ap = 0, AP = 0;
+    bool wide = false;  // some chunk has more than two prefills: reduce by DPP
+#pragma nounroll
+    for (int j = 0; j < nch; ++j) {
+      const Hot h = load_chunk<NCH>(L, h0, j, lane);
+      const bool act = (j * 64 + lane) < nrun;
+      const bool dec = act && h.ctx >= h.tgt;
+      const bool pf = act && !dec && h.q > 0;
+      if (dec) l_cd += h.ctx + 1;
+      uint64_t m = ballot(pf);
+      Rc += popc(ballot(pf && h.ctx + h.q == h.tgt && !(h.fl & FL_FIRST)));  // first tokens
+      if (popc(m) <= 2) {
+        while (m != 0) {  // one or two prefills: read them out lane by lane
           const int l = (int)__builtin_ctzll(m);
           m &= m - 1;
-          const int qq = rdl(q[j], l);
-          const int c0 = rdl(s_ctx[j], l);
-          const int tg = rdl(s_tgt[j], l);
-          const int fd = rdl(s_fd[j], l);
+          const int qq = rdl(h.q, l);
+          const int c0 = rdl(h.ctx, l);
           TP += qq;
           CP += c0 + qq;
           AP += (int64_t)qq * c0 + ((int64_t)qq * (qq + 1)) / 2;
-          if (c0 + qq == tg && fd == 0) Rc += 1;  // emits its first token
+        }
+      } else {
+        wide = true;
+        if (pf) {
+          l_tp += h.q;
+          l_cp += h.ctx + h.q;
+          l_ap += (int64_t)h.q * h.ctx + ((int64_t)h.q * (h.q + 1)) / 2;
         }
       }
-    } else if (npq > 2) {
-      int l_tp = 0, l_cp = 0;
-      int64_t l_ap = 0;
-#pragma unroll
-      for (int j = 0; j < NCH; ++j) {
-        if (j < nch) {
-          const bool pf = (pqm[j] >> lane) & 1;
-          const int qq = pf ? q[j] : 0;
-          const int c0 = s_ctx[j];
-          l_tp += qq;
-          l_cp += pf ? c0 + qq : 0;
-          l_ap += pf ? (int64_t)qq * c0 + ((int64_t)qq * (qq + 1)) / 2 : 0;
-          Rc += popc(ballot(pf && c0 + qq == s_tgt[j] && s_fd[j] == 0));
-        }
-      }
-      TP = wsum(l_tp);
-      CP = wsum(l_cp);
-      AP = wsum64(l_ap);
+    }
+    const int CD = nD > 0 ? wsum(l_cd) : 0;
+    if (wide) {
+      TP += wsum(l_tp);
+      CP += wsum(l_cp);
+      AP += wsum64(l_ap);
     }
     double iter_d;
     const int64_t iter_ns = iteration_ns(roofc, A.n_layers, iF, iB, nD + TP, TP, AP, CP, nD,
@@ -654,101 +630,120 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
     pf_tok += TP;
     dec_tok += nD;
 
-    bool fin[NCH];
-    uint64_t fm[NCH];
-    int nfin = 0;
-#pragma unroll
-    for (int j = 0; j < NCH; ++j) {
-      fin[j] = false;
-      fm[j] = 0;
-      if (j < nch) {
-        if (dec[j]) {
-          s_ctx[j] += 1;
-          s_rem[j] -= 1;
-          s_room[j] -= 1;
-          const int64_t g = t_end - s_last[j];
-          s_gap[j] = g > s_gap[j] ? g : s_gap[j];
-          s_last[j] = t_end;
-          fin[j] = s_rem[j] == 0;
-        } else if ((pqm[j] >> lane) & 1) {
-          s_ctx[j] += q[j];
-          if (s_ctx[j] == s_tgt[j] && s_fd[j] == 0) {  // the full prefill emits a token
-            s_fd[j] = 1;
-            s_last[j] = t_end;
-            L.first[j * 64 + lane] = t_end;
-          }
+    int nfin = 0, base = n_done, l_freed = 0;
+#pragma nounroll
+    for (int j = 0; j < nch; ++j) {
+      Hot h = load_chunk<NCH>(L, h0, j, lane);
+      const int s = j * 64 + lane;
+      const bool act = s < nrun;
+      const bool dec = act && h.ctx >= h.tgt;
+      bool fin = false;
+      if (dec) {
+        h.ctx += 1;
+        h.rem -= 1;
+        h.room -= 1;
+        // consecutive tokens: the gap is this iteration; after a re-prefill
+        // the gap reaches back to the token before the preemption
+        int64_t g = iter_ns;
+        if (h.fl & FL_STALE) {
+          g = t_end - RT[L.id[s]].last;
+          h.fl &= ~FL_STALE;
         }
-        fm[j] = ballot(fin[j]);
-        nfin += popc(fm[j]);
+        h.gap = g > h.gap ? g : h.gap;
+        fin = h.rem == 0;
+      } else if (act && h.q > 0) {
+        h.ctx += h.q;
+        if (h.ctx == h.tgt && !(h.fl & FL_FIRST)) {  // the full prefill emits a token
+          h.fl |= FL_FIRST;
+          RT[L.id[s]].first = t_end;
+        }
+        h.q = 0;
+      }
+      store_chunk<NCH>(L, h0, j, lane, h);
+      const uint64_t fm = ballot(fin);
+      if (fm != 0) {
+        if (fin) {
+          const int id = L.id[s];
+          const int npr = L.npre[s];
+          const ReqTimes rt = RT[id];
+          const int64_t arr = rec[id].arrival_ns;
+          const int64_t tt = rt.first - arr;
+          const int64_t ee = t_end - arr;
+          acc_ttft += tt;
+          acc_e2e += ee;
+          acc_tpot += t_end - rt.first;
+          acc_maxe2e = ee > acc_maxe2e ? ee : acc_maxe2e;
+          acc_last = t_end;
+          if (tt <= A.slo_ttft_ns && h.gap <= A.slo_tpot_ns) acc_slo += 1;
+          acc_dig += record_hash(id, rt.admit, rt.first, t_end, h.gap, npr, TS_REQ_DONE);
+          if (RR) {
+            ts_req_result o;
+            o.admit_ns = rt.admit; o.first_token_ns = rt.first; o.finish_ns = t_end;
+            o.max_gap_ns = h.gap; o.n_preempt = npr; o.status = TS_REQ_DONE;
+            RR[id] = o;
+          }
+          const int pos = base + rank_below(fm);
+          E2E[pos] = ee;
+          TTFT[pos] = tt;
+          l_freed += (h.ctx + h.room) / B;  // held blocks (ctx >= tgt here)
+        }
+        base += popc(fm);
+        nfin += popc(fm);
       }
     }
     if (nfin > 0) {
-      int base = n_done;
-      int l_freed = 0;
-#pragma unroll
-      for (int j = 0; j < NCH; ++j) {
-        if (j < nch) {
-          if (fin[j]) {
-            const int s = j * 64 + lane;
-            const int id = L.id[s];
-            const int npr = L.npre[s];
-            const int64_t admit = L.admit[s];
-            const int64_t first = L.first[s];
-            const int64_t arr = rec[id].arrival_ns;
-            const int64_t tt = first - arr;
-            const int64_t ee = t_end - arr;
-            acc_ttft += tt;
-            acc_e2e += ee;
-            acc_tpot += t_end - first;
-            acc_maxe2e = ee > acc_maxe2e ? ee : acc_maxe2e;
-            acc_last = t_end;
-            if (tt <= A.slo_ttft_ns && s_gap[j] <= A.slo_tpot_ns) acc_slo += 1;
-            acc_dig += record_hash(id, admit, first, t_end, s_gap[j], npr, TS_REQ_DONE);
-            if (RR) {
-              ts_req_result o;
-              o.admit_ns = admit; o.first_token_ns = first; o.finish_ns = t_end;
-              o.max_gap_ns = s_gap[j]; o.n_preempt = npr; o.status = TS_REQ_DONE;
-              RR[id] = o;
-            }
-            const int pos = base + rank_below(fm[j]);
-            E2E[pos] = ee;
-            TTFT[pos] = tt;
-            l_freed += s_alloc[j];
-          }
-          base += popc(fm[j]);
-        }
-      }
       freeb += wsum(l_freed);
       n_done += nfin;
-      // stable compaction of the survivors
-      bool keep[NCH];
-      int pos[NCH];
-      int off = 0;
-#pragma unroll
-      for (int j = 0; j < NCH; ++j) {
-        keep[j] = false;
-        pos[j] = 0;
-        if (j < nch) {
-          keep[j] = act[j] && !fin[j];
-          const uint64_t km = ballot(keep[j]);
-          pos[j] = off + rank_below(km);
-          off += popc(km);
+      // Stable compaction of the survivors through LDS scratch, one field at
+      // a time.  Finished slots have rem == 0; rem moves last so every pass
+      // reads 'keep' from the original slots.
+      const int nsurv = nrun - nfin;
+      const int nch2 = (nsurv + 63) >> 6;
+      int32_t* s32 = reinterpret_cast<int32_t*>(L.u.scratch);
+#pragma nounroll
+      for (int f = 0; f < 8; ++f) {
+        int carry = 0;
+#pragma nounroll
+        for (int j = 0; j < nch; ++j) {
+          const int s = j * 64 + lane;
+          const int e = (j - 1) * 64 + lane;
+          const int rem = j == 0 ? h0.rem : L.x_rem[e];
+          const bool keep = s < nrun && rem > 0;
+          const uint64_t km = ballot(keep);
+          const int pos = carry + rank_below(km);
+          carry += popc(km);
+          if (keep) {
+            switch (f) {
+              case 0: s32[pos] = j == 0 ? h0.ctx : L.x_ctx[e]; break;
+              case 1: s32[pos] = j == 0 ? h0.tgt : L.x_tgt[e]; break;
+              case 2: s32[pos] = j == 0 ? h0.room : L.x_room[e]; break;
+              case 3: s32[pos] = j == 0 ? h0.fl : L.x_fl[e]; break;
+              case 4: s32[pos] = L.id[s]; break;
+              case 5: L.u.scratch[pos] = j == 0 ? h0.gap : L.x_gap[e]; break;
+              case 6: s32[pos] = L.npre[s]; break;
+              default: s32[pos] = rem; break;
+            }
+          }
         }
+        __syncthreads();
+#pragma nounroll
+        for (int j = 0; j < nch2; ++j) {
+          const int s = j * 64 + lane;
+          const int e = (j - 1) * 64 + lane;
+          switch (f) {
+            case 0: if (j == 0) h0.ctx = s32[s]; else L.x_ctx[e] = s32[s]; break;
+            case 1: if (j == 0) h0.tgt = s32[s]; else L.x_tgt[e] = s32[s]; break;
+            case 2: if (j == 0) h0.room = s32[s]; else L.x_room[e] = s32[s]; break;
+            case 3: if (j == 0) h0.fl = s32[s]; else L.x_fl[e] = s32[s]; break;
+            case 4: L.id[s] = s32[s]; break;
+            case 5: if (j == 0) h0.gap = L.u.scratch[s]; else L.x_gap[e] = L.u.scratch[s]; break;
+            case 6: L.npre[s] = s32[s]; break;
+            default: if (j == 0) h0.rem = s32[s]; else L.x_rem[e] = s32[s]; break;
+          }
+        }
+        __syncthreads();
       }
-      int* s32 = reinterpret_cast<int*>(L.u.scratch);
-      compact_reg<NCH, int>(s_ctx, keep, pos, s32, lane, nch);
-      compact_reg<NCH, int>(s_tgt, keep, pos, s32, lane, nch);
-      compact_reg<NCH, int>(s_rem, keep, pos, s32, lane, nch);
-      compact_reg<NCH, int>(s_room, keep, pos, s32, lane, nch);
-      compact_reg<NCH, int>(s_alloc, keep, pos, s32, lane, nch);
-      compact_reg<NCH, int>(s_fd, keep, pos, s32, lane, nch);
-      compact_reg<NCH, int64_t>(s_last, keep, pos, L.u.scratch, lane, nch);
-      compact_reg<NCH, int64_t>(s_gap, keep, pos, L.u.scratch, lane, nch);
-      compact_lds<NCH, int>(L.id, keep, pos, lane, nch);
-      compact_lds<NCH, int>(L.npre, keep, pos, lane, nch);
-      compact_lds<NCH, int64_t>(L.admit, keep, pos, lane, nch);
-      compact_lds<NCH, int64_t>(L.first, keep, pos, lane, nch);
-      nrun -= nfin;
+      nrun = nsurv;
     }
     t = t_end;
   }
@@ -757,7 +752,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
   const int64_t sum_ttft = wsum64(acc_ttft);
   const int64_t sum_e2e = wsum64(acc_e2e);
   const int64_t sum_tpot = wsum64(acc_tpot);
-  const int64_t slo_ok = wsum64(acc_slo);
+  const int slo_ok = wsum(acc_slo);
   const int64_t max_e2e = wmax64_nonneg(acc_maxe2e);
   const int64_t last_fin = wmax64_nonneg(acc_last);
   const uint64_t digest = wsum_u64(acc_dig);
@@ -797,6 +792,7 @@ __global__ __launch_bounds__(64) void sim_kernel(SimArgs A) {
   __shared__ SlotLds<NCH> L;
   const int lane = lane_id();
   QEntry* Q = A.queue + (size_t)blockIdx.x * kQueueCap;
+  ReqTimes* RT = A.times + (size_t)blockIdx.x * (size_t)A.max_n;
   LaneRoof roofc;
   const int cl = lane < 8 ? lane : 7;
   roofc.f = A.lc.f[cl];
@@ -813,7 +809,7 @@ __global__ __launch_bounds__(64) void sim_kernel(SimArgs A) {
     const unsigned old = atomicAdd(A.counter, lane == 0 ? 1u : 0u);
     const int tk = __builtin_amdgcn_readfirstlane((int)old);
     if (tk >= A.n_order) break;
-    simulate_point<NCH>(A, A.order[tk], L, Q, lane, roofc);
+    simulate_point<NCH>(A, A.order[tk], L, Q, RT, lane, roofc);
   }
 }
 

@@ -46,10 +46,17 @@ struct CostCoef {
   double n_layers;
 };
 
-// A request waiting after recompute preemption, 64 bytes.
+// A request waiting after recompute preemption, 32 bytes.
 struct __attribute__((aligned(16))) QEntry {
-  int32_t id, target, rem, n_pre, first_done, pad0, pad1, pad2;
-  int64_t admit, first, last, gap;
+  int32_t id, target, rem, n_pre, flags, pad;
+  int64_t gap;
+};
+
+// Per-request times kept by the workgroup simulating a point, indexed by
+// request: first admission, first token, and the last token before the
+// latest preemption.  Written once per event, read when the request ends.
+struct ReqTimes {
+  int64_t admit, first, last;
 };
 
 // Per-lane roofline coefficients (doubles holding exact integers): lane j < 7
@@ -68,6 +75,7 @@ struct SimArgs {
   int32_t max_n;               // row stride of the per-request buffers
   unsigned int* counter;       // work queue ticket counter (zeroed before launch)
   QEntry* queue;               // kQueueCap entries per workgroup
+  ReqTimes* times;             // max_n entries per workgroup
   ts_point_result* res;
   ts_req_result* req;          // nullptr unless per-request records are requested
   int64_t* e2e;                // max_n per point: end-to-end latency of finished requests
