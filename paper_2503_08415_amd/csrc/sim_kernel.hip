@@ -55,13 +55,18 @@ __device__ __forceinline__ int64_t dpp0_64(int64_t v) {
   const uint32_t hi = (uint32_t)dpp0<CTRL, ROWS>((int)(uint32_t)((uint64_t)v >> 32));
   return (int64_t)(((uint64_t)hi << 32) | lo);
 }
+// Row shift with zero fill (bound_ctrl): every lane is written, no "old".
+template <int CTRL>
+__device__ __forceinline__ int shr0(int v) {
+  return __builtin_amdgcn_mov_dpp(v, CTRL, 0xf, 0xf, true);
+}
 // Inclusive prefix sum over the 64 lanes: Hillis-Steele inside each 16-lane
 // row (row_shr 1, 2, 4, 8), then row 15 -> rows 1,3 and row 31 -> rows 2,3.
 __device__ __forceinline__ int scan_i32(int v) {
-  v += dpp0<0x111, 0xf>(v);
-  v += dpp0<0x112, 0xf>(v);
-  v += dpp0<0x114, 0xf>(v);
-  v += dpp0<0x118, 0xf>(v);
+  v += shr0<0x111>(v);
+  v += shr0<0x112>(v);
+  v += shr0<0x114>(v);
+  v += shr0<0x118>(v);
   v += dpp0<0x142, 0xa>(v);
   v += dpp0<0x143, 0xc>(v);
   return v;
@@ -134,8 +139,8 @@ __device__ __forceinline__ uint64_t record_hash(int64_t idx, int64_t admit, int6
 // lane k adds its term to lane k-1's partial sum.
 __device__ __forceinline__ double dpp_shr1_f64(double v) {
   const uint64_t u = __builtin_bit_cast(uint64_t, v);
-  const uint32_t lo = (uint32_t)dpp0<0x111, 0xf>((int)(uint32_t)u);
-  const uint32_t hi = (uint32_t)dpp0<0x111, 0xf>((int)(uint32_t)(u >> 32));
+  const uint32_t lo = (uint32_t)shr0<0x111>((int)(uint32_t)u);
+  const uint32_t hi = (uint32_t)shr0<0x111>((int)(uint32_t)(u >> 32));
   return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
 }
 __device__ __forceinline__ double rdl_f64(double v, int l) {
@@ -151,16 +156,13 @@ struct LaneRoof {
 __device__ __forceinline__ int64_t iteration_ns(const LaneRoof& c, double n_layers, double iF,
                                                 double iB, int T, int TP, int64_t AP, int CP,
                                                 int nD, int CD, int R, double* iter_d) {
-  const double dT = (double)T;
-  double X = dT, Y = dT, Z = 0.0;
-  X = c.is_attp ? (double)AP : X;
-  Y = c.is_attp ? (double)CP : Y;
-  Z = c.is_attp ? (double)TP : Z;
-  X = c.is_attd ? (double)CD : X;
-  Y = c.is_attd ? (double)CD : Y;
-  Z = c.is_attd ? (double)nD : Z;
-  X = c.is_lm ? (double)R : X;
-  Y = c.is_lm ? (double)R : Y;
+  // operands of this lane's operator, selected as integers, converted once
+  int xi = c.is_attd ? CD : (c.is_lm ? R : T);
+  int yi = c.is_attp ? CP : xi;
+  int zi = c.is_attp ? TP : (c.is_attd ? nD : 0);
+  const double X = c.is_attp ? (double)AP : (double)xi;
+  const double Y = (double)yi;
+  const double Z = (double)zi;
   const double b0 = (c.is_lm && R == 0) ? 0.0 : c.b0;  // no LM head without an emitter
   const double F = c.f * X;
   const double Bv = (b0 + c.b1 * Y) + c.b2 * Z;
@@ -215,6 +217,10 @@ struct SlotLds {
   int32_t x_fl[NX * 64];
   int32_t id[NCH * 64];    // request index per slot
   int32_t npre[NCH * 64];  // times preempted per slot
+  // finished-request statistics of the point, accumulated by LDS atomics
+  unsigned long long sum_ttft, sum_e2e, sum_tpot, digest;
+  long long max_e2e, last_fin;
+  unsigned int slo_ok;
   union {
     StageSlot stage[64];
     int64_t scratch[NCH * 64];
@@ -255,10 +261,11 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
   int64_t* E2E = A.e2e + (size_t)oi * (size_t)A.max_n;
   int64_t* TTFT = A.ttft + (size_t)oi * (size_t)A.max_n;
 
-  // per-lane accumulators of finished / rejected requests
-  int64_t acc_ttft = 0, acc_e2e = 0, acc_tpot = 0, acc_maxe2e = 0, acc_last = 0;
-  int acc_slo = 0;
-  uint64_t acc_dig = 0;
+  // statistics of finished / rejected requests: LDS accumulators, cleared
+  // by every lane storing the same zeros (no lane-dependent branch)
+  L.sum_ttft = 0; L.sum_e2e = 0; L.sum_tpot = 0; L.digest = 0;
+  L.max_e2e = -1; L.last_fin = -1; L.slo_ok = 0;
+  __syncthreads();
   int n_rej = 0;
 
   // Requests that could never fit are rejected up front.
@@ -271,7 +278,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
         rj = (int64_t)r.prompt + (int64_t)r.output > cap_tok;
       }
       if (rj) {
-        acc_dig += record_hash(i, -1, -1, -1, 0, 0, TS_REQ_REJECTED);
+        atomicAdd(&L.digest, (unsigned long long)record_hash(i, -1, -1, -1, 0, 0, TS_REQ_REJECTED));
         if (RR) {
           ts_req_result o;
           o.admit_ns = -1; o.first_token_ns = -1; o.finish_ns = -1; o.max_gap_ns = 0;
@@ -312,42 +319,46 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       status = TS_POINT_TIME_LIMIT;
       break;
     }
-    // ---- 1. intake: every request with arrival <= t joins the waiting set
-    int guard = N / 64 + 2;  // window passes are bounded by the trace length
-    while (next < N && --guard >= 0) {
-      const uint64_t m = ballot(w_arr <= t);  // arrivals are sorted: a lane prefix
-      const int cnt = popc(m);
-      const int nn = wbase + cnt;
-      if (nn > next) {
-        int add = nn - next;
-        if (P.may_reject) {
-          const bool rj = lane >= next - wbase && lane < cnt && (int64_t)w_po > cap_tok;
-          add -= popc(ballot(rj));
+    // ---- 1. intake: every request with arrival <= t joins the waiting set;
+    // ---- 2. when nothing runs or waits, jump to the next arrival
+    bool drained = false;
+    for (;;) {
+      int guard = N / 64 + 2;  // window passes are bounded by the trace length
+      while (next < N && --guard >= 0) {
+        const uint64_t m = ballot(w_arr <= t);  // arrivals are sorted: a lane prefix
+        const int cnt = popc(m);
+        const int nn = wbase + cnt;
+        if (nn > next) {
+          int add = nn - next;
+          if (P.may_reject) {
+            const bool rj = lane >= next - wbase && lane < cnt && (int64_t)w_po > cap_tok;
+            add -= popc(ballot(rj));
+          }
+          if (npre == 0 && nwait == 0) head_need = -1;
+          nwait += add;
+          next = nn;
         }
-        if (npre == 0 && nwait == 0) head_need = -1;
-        nwait += add;
-        next = nn;
-      }
-      if (cnt == 64 && nn < N) {
-        wbase = nn;
-        w_arr = INT64_MAX;
-        w_po = 0;
-        if (wbase + lane < N) {
-          const TraceRec r = rec[wbase + lane];
-          w_arr = r.arrival_ns; w_po = r.prompt + r.output;
+        if (cnt == 64 && nn < N) {
+          wbase = nn;
+          w_arr = INT64_MAX;
+          w_po = 0;
+          if (wbase + lane < N) {
+            const TraceRec r = rec[wbase + lane];
+            w_arr = r.arrival_ns; w_po = r.prompt + r.output;
+          }
+          continue;
         }
-        continue;
+        break;
       }
-      break;
-    }
-    if (nwait == 0) next_new = next;
-
-    // ---- 2. idle: jump to the next arrival, or finish
-    if (nrun == 0 && npre == 0 && nwait == 0) {
-      if (next >= N) break;
+      if (nwait == 0) next_new = next;
+      if (nrun != 0 || npre != 0 || nwait != 0) break;
+      if (next >= N) {
+        drained = true;
+        break;
+      }
       t = rdl64(w_arr, next - wbase);
-      continue;
     }
+    if (drained) break;
     if (n_iters >= A.iter_cap) {
       status = TS_POINT_ITER_LIMIT;
       break;
@@ -669,13 +680,14 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
           const int64_t arr = rec[id].arrival_ns;
           const int64_t tt = rt.first - arr;
           const int64_t ee = t_end - arr;
-          acc_ttft += tt;
-          acc_e2e += ee;
-          acc_tpot += t_end - rt.first;
-          acc_maxe2e = ee > acc_maxe2e ? ee : acc_maxe2e;
-          acc_last = t_end;
-          if (tt <= A.slo_ttft_ns && h.gap <= A.slo_tpot_ns) acc_slo += 1;
-          acc_dig += record_hash(id, rt.admit, rt.first, t_end, h.gap, npr, TS_REQ_DONE);
+          atomicAdd(&L.sum_ttft, (unsigned long long)tt);
+          atomicAdd(&L.sum_e2e, (unsigned long long)ee);
+          atomicAdd(&L.sum_tpot, (unsigned long long)(t_end - rt.first));
+          atomicMax(&L.max_e2e, (long long)ee);
+          atomicMax(&L.last_fin, (long long)t_end);
+          if (tt <= A.slo_ttft_ns && h.gap <= A.slo_tpot_ns) atomicAdd(&L.slo_ok, 1u);
+          atomicAdd(&L.digest, (unsigned long long)record_hash(id, rt.admit, rt.first, t_end,
+                                                               h.gap, npr, TS_REQ_DONE));
           if (RR) {
             ts_req_result o;
             o.admit_ns = rt.admit; o.first_token_ns = rt.first; o.finish_ns = t_end;
@@ -749,13 +761,15 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
   }
 
   // ---- per-point results (percentiles are filled by the statistics kernel)
-  const int64_t sum_ttft = wsum64(acc_ttft);
-  const int64_t sum_e2e = wsum64(acc_e2e);
-  const int64_t sum_tpot = wsum64(acc_tpot);
-  const int slo_ok = wsum(acc_slo);
-  const int64_t max_e2e = wmax64_nonneg(acc_maxe2e);
-  const int64_t last_fin = wmax64_nonneg(acc_last);
-  const uint64_t digest = wsum_u64(acc_dig);
+  __syncthreads();
+  const int64_t sum_ttft = (int64_t)L.sum_ttft;
+  const int64_t sum_e2e = (int64_t)L.sum_e2e;
+  const int64_t sum_tpot = (int64_t)L.sum_tpot;
+  const int slo_ok = (int)L.slo_ok;
+  const int64_t max_e2e = L.max_e2e;
+  const int64_t last_fin = L.last_fin;
+  const uint64_t digest = L.digest;
+  __syncthreads();
   {
     // Every lane stores the same uniform record: no lane-dependent branch
     // next to the work-queue ticket read, which the optimizer could thread
@@ -771,10 +785,10 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
     o.decode_tokens = dec_tok;
     o.peak_used_blocks = peak;
     o.first_arrival_ns = N > 0 ? rec[0].arrival_ns : -1;
-    o.last_finish_ns = n_done > 0 ? last_fin : -1;
+    o.last_finish_ns = last_fin;
     o.sum_ttft_ns = sum_ttft;
     o.sum_e2e_ns = sum_e2e;
-    o.max_e2e_ns = n_done > 0 ? max_e2e : -1;
+    o.max_e2e_ns = max_e2e;
     o.sum_tpot_num_ns = sum_tpot;
     o.p50_e2e_ns = o.p90_e2e_ns = o.p99_e2e_ns = -1;
     o.p50_ttft_ns = o.p99_ttft_ns = -1;
