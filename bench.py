@@ -46,8 +46,45 @@ S_REQ_ITER = 16.0 / 64.0
 KERNEL_NAMES = ("sim_kernel<1>", "sim_kernel<2>", "sim_kernel<4>")
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "sim_kernel_traffic_c5.md")
+# the sources whose change invalidates the recorded traffic counters
+KERNEL_SOURCES = ("paper_2503_08415_amd/csrc/sim_kernel.hip",
+                  "paper_2503_08415_amd/csrc/sweep_internal.h",
+                  "paper_2503_08415_amd/csrc/host.hip")
+
+
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_sources_sha256():
+    import hashlib
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def recorded_traffic(config, kernel):
+    """HBM bytes per launch of ``kernel`` from the committed rocprofv3 FETCH_SIZE /
+    WRITE_SIZE summary, or None when it is missing or the kernel sources have
+    changed since the counters were taken."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            lines = f.read().splitlines()
+    except OSError:
+        return None
+    sha, found = None, None
+    for ln in lines:
+        w = ln.strip().strip("`").split()
+        if len(w) == 2 and w[0] == "sources-sha256:":
+            sha = w[1]
+        if len(w) == 4 and w[0] == "traffic-bytes:" and w[1] == config and w[2] == kernel:
+            found = float(w[3])
+    if sha is None or found is None or sha != kernel_sources_sha256():
+        return None
+    return found
 
 
 def algorithmic_instructions(out):
@@ -95,7 +132,19 @@ def main():
     ap.add_argument("--config", default="c5", choices=["c1", "c2", "c3", "c4", "c5"])
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="wall time budget of the oracle baseline sample (0 = skip)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="only run 8 plain device copies of BYTES bytes (reference for the "
+                         "FETCH_SIZE / WRITE_SIZE traffic counters) and exit")
     args = ap.parse_args()
+    if args.copy_calibration > 0:
+        import torch
+        src = torch.ones(args.copy_calibration, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(8):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": args.copy_calibration, "copies": 8}))
+        return
     if args.gpus != 1:
         print("bench.py runs on one GPU: the sweep's design points are independent and this "
               "build measures one GPU's share; --gpus %d is not supported" % args.gpus,
@@ -155,7 +204,8 @@ def main():
     achieved = w_k / (kmean[k] * 1e-3)
     roofline = {"bound": "alu", "achieved": achieved / 1e9, "peak": VALU_ISSUE_PEAK / 1e9,
                 "unit": "G wave64 VALU instr/s", "frac": achieved / VALU_ISSUE_PEAK,
-                "traffic": None, "kernel": KERNEL_NAMES[k],
+                "traffic": recorded_traffic(args.config, KERNEL_NAMES[k]),
+                "kernel": KERNEL_NAMES[k],
                 "algorithmic_instr": w_k, "kernel_ms": float(kmean[k])}
 
     line = {

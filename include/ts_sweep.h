@@ -193,9 +193,9 @@ int ts_sweep_timing(ts_sweep *h, float *sim_ms, float *stats_ms);
 
 /* Per-kernel device time of the last run.  The points are simulated by up
  * to TS_N_SIM_KERNELS kernels, one per register-chunk class (max_batch
- * <= 64, <= 128, <= 256), which may run concurrently on forked streams.
+ * <= 64, <= 128, <= 256), launched one after another on the run's stream.
  * ms[k] receives kernel k's duration in milliseconds from HIP events
- * recorded on the stream it ran on (0 when the class has no points) and
+ * recorded around it on that stream (0 when the class has no points) and
  * n_points[k] its number of points.  Waits for the run.  TS_ERR_STATE
  * before the first run. */
 #define TS_N_SIM_KERNELS 3

@@ -4,8 +4,9 @@
 // point's block budget and reciprocals, checks that every cost-model integer
 // stays exact in fp64, orders the points longest-expected-first and uploads
 // traces and points.  ts_sweep_run enqueues the simulation kernels (one
-// per register-chunk class, on forked streams so their tails overlap) and
-// the statistics kernel.  ts_sweep_results copies the results back.
+// per register-chunk class, back to back on the caller's stream: each fills
+// the whole GPU with persistent workgroups, so running them concurrently
+// gains nothing) and the statistics kernel.  ts_sweep_results copies the results back.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -179,8 +180,8 @@ struct ts_sweep {
   DevPoint* d_points = nullptr;
   int32_t* d_order = nullptr;       // all classes, concatenated
   unsigned int* d_counter = nullptr;
-  QEntry* d_queue[kClasses] = {nullptr, nullptr, nullptr};
-  ReqTimes* d_times[kClasses] = {nullptr, nullptr, nullptr};
+  QEntry* d_queue = nullptr;        // kQueueCap per workgroup, shared by the classes
+  ReqTimes* d_times = nullptr;      // max_n per workgroup, shared by the classes
   ts_point_result* d_res = nullptr;
   ts_req_result* d_req = nullptr;
   int64_t* d_e2e = nullptr;
@@ -188,8 +189,6 @@ struct ts_sweep {
   int class_off[kClasses] = {0, 0, 0}, class_n[kClasses] = {0, 0, 0};
   int grid[kClasses] = {0, 0, 0};
   int stats_grid = 0;
-  hipStream_t side[kClasses] = {nullptr, nullptr, nullptr};
-  hipEvent_t ev_fork = nullptr, ev_join[kClasses] = {nullptr, nullptr, nullptr};
   hipEvent_t ev_t0 = nullptr, ev_t1 = nullptr, ev_t2 = nullptr;
   hipEvent_t ev_k0[kClasses] = {nullptr, nullptr, nullptr};
   hipEvent_t ev_k1[kClasses] = {nullptr, nullptr, nullptr};
@@ -205,19 +204,16 @@ void release(ts_sweep* h) {
   (void)hipFree(h->d_points);
   (void)hipFree(h->d_order);
   (void)hipFree(h->d_counter);
-  for (int c = 0; c < kClasses; ++c) (void)hipFree(h->d_queue[c]);
-  for (int c = 0; c < kClasses; ++c) (void)hipFree(h->d_times[c]);
+  (void)hipFree(h->d_queue);
+  (void)hipFree(h->d_times);
   (void)hipFree(h->d_res);
   (void)hipFree(h->d_req);
   (void)hipFree(h->d_e2e);
   (void)hipFree(h->d_ttft);
   for (int c = 0; c < kClasses; ++c) {
-    if (h->side[c]) (void)hipStreamDestroy(h->side[c]);
-    if (h->ev_join[c]) (void)hipEventDestroy(h->ev_join[c]);
     if (h->ev_k0[c]) (void)hipEventDestroy(h->ev_k0[c]);
     if (h->ev_k1[c]) (void)hipEventDestroy(h->ev_k1[c]);
   }
-  if (h->ev_fork) (void)hipEventDestroy(h->ev_fork);
   if (h->ev_t0) (void)hipEventDestroy(h->ev_t0);
   if (h->ev_t1) (void)hipEventDestroy(h->ev_t1);
   if (h->ev_t2) (void)hipEventDestroy(h->ev_t2);
@@ -418,11 +414,9 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
   if (ae == hipSuccess) ae = dev_alloc(&h->d_points, dp.size());
   if (ae == hipSuccess) ae = dev_alloc(&h->d_order, order.size());
   if (ae == hipSuccess) ae = dev_alloc(&h->d_counter, (size_t)kClasses);
-  for (int c = 0; c < kClasses && ae == hipSuccess; ++c) {
-    if (h->grid[c] == 0) continue;
-    ae = dev_alloc(&h->d_queue[c], (size_t)h->grid[c] * kQueueCap);
-    if (ae == hipSuccess) ae = dev_alloc(&h->d_times[c], (size_t)h->grid[c] * per_point);
-  }
+  const int max_grid = std::max(1, *std::max_element(h->grid, h->grid + kClasses));
+  if (ae == hipSuccess) ae = dev_alloc(&h->d_queue, (size_t)max_grid * kQueueCap);
+  if (ae == hipSuccess) ae = dev_alloc(&h->d_times, (size_t)max_grid * per_point);
   if (ae == hipSuccess) ae = dev_alloc(&h->d_res, (size_t)count);
   if (ae == hipSuccess) ae = dev_alloc(&h->d_e2e, (size_t)count * per_point);
   if (ae == hipSuccess) ae = dev_alloc(&h->d_ttft, (size_t)count * per_point);
@@ -442,12 +436,9 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
                   hipMemcpyHostToDevice);
   if (e != hipSuccess) { release(h); return device_error(e, "upload"); }
   for (int c = 0; c < kClasses && e == hipSuccess; ++c) {
-    e = hipStreamCreateWithFlags(&h->side[c], hipStreamNonBlocking);
-    if (e == hipSuccess) e = hipEventCreateWithFlags(&h->ev_join[c], hipEventDisableTiming);
-    if (e == hipSuccess) e = hipEventCreate(&h->ev_k0[c]);
+    e = hipEventCreate(&h->ev_k0[c]);
     if (e == hipSuccess) e = hipEventCreate(&h->ev_k1[c]);
   }
-  if (e == hipSuccess) e = hipEventCreateWithFlags(&h->ev_fork, hipEventDisableTiming);
   if (e == hipSuccess) e = hipEventCreate(&h->ev_t0);
   if (e == hipSuccess) e = hipEventCreate(&h->ev_t1);
   if (e == hipSuccess) e = hipEventCreate(&h->ev_t2);
@@ -467,12 +458,6 @@ int ts_sweep_run(ts_sweep* h, void* hip_stream) {
     const int blocks = (int)std::min<size_t>((n + 255) / 256, 65536);
     fill_pending_kernel<<<std::max(blocks, 1), 256, 0, s>>>(h->d_req, n);
   }
-  int used = 0;
-  for (int c = 0; c < kClasses; ++c) used += h->class_n[c] > 0;
-  if (used > 1) {
-    e = hipEventRecord(h->ev_fork, s);
-    if (e != hipSuccess) return device_error(e, "event record");
-  }
   for (int c = 0; c < kClasses; ++c) {
     if (h->class_n[c] == 0) continue;
     SimArgs a;
@@ -482,8 +467,8 @@ int ts_sweep_run(ts_sweep* h, void* hip_stream) {
     a.n_order = h->class_n[c];
     a.max_n = h->max_n;
     a.counter = h->d_counter + c;
-    a.queue = h->d_queue[c];
-    a.times = h->d_times[c];
+    a.queue = h->d_queue;
+    a.times = h->d_times;
     a.res = h->d_res;
     a.req = h->d_req;
     a.e2e = h->d_e2e;
@@ -495,11 +480,6 @@ int ts_sweep_run(ts_sweep* h, void* hip_stream) {
     a.n_layers = h->coef.n_layers;
     a.lc = h->lc;
     hipStream_t ks = s;
-    if (used > 1) {
-      ks = h->side[c];
-      e = hipStreamWaitEvent(ks, h->ev_fork, 0);
-      if (e != hipSuccess) return device_error(e, "stream wait");
-    }
     e = hipEventRecord(h->ev_k0[c], ks);
     if (e != hipSuccess) return device_error(e, "event record");
     if (kClassChunks[c] == 1) sim_kernel<1><<<h->grid[c], 64, 0, ks>>>(a);
@@ -509,11 +489,6 @@ int ts_sweep_run(ts_sweep* h, void* hip_stream) {
     if (e != hipSuccess) return device_error(e, "sim kernel launch");
     e = hipEventRecord(h->ev_k1[c], ks);
     if (e != hipSuccess) return device_error(e, "event record");
-    if (used > 1) {
-      e = hipEventRecord(h->ev_join[c], ks);
-      if (e == hipSuccess) e = hipStreamWaitEvent(s, h->ev_join[c], 0);
-      if (e != hipSuccess) return device_error(e, "stream join");
-    }
   }
   e = hipEventRecord(h->ev_t1, s);
   if (e != hipSuccess) return device_error(e, "event record");
