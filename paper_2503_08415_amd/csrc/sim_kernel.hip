@@ -91,6 +91,17 @@ __device__ __forceinline__ int64_t scan_max_i64(int64_t v) {
   u = dpp0_64<0x143, 0xc>(v); v = u > v ? u : v;
   return v;
 }
+// Inclusive prefix max of non-negative 32-bit values (0 is the identity).
+__device__ __forceinline__ int scan_max_i32(int v) {
+  int u;
+  u = shr0<0x111>(v); v = u > v ? u : v;
+  u = shr0<0x112>(v); v = u > v ? u : v;
+  u = shr0<0x114>(v); v = u > v ? u : v;
+  u = shr0<0x118>(v); v = u > v ? u : v;
+  u = dpp0<0x142, 0xa>(v); v = u > v ? u : v;
+  u = dpp0<0x143, 0xc>(v); v = u > v ? u : v;
+  return v;
+}
 // Wrapping (mod 2^64) sum over the lanes, for hashes.
 __device__ __forceinline__ uint64_t wsum_u64(uint64_t v) {
   v += (uint64_t)dpp0_64<0x111, 0xf>((int64_t)v);
@@ -143,6 +154,13 @@ __device__ __forceinline__ double dpp_shr1_f64(double v) {
   const uint32_t hi = (uint32_t)shr0<0x111>((int)(uint32_t)(u >> 32));
   return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
 }
+// lane i <- lane i + 1 within each 16-lane row
+__device__ __forceinline__ double dpp_shl1_f64(double v) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, v);
+  const uint32_t lo = (uint32_t)shr0<0x101>((int)(uint32_t)u);
+  const uint32_t hi = (uint32_t)shr0<0x101>((int)(uint32_t)(u >> 32));
+  return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
 __device__ __forceinline__ double rdl_f64(double v, int l) {
   return __builtin_bit_cast(double, (uint64_t)rdl64((int64_t)__builtin_bit_cast(uint64_t, v), l));
 }
@@ -152,10 +170,9 @@ struct LaneRoof {
   bool is_attp, is_attd, is_lm;
 };
 
-// Returns max(1, ceil(L * layer_sum + lm_head)) and the same value as a double.
-__device__ __forceinline__ int64_t iteration_ns(const LaneRoof& c, double n_layers, double iF,
-                                                double iB, int T, int TP, int64_t AP, int CP,
-                                                int nD, int CD, int R, double* iter_d) {
+// This lane's operator FLOPs F and bytes B for the batch sums (exact integers).
+__device__ __forceinline__ void lane_work(const LaneRoof& c, int T, int TP, int64_t AP, int CP,
+                                          int nD, int CD, int R, double* F, double* Bv) {
   // operands of this lane's operator, selected as integers, converted once
   int xi = c.is_attd ? CD : (c.is_lm ? R : T);
   int yi = c.is_attp ? CP : xi;
@@ -164,8 +181,16 @@ __device__ __forceinline__ int64_t iteration_ns(const LaneRoof& c, double n_laye
   const double Y = (double)yi;
   const double Z = (double)zi;
   const double b0 = (c.is_lm && R == 0) ? 0.0 : c.b0;  // no LM head without an emitter
-  const double F = c.f * X;
-  const double Bv = (b0 + c.b1 * Y) + c.b2 * Z;
+  *F = c.f * X;
+  *Bv = (b0 + c.b1 * Y) + c.b2 * Z;
+}
+
+// Returns max(1, ceil(L * layer_sum + lm_head)) and the same value as a double.
+__device__ __forceinline__ int64_t iteration_ns(const LaneRoof& c, double n_layers, double iF,
+                                                double iB, int T, int TP, int64_t AP, int CP,
+                                                int nD, int CD, int R, double* iter_d) {
+  double F, Bv;
+  lane_work(c, T, TP, AP, CP, nD, CD, R, &F, &Bv);
   const double tf = F * iF;
   const double tb = Bv * iB;
   const double t = tf > tb ? tf : tb;
@@ -311,8 +336,200 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
   h0.ctx = h0.tgt = h0.rem = h0.room = h0.fl = h0.q = 0;
   h0.gap = 0;
 
+  // intake: every request with arrival <= t joins the waiting set
+  auto intake = [&]() {
+    int guard = N / 64 + 2;  // window passes are bounded by the trace length
+    while (next < N && --guard >= 0) {
+      const uint64_t m = ballot(w_arr <= t);  // arrivals are sorted: a lane prefix
+      const int cnt = popc(m);
+      const int nn = wbase + cnt;
+      if (nn > next) {
+        int add = nn - next;
+        if (P.may_reject) {
+          const bool rj = lane >= next - wbase && lane < cnt && (int64_t)w_po > cap_tok;
+          add -= popc(ballot(rj));
+        }
+        if (npre == 0 && nwait == 0) head_need = -1;
+        nwait += add;
+        next = nn;
+      }
+      if (cnt == 64 && nn < N) {
+        wbase = nn;
+        w_arr = INT64_MAX;
+        w_po = 0;
+        if (wbase + lane < N) {
+          const TraceRec r = rec[wbase + lane];
+          w_arr = r.arrival_ns; w_po = r.prompt + r.output;
+        }
+        continue;
+      }
+      break;
+    }
+    if (nwait == 0) next_new = next;
+  };
+
   const uint64_t clock0 = A.time_limit_ticks ? __builtin_amdgcn_s_memrealtime() : 0;
   while (status == TS_POINT_OK) {
+    // ---- 0. steady stretch.  As long as no request is admitted, preempted
+    // or finishes and no prefill completes, an iteration advances every
+    // decode by one token and the head prefill by the whole remaining chunk
+    // budget, so every batch sum moves by a fixed integer per iteration.
+    // Such iterations keep the decodes' slot state lazily (materialised when
+    // the stretch ends: tokens and the per-request gap by the iteration
+    // count, block boundaries by a countdown per slot) and step the two
+    // attention operators' FLOPs and bytes by exact integer increments; the
+    // other operators' times are constant.  Decodes hold slots [0, nD) and
+    // prefills the slots after them: prefills receive tokens in slot order,
+    // so they complete in slot order.
+    if (nrun > 0) {
+      const int nch0 = ((nrun + 63) >> 6) < NCH ? ((nrun + 63) >> 6) : NCH;
+      int nD = 0;
+      bool go = true;
+      int rr[NCH];  // decode slots: room + B * (blocks taken) in this stretch
+#pragma unroll
+      for (int j = 0; j < NCH; ++j) {
+        rr[j] = -0x40000000;  // never equal to an iteration count
+        if (j < nch0) {
+          const Hot h = load_chunk<NCH>(L, h0, j, lane);
+          const bool dec = (j * 64 + lane) < nrun && h.ctx >= h.tgt;
+          nD += popc(ballot(dec));
+          if (ballot(dec && ((h.fl & FL_STALE) != 0 || h.rem == 1)) != 0) go = false;
+          rr[j] = dec ? h.room : -0x40000000;
+        }
+      }
+      const int npf = nrun - nD;
+      if (npf > 0 && unlimited) go = false;
+      const int R0 = unlimited ? 0 : K - nD;  // chunk budget left after the decodes
+      const int q = npf > 0 ? R0 : 0;         // the head prefill's tokens per iteration
+      const bool adm_budget = unlimited || (npf == 0 && R0 > 0);
+      int ctx_p = 0, tgt_p = 0;
+      if (go && npf > 0) {
+        const int jp = nD >> 6, lp = nD & 63;
+        if (NCH == 1 || jp == 0) {
+          ctx_p = rdl(h0.ctx, lp);
+          tgt_p = rdl(h0.tgt, lp);
+        } else {
+          ctx_p = __builtin_amdgcn_readfirstlane(L.x_ctx[(jp - 1) * 64 + lp]);
+          tgt_p = __builtin_amdgcn_readfirstlane(L.x_tgt[(jp - 1) * 64 + lp]);
+        }
+      }
+      const int nchd = (nD + 63) >> 6;
+      int64_t nxt_arr = next < N ? rdl64(w_arr, next - wbase) : INT64_MAX;
+      int dG = 0, minrem = 0x7fffffff;
+      double Fw = 0.0, Bw = 0.0, dF = 0.0, dB = 0.0, emax = 0.0;
+      double c_t0 = 0.0, c_t3 = 0.0, c_t4 = 0.0, c_t5 = 0.0, c_lm = 0.0;
+      while (go) {
+        if (n_iters >= A.iter_cap) break;
+        if (A.time_limit_ticks != 0 && (n_iters & 255) == 0) break;  // watchdog below
+        if (next < N && nxt_arr <= t) {
+          intake();
+          nxt_arr = next < N ? rdl64(w_arr, next - wbase) : INT64_MAX;
+        }
+        if (minrem - dG == 1) break;                // a decode finishes
+        if (npf > 0 && tgt_p - ctx_p <= R0) break;  // the head prefill completes
+        int nneed = 0;
+#pragma unroll
+        for (int j = 0; j < NCH; ++j)
+          if (j < nchd) nneed += popc(ballot(rr[j] == dG));
+        if (nneed > freeb) break;                   // recompute preemption
+        const int fb = freeb - nneed;
+        if ((npre > 0 || nwait > 0) && nrun < M && adm_budget &&
+            !(head_need >= 0 && head_need > fb))
+          break;                                    // an admission may happen
+        if (dG == 0) {
+          // set-up: the decodes' smallest remaining count, their key sum, and
+          // every operator's work at this iteration with its per-iteration step
+          int mx = 0, cd = 0;
+#pragma unroll
+          for (int j = 0; j < NCH; ++j) {
+            if (j < nchd) {
+              const Hot h = load_chunk<NCH>(L, h0, j, lane);
+              const bool dec = (j * 64 + lane) < nD;
+              const int m = rdl(scan_max_i32(dec ? 0x7fffffff - h.rem : 0), 63);
+              mx = m > mx ? m : mx;
+              cd += wsum(dec ? h.ctx + 1 : 0);
+            }
+          }
+          minrem = 0x7fffffff - mx;
+          const int64_t AP0 = (int64_t)q * ctx_p + ((int64_t)q * (q + 1)) / 2;
+          lane_work(roofc, nD + q, q, AP0, q > 0 ? ctx_p + q : 0, nD, cd, nD, &Fw, &Bw);
+          const double dX = roofc.is_attp ? (double)((int64_t)q * q)
+                                          : (roofc.is_attd ? (double)nD : 0.0);
+          const double dY = roofc.is_attp ? (double)q : (roofc.is_attd ? (double)nD : 0.0);
+          dF = roofc.f * dX;
+          dB = roofc.b1 * dY;
+          const double tf = Fw * iF, tb = Bw * iB;
+          const double tl = tf > tb ? tf : tb;
+          c_t0 = rdl_f64(tl, 0);
+          c_t3 = rdl_f64(tl, 3);
+          c_t4 = rdl_f64(tl, 4);
+          c_t5 = rdl_f64(tl, 5);
+          c_lm = rdl_f64(tl, 6);
+        }
+        freeb = fb;
+        if (nneed > 0) {
+#pragma unroll
+          for (int j = 0; j < NCH; ++j)
+            if (j < nchd) rr[j] = rr[j] == dG ? rr[j] + B : rr[j];
+        }
+        // prefill attention on lane 1, decode attention on lane 2 (moved to
+        // lane 1), then the layer sum in the fixed operator order
+        const double tf = Fw * iF, tb = Bw * iB;
+        const double tl = tf > tb ? tf : tb;
+        const double t2 = dpp_shl1_f64(tl);
+        double lay = c_t0 + tl;
+        lay = lay + t2;
+        lay = lay + c_t3;
+        lay = lay + c_t4;
+        lay = lay + c_t5;
+        double tot = A.n_layers * lay;
+        tot = tot + c_lm;
+        double it = ceil(tot);
+        it = it < 1.0 ? 1.0 : it;
+        const double iter_d = rdl_f64(it, 1);
+        const int64_t iter_ns = rdl64((int64_t)it, 1);
+        const int used = NB - freeb;
+        if (used > peak) peak = used;
+        ubns = ubns + (double)used * iter_d;
+        ++n_iters;
+        pf_tok += q;
+        dec_tok += nD;
+        ctx_p += q;
+        emax = iter_d > emax ? iter_d : emax;
+        Fw = Fw + dF;
+        Bw = Bw + dB;
+        t = t + iter_ns;
+        ++dG;
+      }
+      if (dG > 0) {
+        // materialise the decodes and the head prefill
+        const int64_t gx = (int64_t)emax;
+#pragma unroll
+        for (int j = 0; j < NCH; ++j) {
+          if (j < nchd) {
+            const bool dec = (j * 64 + lane) < nD;
+            if (j == 0) {
+              h0.ctx = dec ? h0.ctx + dG : h0.ctx;
+              h0.rem = dec ? h0.rem - dG : h0.rem;
+              h0.room = dec ? rr[0] - dG : h0.room;
+              h0.gap = dec && gx > h0.gap ? gx : h0.gap;
+            } else {
+              const int e = (j - 1) * 64 + lane;
+              const int64_t g = L.x_gap[e];
+              L.x_ctx[e] = dec ? L.x_ctx[e] + dG : L.x_ctx[e];
+              L.x_rem[e] = dec ? L.x_rem[e] - dG : L.x_rem[e];
+              L.x_room[e] = dec ? rr[j] - dG : L.x_room[e];
+              L.x_gap[e] = dec && gx > g ? gx : g;
+            }
+          }
+        }
+        if (q > 0) {
+          const int jp = nD >> 6, lp = nD & 63;
+          if (NCH == 1 || jp == 0) h0.ctx = lane == lp ? ctx_p : h0.ctx;
+          else L.x_ctx[(jp - 1) * 64 + lp] = ctx_p;  // every lane stores the same value
+        }
+      }
+    }
     // watchdog: a point running longer than the wall-clock limit stops
     if (A.time_limit_ticks != 0 && (n_iters & 255) == 0 &&
         __builtin_amdgcn_s_memrealtime() - clock0 > A.time_limit_ticks) {
@@ -323,34 +540,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
     // ---- 2. when nothing runs or waits, jump to the next arrival
     bool drained = false;
     for (;;) {
-      int guard = N / 64 + 2;  // window passes are bounded by the trace length
-      while (next < N && --guard >= 0) {
-        const uint64_t m = ballot(w_arr <= t);  // arrivals are sorted: a lane prefix
-        const int cnt = popc(m);
-        const int nn = wbase + cnt;
-        if (nn > next) {
-          int add = nn - next;
-          if (P.may_reject) {
-            const bool rj = lane >= next - wbase && lane < cnt && (int64_t)w_po > cap_tok;
-            add -= popc(ballot(rj));
-          }
-          if (npre == 0 && nwait == 0) head_need = -1;
-          nwait += add;
-          next = nn;
-        }
-        if (cnt == 64 && nn < N) {
-          wbase = nn;
-          w_arr = INT64_MAX;
-          w_po = 0;
-          if (wbase + lane < N) {
-            const TraceRec r = rec[wbase + lane];
-            w_arr = r.arrival_ns; w_po = r.prompt + r.output;
-          }
-          continue;
-        }
-        break;
-      }
-      if (nwait == 0) next_new = next;
+      intake();
       if (nrun != 0 || npre != 0 || nwait != 0) break;
       if (next >= N) {
         drained = true;
