@@ -222,6 +222,8 @@ def main():
         "simulation_phase_ms": float(np.mean(sim_ms)), "statistics_ms": float(np.mean(stats_ms)),
         "results_copy_ms": 1e3 * results_s,
         "simulated_iterations": int(out["n_iters"].sum()),
+        "simulated_iterations_by_kernel": {KERNEL_NAMES[i]: int(out["n_iters"][cls == i].sum())
+                                           for i in range(3) if (cls == i).any()},
         "point_status_counts": status,
     }
     if args.cpu_seconds > 0:

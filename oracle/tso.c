@@ -169,7 +169,10 @@ int64_t tso_iter_ns(const tso_model *m, double iF, double iB, int32_t n, const i
 }
 
 /* ------------------------------------------------------------ record hash
- * MurmurHash3's 64-bit finaliser (fmix64) chained over the record fields. */
+ * The digest is this library's own checksum of the per-request records (the
+ * paper defines none): a multilinear combination of the record's fields with
+ * fixed odd 64-bit multipliers, wrapped mod 2^64, then MurmurHash3's 64-bit
+ * finaliser (fmix64). */
 static uint64_t fmix64(uint64_t k) {
   k ^= k >> 33;
   k *= 0xff51afd7ed558ccdULL;
@@ -180,13 +183,14 @@ static uint64_t fmix64(uint64_t k) {
 }
 
 uint64_t tso_record_hash(int64_t index, const tso_req *r) {
-  uint64_t h = fmix64((uint64_t)index + 0x9e3779b97f4a7c15ULL);
-  h = fmix64(h ^ (uint64_t)r->admit_ns);
-  h = fmix64(h ^ (uint64_t)r->first_token_ns);
-  h = fmix64(h ^ (uint64_t)r->finish_ns);
-  h = fmix64(h ^ (uint64_t)r->max_gap_ns);
-  h = fmix64(h ^ (((uint64_t)(uint32_t)r->n_preempt << 32) | (uint32_t)r->status));
-  return h;
+  const uint64_t tail = ((uint64_t)(uint32_t)r->n_preempt << 32) | (uint32_t)r->status;
+  uint64_t h = (uint64_t)index * 0x9e3779b97f4a7c15ULL;
+  h += (uint64_t)r->admit_ns * 0xbf58476d1ce4e5b9ULL;
+  h += (uint64_t)r->first_token_ns * 0x94d049bb133111ebULL;
+  h += (uint64_t)r->finish_ns * 0xd6e8feb86659fd93ULL;
+  h += (uint64_t)r->max_gap_ns * 0xa0761d6478bd642fULL;
+  h += tail * 0xe7037ed1a0b428dbULL;
+  return fmix64(h);
 }
 
 /* ------------------------------------------------------------ simulation */

@@ -117,7 +117,8 @@ __device__ __forceinline__ int64_t wsum64(int64_t v) { return rdl64(scan_i64(v),
 __device__ __forceinline__ int64_t wmax64_nonneg(int64_t v) { return rdl64(scan_max_i64(v), 63); }
 
 // ------------------------------------------------------------ record hash
-// MurmurHash3's 64-bit finaliser chained over a request record.
+// Checksum of a request record: the fields times fixed odd 64-bit constants,
+// summed mod 2^64, then MurmurHash3's 64-bit finaliser.
 __device__ __forceinline__ uint64_t fmix64(uint64_t k) {
   k ^= k >> 33;
   k *= 0xff51afd7ed558ccdULL;
@@ -129,13 +130,13 @@ __device__ __forceinline__ uint64_t fmix64(uint64_t k) {
 __device__ __forceinline__ uint64_t record_hash(int64_t idx, int64_t admit, int64_t first,
                                                 int64_t finish, int64_t gap, int32_t npre,
                                                 int32_t status) {
-  uint64_t h = fmix64((uint64_t)idx + 0x9e3779b97f4a7c15ULL);
-  h = fmix64(h ^ (uint64_t)admit);
-  h = fmix64(h ^ (uint64_t)first);
-  h = fmix64(h ^ (uint64_t)finish);
-  h = fmix64(h ^ (uint64_t)gap);
-  h = fmix64(h ^ (((uint64_t)(uint32_t)npre << 32) | (uint32_t)status));
-  return h;
+  uint64_t h = (uint64_t)idx * 0x9e3779b97f4a7c15ULL;
+  h += (uint64_t)admit * 0xbf58476d1ce4e5b9ULL;
+  h += (uint64_t)first * 0x94d049bb133111ebULL;
+  h += (uint64_t)finish * 0xd6e8feb86659fd93ULL;
+  h += (uint64_t)gap * 0xa0761d6478bd642fULL;
+  h += (((uint64_t)(uint32_t)npre << 32) | (uint32_t)status) * 0xe7037ed1a0b428dbULL;
+  return fmix64(h);
 }
 
 // ------------------------------------------------------------ roofline
@@ -193,7 +194,7 @@ __device__ __forceinline__ int64_t iteration_ns(const LaneRoof& c, double n_laye
   lane_work(c, T, TP, AP, CP, nD, CD, R, &F, &Bv);
   const double tf = F * iF;
   const double tb = Bv * iB;
-  const double t = tf > tb ? tf : tb;
+  const double t = __builtin_fmax(tf, tb);  // both finite and >= 0
   double s = t;
   s = dpp_shr1_f64(s) + t;  // lane 1: t0 + t1
   s = dpp_shr1_f64(s) + t;  // lane 2: (t0 + t1) + t2
@@ -204,8 +205,7 @@ __device__ __forceinline__ int64_t iteration_ns(const LaneRoof& c, double n_laye
   const double lm = rdl_f64(t, 6);
   double total = n_layers * layer;
   total = total + lm;
-  double it = ceil(total);
-  it = it < 1.0 ? 1.0 : it;
+  const double it = __builtin_fmax(ceil(total), 1.0);
   *iter_d = it;
   return (int64_t)it;
 }
@@ -458,8 +458,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
           const double dY = roofc.is_attp ? (double)q : (roofc.is_attd ? (double)nD : 0.0);
           dF = roofc.f * dX;
           dB = roofc.b1 * dY;
-          const double tf = Fw * iF, tb = Bw * iB;
-          const double tl = tf > tb ? tf : tb;
+          const double tl = __builtin_fmax(Fw * iF, Bw * iB);
           c_t0 = rdl_f64(tl, 0);
           c_t3 = rdl_f64(tl, 3);
           c_t4 = rdl_f64(tl, 4);
@@ -474,8 +473,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
         }
         // prefill attention on lane 1, decode attention on lane 2 (moved to
         // lane 1), then the layer sum in the fixed operator order
-        const double tf = Fw * iF, tb = Bw * iB;
-        const double tl = tf > tb ? tf : tb;
+        const double tl = __builtin_fmax(Fw * iF, Bw * iB);
         const double t2 = dpp_shl1_f64(tl);
         double lay = c_t0 + tl;
         lay = lay + t2;
@@ -484,8 +482,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
         lay = lay + c_t5;
         double tot = A.n_layers * lay;
         tot = tot + c_lm;
-        double it = ceil(tot);
-        it = it < 1.0 ? 1.0 : it;
+        const double it = __builtin_fmax(ceil(tot), 1.0);
         const double iter_d = rdl_f64(it, 1);
         const int64_t iter_ns = rdl64((int64_t)it, 1);
         const int used = NB - freeb;
@@ -495,7 +492,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
         pf_tok += q;
         dec_tok += nD;
         ctx_p += q;
-        emax = iter_d > emax ? iter_d : emax;
+        emax = __builtin_fmax(iter_d, emax);
         Fw = Fw + dF;
         Bw = Bw + dB;
         t = t + iter_ns;
@@ -896,6 +893,30 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
     if (nfin > 0) {
       freeb += wsum(l_freed);
       n_done += nfin;
+      const int nsurv = nrun - nfin;
+      if (nrun <= 64) {
+        // One chunk: every lane pushes its slot through the LDS crossbar to
+        // its new lane, survivors first in slot order, then the others.
+        const bool keep = lane < nrun && h0.rem > 0;
+        const uint64_t km = ballot(keep);
+        const int ad = (keep ? rank_below(km) : nsurv + rank_below(~km)) << 2;
+        h0.ctx = __builtin_amdgcn_ds_permute(ad, h0.ctx);
+        h0.tgt = __builtin_amdgcn_ds_permute(ad, h0.tgt);
+        h0.rem = __builtin_amdgcn_ds_permute(ad, h0.rem);
+        h0.room = __builtin_amdgcn_ds_permute(ad, h0.room);
+        h0.fl = __builtin_amdgcn_ds_permute(ad, h0.fl);
+        const uint32_t glo = (uint32_t)__builtin_amdgcn_ds_permute(ad, (int)(uint32_t)h0.gap);
+        const uint32_t ghi =
+            (uint32_t)__builtin_amdgcn_ds_permute(ad, (int)(uint32_t)((uint64_t)h0.gap >> 32));
+        h0.gap = (int64_t)(((uint64_t)ghi << 32) | glo);
+        const int idv = __builtin_amdgcn_ds_permute(ad, L.id[lane]);
+        const int npv = __builtin_amdgcn_ds_permute(ad, L.npre[lane]);
+        L.id[lane] = idv;
+        L.npre[lane] = npv;
+        nrun = nsurv;
+      }
+    }
+    if (nfin > 0 && nrun > 64) {
       // Stable compaction of the survivors through LDS scratch, one field at
       // a time.  Finished slots have rem == 0; rem moves last so every pass
       // reads 'keep' from the original slots.

@@ -214,11 +214,13 @@ def test_digest_definition(oracle):
         for idx, r in enumerate(req):
             if r["status"] == 0:
                 continue
-            h = _fmix64((idx + 0x9e3779b97f4a7c15) & M)
-            for f in ("admit_ns", "first_token_ns", "finish_ns", "max_gap_ns"):
-                h = _fmix64(h ^ (int(r[f]) & M))
-            h = _fmix64(h ^ (((int(r["n_preempt"]) & 0xffffffff) << 32) | int(r["status"])))
-            acc = (acc + h) & M
+            tail = ((int(r["n_preempt"]) & 0xffffffff) << 32) | int(r["status"])
+            fields = (idx, int(r["admit_ns"]), int(r["first_token_ns"]), int(r["finish_ns"]),
+                      int(r["max_gap_ns"]), tail)
+            mult = (0x9e3779b97f4a7c15, 0xbf58476d1ce4e5b9, 0x94d049bb133111eb,
+                    0xd6e8feb86659fd93, 0xa0761d6478bd642f, 0xe7037ed1a0b428db)
+            h = sum((v & M) * k for v, k in zip(fields, mult)) & M
+            acc = (acc + _fmix64(h)) & M
         assert int(out["digest"]) == acc
 
 
