@@ -155,11 +155,13 @@ __device__ __forceinline__ double dpp_shr1_f64(double v) {
   const uint32_t hi = (uint32_t)shr0<0x111>((int)(uint32_t)(u >> 32));
   return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
 }
-// lane i <- lane i + 1 within each 16-lane row
-__device__ __forceinline__ double dpp_shl1_f64(double v) {
+// Row shift of a double (zero fill): CTRL 0x100 + k takes lane i + k,
+// 0x110 + k lane i - k, within each 16-lane row.
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double v) {
   const uint64_t u = __builtin_bit_cast(uint64_t, v);
-  const uint32_t lo = (uint32_t)shr0<0x101>((int)(uint32_t)u);
-  const uint32_t hi = (uint32_t)shr0<0x101>((int)(uint32_t)(u >> 32));
+  const uint32_t lo = (uint32_t)shr0<CTRL>((int)(uint32_t)u);
+  const uint32_t hi = (uint32_t)shr0<CTRL>((int)(uint32_t)(u >> 32));
   return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
 }
 __device__ __forceinline__ double rdl_f64(double v, int l) {
@@ -378,9 +380,11 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
     // the stretch ends: tokens and the per-request gap by the iteration
     // count, block boundaries by a countdown per slot) and step the two
     // attention operators' FLOPs and bytes by exact integer increments; the
-    // other operators' times are constant.  Decodes hold slots [0, nD) and
-    // prefills the slots after them: prefills receive tokens in slot order,
-    // so they complete in slot order.
+    // other operators' times are constant.  The iteration that ends the
+    // stretch (first finish, head prefill completion, iteration cap) is
+    // known when it starts.  The clock runs in fp64, exact below 2^53.
+    // Decodes hold slots [0, nD) and prefills the slots after them:
+    // prefills receive tokens in slot order, so they complete in slot order.
     if (nrun > 0) {
       const int nch0 = ((nrun + 63) >> 6) < NCH ? ((nrun + 63) >> 6) : NCH;
       int nD = 0;
@@ -401,7 +405,8 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       if (npf > 0 && unlimited) go = false;
       const int R0 = unlimited ? 0 : K - nD;  // chunk budget left after the decodes
       const int q = npf > 0 ? R0 : 0;         // the head prefill's tokens per iteration
-      const bool adm_budget = unlimited || (npf == 0 && R0 > 0);
+      // an admission would find a free slot and token budget
+      const bool adm_open = nrun < M && (unlimited || (npf == 0 && R0 > 0));
       int ctx_p = 0, tgt_p = 0;
       if (go && npf > 0) {
         const int jp = nD >> 6, lp = nD & 63;
@@ -412,95 +417,120 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
           ctx_p = __builtin_amdgcn_readfirstlane(L.x_ctx[(jp - 1) * 64 + lp]);
           tgt_p = __builtin_amdgcn_readfirstlane(L.x_tgt[(jp - 1) * 64 + lp]);
         }
+        if (tgt_p - ctx_p <= R0) go = false;  // the head prefill completes now
       }
+      constexpr int64_t kT52 = (int64_t)1 << 52;
+      if (n_iters >= A.iter_cap || t >= kT52) go = false;
+      if (A.time_limit_ticks != 0 && (n_iters & 255) == 0) go = false;  // watchdog below
       const int nchd = (nD + 63) >> 6;
-      int64_t nxt_arr = next < N ? rdl64(w_arr, next - wbase) : INT64_MAX;
-      int dG = 0, minrem = 0x7fffffff;
-      double Fw = 0.0, Bw = 0.0, dF = 0.0, dB = 0.0, emax = 0.0;
-      double c_t0 = 0.0, c_t3 = 0.0, c_t4 = 0.0, c_t5 = 0.0, c_lm = 0.0;
-      while (go) {
-        if (n_iters >= A.iter_cap) break;
-        if (A.time_limit_ticks != 0 && (n_iters & 255) == 0) break;  // watchdog below
-        if (next < N && nxt_arr <= t) {
-          intake();
-          nxt_arr = next < N ? rdl64(w_arr, next - wbase) : INT64_MAX;
-        }
-        if (minrem - dG == 1) break;                // a decode finishes
-        if (npf > 0 && tgt_p - ctx_p <= R0) break;  // the head prefill completes
-        int nneed = 0;
+      int nneed = 0;
+      if (go) {
+        if (next < N && rdl64(w_arr, next - wbase) <= t) intake();
 #pragma unroll
         for (int j = 0; j < NCH; ++j)
-          if (j < nchd) nneed += popc(ballot(rr[j] == dG));
-        if (nneed > freeb) break;                   // recompute preemption
-        const int fb = freeb - nneed;
-        if ((npre > 0 || nwait > 0) && nrun < M && adm_budget &&
-            !(head_need >= 0 && head_need > fb))
-          break;                                    // an admission may happen
-        if (dG == 0) {
-          // set-up: the decodes' smallest remaining count, their key sum, and
-          // every operator's work at this iteration with its per-iteration step
-          int mx = 0, cd = 0;
+          if (j < nchd) nneed += popc(ballot(rr[j] == 0));
+        if (nneed > freeb) go = false;  // recompute preemption
+        else if ((npre > 0 || nwait > 0) && adm_open &&
+                 !(head_need >= 0 && head_need > freeb - nneed))
+          go = false;  // an admission may happen
+      }
+      if (go) {
+        // the decodes' smallest remaining count and key sum
+        int mx = 0, cd = 0;
 #pragma unroll
-          for (int j = 0; j < NCH; ++j) {
-            if (j < nchd) {
-              const Hot h = load_chunk<NCH>(L, h0, j, lane);
-              const bool dec = (j * 64 + lane) < nD;
-              const int m = rdl(scan_max_i32(dec ? 0x7fffffff - h.rem : 0), 63);
-              mx = m > mx ? m : mx;
-              cd += wsum(dec ? h.ctx + 1 : 0);
-            }
+        for (int j = 0; j < NCH; ++j) {
+          if (j < nchd) {
+            const Hot h = load_chunk<NCH>(L, h0, j, lane);
+            const bool dec = (j * 64 + lane) < nD;
+            const int m = rdl(scan_max_i32(dec ? 0x7fffffff - h.rem : 0), 63);
+            mx = m > mx ? m : mx;
+            cd += wsum(dec ? h.ctx + 1 : 0);
           }
-          minrem = 0x7fffffff - mx;
-          const int64_t AP0 = (int64_t)q * ctx_p + ((int64_t)q * (q + 1)) / 2;
-          lane_work(roofc, nD + q, q, AP0, q > 0 ? ctx_p + q : 0, nD, cd, nD, &Fw, &Bw);
-          const double dX = roofc.is_attp ? (double)((int64_t)q * q)
-                                          : (roofc.is_attd ? (double)nD : 0.0);
-          const double dY = roofc.is_attp ? (double)q : (roofc.is_attd ? (double)nD : 0.0);
-          dF = roofc.f * dX;
-          dB = roofc.b1 * dY;
-          const double tl = __builtin_fmax(Fw * iF, Bw * iB);
-          c_t0 = rdl_f64(tl, 0);
-          c_t3 = rdl_f64(tl, 3);
-          c_t4 = rdl_f64(tl, 4);
-          c_t5 = rdl_f64(tl, 5);
-          c_lm = rdl_f64(tl, 6);
         }
-        freeb = fb;
-        if (nneed > 0) {
+        // every operator's work at this iteration and its per-iteration step
+        double Fw, Bw;
+        const int64_t AP0 = (int64_t)q * ctx_p + ((int64_t)q * (q + 1)) / 2;
+        lane_work(roofc, nD + q, q, AP0, q > 0 ? ctx_p + q : 0, nD, cd, nD, &Fw, &Bw);
+        const double dX = roofc.is_attp ? (double)((int64_t)q * q)
+                                        : (roofc.is_attd ? (double)nD : 0.0);
+        const double dY = roofc.is_attp ? (double)q : (roofc.is_attd ? (double)nD : 0.0);
+        const double dF = roofc.f * dX;
+        const double dB = roofc.b1 * dY;
+        // the constant operators' times, moved to lane 1 where the layer sum runs
+        const double tl0 = __builtin_fmax(Fw * iF, Bw * iB);
+        const double k_t0 = dpp_f64<0x111>(tl0);
+        const double k_t3 = dpp_f64<0x102>(tl0);
+        const double k_t4 = dpp_f64<0x103>(tl0);
+        const double k_t5 = dpp_f64<0x104>(tl0);
+        const double k_lm = dpp_f64<0x105>(tl0);
+        // the iteration at which the stretch ends
+        int stop = 0x3fffffff;
+        if (nD > 0) stop = 0x7fffffff - mx - 1;          // first decode finishes
+        if (q > 0) {                                      // the head prefill completes
+          const int kc = (tgt_p - ctx_p - 1) / q;
+          stop = kc < stop ? kc : stop;
+        }
+        if (A.iter_cap - n_iters < (int64_t)stop) stop = (int)(A.iter_cap - n_iters);
+        if (A.time_limit_ticks != 0) {
+          const int wd = 256 - (int)(n_iters & 255);
+          stop = wd < stop ? wd : stop;
+        }
+        const double kT52d = 4503599627370496.0;
+        double thr = next < N ? __builtin_fmin((double)rdl64(w_arr, next - wbase), kT52d) : kT52d;
+        // lane 1 carries the clock, the block-time integral and the largest
+        // iteration time of the stretch
+        double t_d = (double)t, ub = ubns, em = 0.0;
+        double used_d = (double)(NB - freeb);
+        int dG = 0;
+        for (;;) {
+          if (nneed > 0) {
+            freeb -= nneed;
+            used_d = (double)(NB - freeb);
+#pragma unroll
+            for (int j = 0; j < NCH; ++j)
+              if (j < nchd) rr[j] = rr[j] == dG ? rr[j] + B : rr[j];
+          }
+          // prefill attention (lane 1) and decode attention (lane 2, moved
+          // to lane 1), then the layer sum in the fixed operator order
+          const double tl = __builtin_fmax(Fw * iF, Bw * iB);
+          const double t2 = dpp_f64<0x101>(tl);
+          double lay = k_t0 + tl;
+          lay = lay + t2;
+          lay = lay + k_t3;
+          lay = lay + k_t4;
+          lay = lay + k_t5;
+          double tot = A.n_layers * lay;
+          tot = tot + k_lm;
+          const double it = __builtin_fmax(ceil(tot), 1.0);
+          ub = ub + used_d * it;
+          t_d = t_d + it;
+          em = __builtin_fmax(em, it);
+          Fw = Fw + dF;
+          Bw = Bw + dB;
+          ++dG;
+          if (dG == stop) break;
+          // the next iteration: arrivals, then block boundaries
+          if ((ballot(t_d >= thr) & 2ull) != 0) {
+            t = (int64_t)rdl_f64(t_d, 1);
+            if (t >= kT52) break;
+            intake();
+            thr = next < N ? __builtin_fmin((double)rdl64(w_arr, next - wbase), kT52d) : kT52d;
+            if ((npre > 0 || nwait > 0) && adm_open && head_need < 0) break;  // a new head
+          }
+          nneed = 0;
 #pragma unroll
           for (int j = 0; j < NCH; ++j)
-            if (j < nchd) rr[j] = rr[j] == dG ? rr[j] + B : rr[j];
+            if (j < nchd) nneed += popc(ballot(rr[j] == dG));
+          if (nneed > freeb) break;
         }
-        // prefill attention on lane 1, decode attention on lane 2 (moved to
-        // lane 1), then the layer sum in the fixed operator order
-        const double tl = __builtin_fmax(Fw * iF, Bw * iB);
-        const double t2 = dpp_shl1_f64(tl);
-        double lay = c_t0 + tl;
-        lay = lay + t2;
-        lay = lay + c_t3;
-        lay = lay + c_t4;
-        lay = lay + c_t5;
-        double tot = A.n_layers * lay;
-        tot = tot + c_lm;
-        const double it = __builtin_fmax(ceil(tot), 1.0);
-        const double iter_d = rdl_f64(it, 1);
-        const int64_t iter_ns = rdl64((int64_t)it, 1);
-        const int used = NB - freeb;
-        if (used > peak) peak = used;
-        ubns = ubns + (double)used * iter_d;
-        ++n_iters;
-        pf_tok += q;
-        dec_tok += nD;
-        ctx_p += q;
-        emax = __builtin_fmax(iter_d, emax);
-        Fw = Fw + dF;
-        Bw = Bw + dB;
-        t = t + iter_ns;
-        ++dG;
-      }
-      if (dG > 0) {
-        // materialise the decodes and the head prefill
-        const int64_t gx = (int64_t)emax;
+        // materialise the point's counters, the decodes and the head prefill
+        t = (int64_t)rdl_f64(t_d, 1);
+        ubns = rdl_f64(ub, 1);
+        n_iters += dG;
+        pf_tok += (int64_t)q * dG;
+        dec_tok += (int64_t)nD * dG;
+        if (NB - freeb > peak) peak = NB - freeb;
+        const int64_t gx = (int64_t)rdl_f64(em, 1);
 #pragma unroll
         for (int j = 0; j < NCH; ++j) {
           if (j < nchd) {
@@ -522,6 +552,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
         }
         if (q > 0) {
           const int jp = nD >> 6, lp = nD & 63;
+          ctx_p += q * dG;
           if (NCH == 1 || jp == 0) h0.ctx = lane == lp ? ctx_p : h0.ctx;
           else L.x_ctx[(jp - 1) * 64 + lp] = ctx_p;  // every lane stores the same value
         }
