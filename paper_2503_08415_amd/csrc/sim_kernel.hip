@@ -370,18 +370,128 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
     if (nwait == 0) next_new = next;
   };
 
+  // x / B; block sizes are usually powers of two
+  const int lgB = (B & (B - 1)) == 0 ? 31 - __builtin_clz((unsigned)B) : -1;
+  auto divB = [&](int x) { return lgB >= 0 ? x >> lgB : x / B; };
+
+  // A request finishing at t_end (lanes with fin): its statistics and record.
+  auto record_done = [&](bool fin, int s, int64_t t_end, int64_t gap, int pos) {
+    if (fin) {
+      const int id = L.id[s];
+      const int npr = L.npre[s];
+      const ReqTimes rt = RT[id];
+      const int64_t arr = rec[id].arrival_ns;
+      const int64_t tt = rt.first - arr;
+      const int64_t ee = t_end - arr;
+      atomicAdd(&L.sum_ttft, (unsigned long long)tt);
+      atomicAdd(&L.sum_e2e, (unsigned long long)ee);
+      atomicAdd(&L.sum_tpot, (unsigned long long)(t_end - rt.first));
+      atomicMax(&L.max_e2e, (long long)ee);
+      atomicMax(&L.last_fin, (long long)t_end);
+      if (tt <= A.slo_ttft_ns && gap <= A.slo_tpot_ns) atomicAdd(&L.slo_ok, 1u);
+      atomicAdd(&L.digest, (unsigned long long)record_hash(id, rt.admit, rt.first, t_end, gap,
+                                                           npr, TS_REQ_DONE));
+      if (RR) {
+        ts_req_result o;
+        o.admit_ns = rt.admit; o.first_token_ns = rt.first; o.finish_ns = t_end;
+        o.max_gap_ns = gap; o.n_preempt = npr; o.status = TS_REQ_DONE;
+        RR[id] = o;
+      }
+      E2E[pos] = ee;
+      TTFT[pos] = tt;
+    }
+  };
+
+  // Remove the slots whose rem is 0, keeping the others in slot order.
+  auto compact = [&](int nfin) {
+    const int nsurv = nrun - nfin;
+    if (nrun <= 64) {
+      // One chunk: every lane pushes its slot through the LDS crossbar to
+      // its new lane, survivors first in slot order, then the others.
+      const bool keep = lane < nrun && h0.rem > 0;
+      const uint64_t km = ballot(keep);
+      const int ad = (keep ? rank_below(km) : nsurv + rank_below(~km)) << 2;
+      h0.ctx = __builtin_amdgcn_ds_permute(ad, h0.ctx);
+      h0.tgt = __builtin_amdgcn_ds_permute(ad, h0.tgt);
+      h0.rem = __builtin_amdgcn_ds_permute(ad, h0.rem);
+      h0.room = __builtin_amdgcn_ds_permute(ad, h0.room);
+      h0.fl = __builtin_amdgcn_ds_permute(ad, h0.fl);
+      const uint32_t glo = (uint32_t)__builtin_amdgcn_ds_permute(ad, (int)(uint32_t)h0.gap);
+      const uint32_t ghi =
+          (uint32_t)__builtin_amdgcn_ds_permute(ad, (int)(uint32_t)((uint64_t)h0.gap >> 32));
+      h0.gap = (int64_t)(((uint64_t)ghi << 32) | glo);
+      const int idv = __builtin_amdgcn_ds_permute(ad, L.id[lane]);
+      const int npv = __builtin_amdgcn_ds_permute(ad, L.npre[lane]);
+      L.id[lane] = idv;
+      L.npre[lane] = npv;
+    } else {
+      // Stable compaction of the survivors through LDS scratch, one field at
+      // a time.  Finished slots have rem == 0; rem moves last so every pass
+      // reads 'keep' from the original slots.
+      const int nch = ((nrun + 63) >> 6) < NCH ? ((nrun + 63) >> 6) : NCH;
+      const int nch2 = (nsurv + 63) >> 6;
+      int32_t* s32 = reinterpret_cast<int32_t*>(L.u.scratch);
+#pragma nounroll
+      for (int f = 0; f < 8; ++f) {
+        int carry = 0;
+#pragma nounroll
+        for (int j = 0; j < nch; ++j) {
+          const int s = j * 64 + lane;
+          const int e = (j - 1) * 64 + lane;
+          const int rem = j == 0 ? h0.rem : L.x_rem[e];
+          const bool keep = s < nrun && rem > 0;
+          const uint64_t km = ballot(keep);
+          const int pos = carry + rank_below(km);
+          carry += popc(km);
+          if (keep) {
+            switch (f) {
+              case 0: s32[pos] = j == 0 ? h0.ctx : L.x_ctx[e]; break;
+              case 1: s32[pos] = j == 0 ? h0.tgt : L.x_tgt[e]; break;
+              case 2: s32[pos] = j == 0 ? h0.room : L.x_room[e]; break;
+              case 3: s32[pos] = j == 0 ? h0.fl : L.x_fl[e]; break;
+              case 4: s32[pos] = L.id[s]; break;
+              case 5: L.u.scratch[pos] = j == 0 ? h0.gap : L.x_gap[e]; break;
+              case 6: s32[pos] = L.npre[s]; break;
+              default: s32[pos] = rem; break;
+            }
+          }
+        }
+        __syncthreads();
+#pragma nounroll
+        for (int j = 0; j < nch2; ++j) {
+          const int s = j * 64 + lane;
+          const int e = (j - 1) * 64 + lane;
+          switch (f) {
+            case 0: if (j == 0) h0.ctx = s32[s]; else L.x_ctx[e] = s32[s]; break;
+            case 1: if (j == 0) h0.tgt = s32[s]; else L.x_tgt[e] = s32[s]; break;
+            case 2: if (j == 0) h0.room = s32[s]; else L.x_room[e] = s32[s]; break;
+            case 3: if (j == 0) h0.fl = s32[s]; else L.x_fl[e] = s32[s]; break;
+            case 4: L.id[s] = s32[s]; break;
+            case 5: if (j == 0) h0.gap = L.u.scratch[s]; else L.x_gap[e] = L.u.scratch[s]; break;
+            case 6: L.npre[s] = s32[s]; break;
+            default: if (j == 0) h0.rem = s32[s]; else L.x_rem[e] = s32[s]; break;
+          }
+        }
+        __syncthreads();
+      }
+    }
+    nrun = nsurv;
+  };
+
   const uint64_t clock0 = A.time_limit_ticks ? __builtin_amdgcn_s_memrealtime() : 0;
   while (status == TS_POINT_OK) {
-    // ---- 0. steady stretch.  As long as no request is admitted, preempted
-    // or finishes and no prefill completes, an iteration advances every
-    // decode by one token and the head prefill by the whole remaining chunk
-    // budget, so every batch sum moves by a fixed integer per iteration.
-    // Such iterations keep the decodes' slot state lazily (materialised when
-    // the stretch ends: tokens and the per-request gap by the iteration
-    // count, block boundaries by a countdown per slot) and step the two
-    // attention operators' FLOPs and bytes by exact integer increments; the
-    // other operators' times are constant.  The iteration that ends the
-    // stretch (first finish, head prefill completion, iteration cap) is
+    // ---- 0. steady stretch.  As long as no request is admitted or
+    // preempted and no prefill completes, an iteration advances every decode
+    // by one token and the head prefill by the whole remaining chunk budget,
+    // so every batch sum moves by a fixed integer per iteration.  Such
+    // iterations keep the decodes' slot state lazily (materialised when the
+    // stretch ends: tokens and the per-request gap by the iteration count,
+    // block boundaries by a countdown per slot) and step the two attention
+    // operators' FLOPs and bytes by exact integer increments; the other
+    // operators' times are constant.  Decodes that finish are recorded in
+    // place and leave holes, removed when the stretch ends; the sums are then
+    // re-derived for the next segment of the stretch.  The iteration that ends
+    // a segment (first finish, head prefill completion, iteration cap) is
     // known when it starts.  The clock runs in fp64, exact below 2^53.
     // Decodes hold slots [0, nD) and prefills the slots after them:
     // prefills receive tokens in slot order, so they complete in slot order.
@@ -389,10 +499,12 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       const int nch0 = ((nrun + 63) >> 6) < NCH ? ((nrun + 63) >> 6) : NCH;
       int nD = 0;
       bool go = true;
-      int rr[NCH];  // decode slots: room + B * (blocks taken) in this stretch
+      // alive decode slots: room + B * (blocks taken in this stretch), >= 0;
+      // every other lane (prefills, unused, finished) holds a negative value
+      int rr[NCH];
 #pragma unroll
       for (int j = 0; j < NCH; ++j) {
-        rr[j] = -0x40000000;  // never equal to an iteration count
+        rr[j] = -0x40000000;
         if (j < nch0) {
           const Hot h = load_chunk<NCH>(L, h0, j, lane);
           const bool dec = (j * 64 + lane) < nrun && h.ctx >= h.tgt;
@@ -403,10 +515,6 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       }
       const int npf = nrun - nD;
       if (npf > 0 && unlimited) go = false;
-      const int R0 = unlimited ? 0 : K - nD;  // chunk budget left after the decodes
-      const int q = npf > 0 ? R0 : 0;         // the head prefill's tokens per iteration
-      // an admission would find a free slot and token budget
-      const bool adm_open = nrun < M && (unlimited || (npf == 0 && R0 > 0));
       int ctx_p = 0, tgt_p = 0;
       if (go && npf > 0) {
         const int jp = nD >> 6, lp = nD & 63;
@@ -417,12 +525,15 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
           ctx_p = __builtin_amdgcn_readfirstlane(L.x_ctx[(jp - 1) * 64 + lp]);
           tgt_p = __builtin_amdgcn_readfirstlane(L.x_tgt[(jp - 1) * 64 + lp]);
         }
-        if (tgt_p - ctx_p <= R0) go = false;  // the head prefill completes now
+        if (tgt_p - ctx_p <= K - nD) go = false;  // the head prefill completes now
       }
       constexpr int64_t kT52 = (int64_t)1 << 52;
       if (n_iters >= A.iter_cap || t >= kT52) go = false;
       if (A.time_limit_ticks != 0 && (n_iters & 255) == 0) go = false;  // watchdog below
       const int nchd = (nD + 63) >> 6;
+      int nDa = nD, nruna = nrun;  // alive decodes and running requests
+      // an admission would find a free slot and token budget
+      auto adm_open = [&]() { return nruna < M && (unlimited || (npf == 0 && K - nDa > 0)); };
       int nneed = 0;
       if (go) {
         if (next < N && rdl64(w_arr, next - wbase) <= t) intake();
@@ -430,66 +541,77 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
         for (int j = 0; j < NCH; ++j)
           if (j < nchd) nneed += popc(ballot(rr[j] == 0));
         if (nneed > freeb) go = false;  // recompute preemption
-        else if ((npre > 0 || nwait > 0) && adm_open &&
+        else if ((npre > 0 || nwait > 0) && adm_open() &&
                  !(head_need >= 0 && head_need > freeb - nneed))
           go = false;  // an admission may happen
       }
       if (go) {
-        // the decodes' smallest remaining count and key sum
-        int mx = 0, cd = 0;
-#pragma unroll
-        for (int j = 0; j < NCH; ++j) {
-          if (j < nchd) {
-            const Hot h = load_chunk<NCH>(L, h0, j, lane);
-            const bool dec = (j * 64 + lane) < nD;
-            const int m = rdl(scan_max_i32(dec ? 0x7fffffff - h.rem : 0), 63);
-            mx = m > mx ? m : mx;
-            cd += wsum(dec ? h.ctx + 1 : 0);
-          }
-        }
-        // every operator's work at this iteration and its per-iteration step
-        double Fw, Bw;
-        const int64_t AP0 = (int64_t)q * ctx_p + ((int64_t)q * (q + 1)) / 2;
-        lane_work(roofc, nD + q, q, AP0, q > 0 ? ctx_p + q : 0, nD, cd, nD, &Fw, &Bw);
-        const double dX = roofc.is_attp ? (double)((int64_t)q * q)
-                                        : (roofc.is_attd ? (double)nD : 0.0);
-        const double dY = roofc.is_attp ? (double)q : (roofc.is_attd ? (double)nD : 0.0);
-        const double dF = roofc.f * dX;
-        const double dB = roofc.b1 * dY;
-        // the constant operators' times, moved to lane 1 where the layer sum runs
-        const double tl0 = __builtin_fmax(Fw * iF, Bw * iB);
-        const double k_t0 = dpp_f64<0x111>(tl0);
-        const double k_t3 = dpp_f64<0x102>(tl0);
-        const double k_t4 = dpp_f64<0x103>(tl0);
-        const double k_t5 = dpp_f64<0x104>(tl0);
-        const double k_lm = dpp_f64<0x105>(tl0);
-        // the iteration at which the stretch ends
-        int stop = 0x3fffffff;
-        if (nD > 0) stop = 0x7fffffff - mx - 1;          // first decode finishes
-        if (q > 0) {                                      // the head prefill completes
-          const int kc = (tgt_p - ctx_p - 1) / q;
-          stop = kc < stop ? kc : stop;
-        }
-        if (A.iter_cap - n_iters < (int64_t)stop) stop = (int)(A.iter_cap - n_iters);
+        // iterations (counted from the stretch start) that must run elsewhere:
+        // the iteration cap and the watchdog's clock checks
+        int stop_fix = 0x3fffffff;
+        if (A.iter_cap - n_iters < (int64_t)stop_fix) stop_fix = (int)(A.iter_cap - n_iters);
         if (A.time_limit_ticks != 0) {
           const int wd = 256 - (int)(n_iters & 255);
-          stop = wd < stop ? wd : stop;
+          stop_fix = wd < stop_fix ? wd : stop_fix;
         }
+        int dG = 0, seg0 = 0, q = 0, fin_at = 0, stop = 0;
+        double Fw = 0.0, Bw = 0.0, dF = 0.0, dB = 0.0;
+        double k_t0 = 0.0, k_t3 = 0.0, k_t4 = 0.0, k_t5 = 0.0, k_lm = 0.0;
+        // Segment set-up at iteration dG: the alive decodes' first finishing
+        // iteration and key sum, the head prefill's chunk, every operator's
+        // work and its per-iteration step, and the segment's last iteration.
+        auto setup = [&]() {
+          int mx = 0, cs = 0;
+#pragma unroll
+          for (int j = 0; j < NCH; ++j) {
+            if (j < nchd) {
+              const int e = (j - 1) * 64 + lane;
+              const int rem0 = j == 0 ? h0.rem : L.x_rem[e];
+              const int ctx0 = j == 0 ? h0.ctx : L.x_ctx[e];
+              const bool al = rr[j] >= 0;
+              const int m = rdl(scan_max_i32(al ? 0x7fffffff - rem0 : 0), 63);
+              mx = m > mx ? m : mx;
+              cs += wsum(al ? ctx0 + 1 : 0);
+            }
+          }
+          fin_at = nDa > 0 ? 0x7fffffff - mx - 1 : 0x3fffffff;
+          const int cd = cs + nDa * dG;
+          q = npf > 0 ? K - nDa : 0;
+          const int64_t AP0 = (int64_t)q * ctx_p + ((int64_t)q * (q + 1)) / 2;
+          lane_work(roofc, nDa + q, q, AP0, q > 0 ? ctx_p + q : 0, nDa, cd, nDa, &Fw, &Bw);
+          const double dX = roofc.is_attp ? (double)((int64_t)q * q)
+                                          : (roofc.is_attd ? (double)nDa : 0.0);
+          const double dY = roofc.is_attp ? (double)q : (roofc.is_attd ? (double)nDa : 0.0);
+          dF = roofc.f * dX;
+          dB = roofc.b1 * dY;
+          // the constant operators' times, moved to lane 1 where the layer sum runs
+          const double tl0 = __builtin_fmax(Fw * iF, Bw * iB);
+          k_t0 = dpp_f64<0x111>(tl0);
+          k_t3 = dpp_f64<0x102>(tl0);
+          k_t4 = dpp_f64<0x103>(tl0);
+          k_t5 = dpp_f64<0x104>(tl0);
+          k_lm = dpp_f64<0x105>(tl0);
+          stop = stop_fix;
+          if (q > 0) {  // the head prefill completes in iteration kc
+            const int kc = dG + (tgt_p - ctx_p - 1) / q;
+            stop = kc < stop ? kc : stop;
+          }
+          seg0 = dG;
+        };
         const double kT52d = 4503599627370496.0;
         double thr = next < N ? __builtin_fmin((double)rdl64(w_arr, next - wbase), kT52d) : kT52d;
-        // lane 1 carries the clock, the block-time integral and the largest
-        // iteration time of the stretch
-        double t_d = (double)t, ub = ubns, em = 0.0;
-        double used_d = (double)(NB - freeb);
-        int dG = 0;
+        // lane 1 carries the clock, the block-time integral, the iteration
+        // time and the largest iteration time of the finished segments
+        double t_d = (double)t, ub = ubns, it = 0.0, em = 0.0;
+        setup();
         for (;;) {
           if (nneed > 0) {
             freeb -= nneed;
-            used_d = (double)(NB - freeb);
 #pragma unroll
             for (int j = 0; j < NCH; ++j)
-              if (j < nchd) rr[j] = rr[j] == dG ? rr[j] + B : rr[j];
+              if (j < nchd) rr[j] += rr[j] == dG ? B : 0;
           }
+          const double used_d = (double)(NB - freeb);
           // prefill attention (lane 1) and decode attention (lane 2, moved
           // to lane 1), then the layer sum in the fixed operator order
           const double tl = __builtin_fmax(Fw * iF, Bw * iB);
@@ -501,13 +623,56 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
           lay = lay + k_t5;
           double tot = A.n_layers * lay;
           tot = tot + k_lm;
-          const double it = __builtin_fmax(ceil(tot), 1.0);
+          it = __builtin_fmax(ceil(tot), 1.0);
           ub = ub + used_d * it;
           t_d = t_d + it;
-          em = __builtin_fmax(em, it);
           Fw = Fw + dF;
           Bw = Bw + dB;
-          ++dG;
+          if (dG == fin_at) {
+            // Alive decodes emitting their last token finish at the end of
+            // this iteration.  Iteration times never fall within a segment,
+            // so the largest so far is the larger of em and this one.
+            em = __builtin_fmax(em, it);
+            const int64_t t_end = (int64_t)rdl_f64(t_d, 1);
+            const int64_t gx = (int64_t)rdl_f64(em, 1);
+            int nfin = 0, l_freed = 0;
+#pragma unroll
+            for (int j = 0; j < NCH; ++j) {
+              if (j < nchd) {
+                const int e = (j - 1) * 64 + lane;
+                const int rem0 = j == 0 ? h0.rem : L.x_rem[e];
+                const bool fin = rr[j] >= 0 && rem0 - 1 == dG;
+                const uint64_t fm = ballot(fin);
+                if (fm != 0) {
+                  const int ctx0 = j == 0 ? h0.ctx : L.x_ctx[e];
+                  const int64_t gap0 = j == 0 ? h0.gap : L.x_gap[e];
+                  record_done(fin, j * 64 + lane, t_end, gx > gap0 ? gx : gap0,
+                              n_done + nfin + rank_below(fm));
+                  l_freed += fin ? divB(ctx0 + rr[j]) : 0;  // held blocks
+                  rr[j] = fin ? -0x40000000 : rr[j];
+                  nfin += popc(fm);
+                }
+              }
+            }
+            // the segment's bookkeeping, through this iteration
+            const int len = dG + 1 - seg0;
+            pf_tok += (int64_t)q * len;
+            dec_tok += (int64_t)nDa * len;
+            ctx_p += q * len;
+            if (NB - freeb > peak) peak = NB - freeb;
+            freeb += wsum(l_freed);
+            n_done += nfin;
+            nDa -= nfin;
+            nruna -= nfin;
+            ++dG;
+            seg0 = dG;
+            if (nruna == 0) break;
+            if ((npre > 0 || nwait > 0) && adm_open() && !(head_need >= 0 && head_need > freeb))
+              break;  // the freed slot or blocks may admit
+            setup();
+          } else {
+            ++dG;
+          }
           if (dG == stop) break;
           // the next iteration: arrivals, then block boundaries
           if ((ballot(t_d >= thr) & 2ull) != 0) {
@@ -515,7 +680,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
             if (t >= kT52) break;
             intake();
             thr = next < N ? __builtin_fmin((double)rdl64(w_arr, next - wbase), kT52d) : kT52d;
-            if ((npre > 0 || nwait > 0) && adm_open && head_need < 0) break;  // a new head
+            if ((npre > 0 || nwait > 0) && adm_open() && head_need < 0) break;  // a new head
           }
           nneed = 0;
 #pragma unroll
@@ -523,39 +688,46 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
             if (j < nchd) nneed += popc(ballot(rr[j] == dG));
           if (nneed > freeb) break;
         }
-        // materialise the point's counters, the decodes and the head prefill
+        // the last segment's bookkeeping, the point's counters, the decodes
+        // (finished ones get rem 0) and the head prefill, then close the holes
+        {
+          const int len = dG - seg0;
+          pf_tok += (int64_t)q * len;
+          dec_tok += (int64_t)nDa * len;
+          ctx_p += q * len;
+        }
+        if (NB - freeb > peak) peak = NB - freeb;
+        em = __builtin_fmax(em, it);
         t = (int64_t)rdl_f64(t_d, 1);
         ubns = rdl_f64(ub, 1);
         n_iters += dG;
-        pf_tok += (int64_t)q * dG;
-        dec_tok += (int64_t)nD * dG;
-        if (NB - freeb > peak) peak = NB - freeb;
         const int64_t gx = (int64_t)rdl_f64(em, 1);
 #pragma unroll
         for (int j = 0; j < NCH; ++j) {
           if (j < nchd) {
             const bool dec = (j * 64 + lane) < nD;
+            const bool al = rr[j] >= 0;
             if (j == 0) {
-              h0.ctx = dec ? h0.ctx + dG : h0.ctx;
-              h0.rem = dec ? h0.rem - dG : h0.rem;
-              h0.room = dec ? rr[0] - dG : h0.room;
-              h0.gap = dec && gx > h0.gap ? gx : h0.gap;
+              h0.ctx = al ? h0.ctx + dG : h0.ctx;
+              h0.rem = al ? h0.rem - dG : (dec ? 0 : h0.rem);
+              h0.room = al ? rr[0] - dG : h0.room;
+              h0.gap = al && gx > h0.gap ? gx : h0.gap;
             } else {
               const int e = (j - 1) * 64 + lane;
               const int64_t g = L.x_gap[e];
-              L.x_ctx[e] = dec ? L.x_ctx[e] + dG : L.x_ctx[e];
-              L.x_rem[e] = dec ? L.x_rem[e] - dG : L.x_rem[e];
-              L.x_room[e] = dec ? rr[j] - dG : L.x_room[e];
-              L.x_gap[e] = dec && gx > g ? gx : g;
+              L.x_ctx[e] = al ? L.x_ctx[e] + dG : L.x_ctx[e];
+              L.x_rem[e] = al ? L.x_rem[e] - dG : (dec ? 0 : L.x_rem[e]);
+              L.x_room[e] = al ? rr[j] - dG : L.x_room[e];
+              L.x_gap[e] = al && gx > g ? gx : g;
             }
           }
         }
-        if (q > 0) {
+        if (npf > 0) {
           const int jp = nD >> 6, lp = nD & 63;
-          ctx_p += q * dG;
           if (NCH == 1 || jp == 0) h0.ctx = lane == lp ? ctx_p : h0.ctx;
           else L.x_ctx[(jp - 1) * 64 + lp] = ctx_p;  // every lane stores the same value
         }
+        if (nruna < nrun) compact(nrun - nruna);
       }
     }
     // watchdog: a point running longer than the wall-clock limit stops
@@ -617,7 +789,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
         const bool act = (j * 64 + lane) < nrun;
         const int top = h.ctx > h.tgt ? h.ctx : h.tgt;
         const int need = (h.ctx >= h.tgt && h.room == 0) ? 1 : 0;
-        const int v = act ? (top + h.room) / B + need : 0;  // held + needed blocks
+        const int v = act ? divB(top + h.room) + need : 0;  // held + needed blocks
         const int S = scan_i32(v) + carry;
         const bool keep = act && S <= NB;
         k += popc(ballot(keep));
@@ -751,7 +923,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
           continue;
         }
         const int rank = rank_below(vm);
-        const int need = valid ? (c_tgt + B - 1) / B : 0;
+        const int need = valid ? divB(c_tgt + B - 1) : 0;
         const int SN = scan_i32(need);
         const int tq = valid ? c_tgt : 0;
         const int ET = scan_i32(tq) - tq;
@@ -891,32 +1063,8 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       store_chunk<NCH>(L, h0, j, lane, h);
       const uint64_t fm = ballot(fin);
       if (fm != 0) {
-        if (fin) {
-          const int id = L.id[s];
-          const int npr = L.npre[s];
-          const ReqTimes rt = RT[id];
-          const int64_t arr = rec[id].arrival_ns;
-          const int64_t tt = rt.first - arr;
-          const int64_t ee = t_end - arr;
-          atomicAdd(&L.sum_ttft, (unsigned long long)tt);
-          atomicAdd(&L.sum_e2e, (unsigned long long)ee);
-          atomicAdd(&L.sum_tpot, (unsigned long long)(t_end - rt.first));
-          atomicMax(&L.max_e2e, (long long)ee);
-          atomicMax(&L.last_fin, (long long)t_end);
-          if (tt <= A.slo_ttft_ns && h.gap <= A.slo_tpot_ns) atomicAdd(&L.slo_ok, 1u);
-          atomicAdd(&L.digest, (unsigned long long)record_hash(id, rt.admit, rt.first, t_end,
-                                                               h.gap, npr, TS_REQ_DONE));
-          if (RR) {
-            ts_req_result o;
-            o.admit_ns = rt.admit; o.first_token_ns = rt.first; o.finish_ns = t_end;
-            o.max_gap_ns = h.gap; o.n_preempt = npr; o.status = TS_REQ_DONE;
-            RR[id] = o;
-          }
-          const int pos = base + rank_below(fm);
-          E2E[pos] = ee;
-          TTFT[pos] = tt;
-          l_freed += (h.ctx + h.room) / B;  // held blocks (ctx >= tgt here)
-        }
+        record_done(fin, s, t_end, h.gap, base + rank_below(fm));
+        if (fin) l_freed += divB(h.ctx + h.room);  // held blocks (ctx >= tgt here)
         base += popc(fm);
         nfin += popc(fm);
       }
@@ -924,80 +1072,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
     if (nfin > 0) {
       freeb += wsum(l_freed);
       n_done += nfin;
-      const int nsurv = nrun - nfin;
-      if (nrun <= 64) {
-        // One chunk: every lane pushes its slot through the LDS crossbar to
-        // its new lane, survivors first in slot order, then the others.
-        const bool keep = lane < nrun && h0.rem > 0;
-        const uint64_t km = ballot(keep);
-        const int ad = (keep ? rank_below(km) : nsurv + rank_below(~km)) << 2;
-        h0.ctx = __builtin_amdgcn_ds_permute(ad, h0.ctx);
-        h0.tgt = __builtin_amdgcn_ds_permute(ad, h0.tgt);
-        h0.rem = __builtin_amdgcn_ds_permute(ad, h0.rem);
-        h0.room = __builtin_amdgcn_ds_permute(ad, h0.room);
-        h0.fl = __builtin_amdgcn_ds_permute(ad, h0.fl);
-        const uint32_t glo = (uint32_t)__builtin_amdgcn_ds_permute(ad, (int)(uint32_t)h0.gap);
-        const uint32_t ghi =
-            (uint32_t)__builtin_amdgcn_ds_permute(ad, (int)(uint32_t)((uint64_t)h0.gap >> 32));
-        h0.gap = (int64_t)(((uint64_t)ghi << 32) | glo);
-        const int idv = __builtin_amdgcn_ds_permute(ad, L.id[lane]);
-        const int npv = __builtin_amdgcn_ds_permute(ad, L.npre[lane]);
-        L.id[lane] = idv;
-        L.npre[lane] = npv;
-        nrun = nsurv;
-      }
-    }
-    if (nfin > 0 && nrun > 64) {
-      // Stable compaction of the survivors through LDS scratch, one field at
-      // a time.  Finished slots have rem == 0; rem moves last so every pass
-      // reads 'keep' from the original slots.
-      const int nsurv = nrun - nfin;
-      const int nch2 = (nsurv + 63) >> 6;
-      int32_t* s32 = reinterpret_cast<int32_t*>(L.u.scratch);
-#pragma nounroll
-      for (int f = 0; f < 8; ++f) {
-        int carry = 0;
-#pragma nounroll
-        for (int j = 0; j < nch; ++j) {
-          const int s = j * 64 + lane;
-          const int e = (j - 1) * 64 + lane;
-          const int rem = j == 0 ? h0.rem : L.x_rem[e];
-          const bool keep = s < nrun && rem > 0;
-          const uint64_t km = ballot(keep);
-          const int pos = carry + rank_below(km);
-          carry += popc(km);
-          if (keep) {
-            switch (f) {
-              case 0: s32[pos] = j == 0 ? h0.ctx : L.x_ctx[e]; break;
-              case 1: s32[pos] = j == 0 ? h0.tgt : L.x_tgt[e]; break;
-              case 2: s32[pos] = j == 0 ? h0.room : L.x_room[e]; break;
-              case 3: s32[pos] = j == 0 ? h0.fl : L.x_fl[e]; break;
-              case 4: s32[pos] = L.id[s]; break;
-              case 5: L.u.scratch[pos] = j == 0 ? h0.gap : L.x_gap[e]; break;
-              case 6: s32[pos] = L.npre[s]; break;
-              default: s32[pos] = rem; break;
-            }
-          }
-        }
-        __syncthreads();
-#pragma nounroll
-        for (int j = 0; j < nch2; ++j) {
-          const int s = j * 64 + lane;
-          const int e = (j - 1) * 64 + lane;
-          switch (f) {
-            case 0: if (j == 0) h0.ctx = s32[s]; else L.x_ctx[e] = s32[s]; break;
-            case 1: if (j == 0) h0.tgt = s32[s]; else L.x_tgt[e] = s32[s]; break;
-            case 2: if (j == 0) h0.room = s32[s]; else L.x_room[e] = s32[s]; break;
-            case 3: if (j == 0) h0.fl = s32[s]; else L.x_fl[e] = s32[s]; break;
-            case 4: L.id[s] = s32[s]; break;
-            case 5: if (j == 0) h0.gap = L.u.scratch[s]; else L.x_gap[e] = L.u.scratch[s]; break;
-            case 6: L.npre[s] = s32[s]; break;
-            default: if (j == 0) h0.rem = s32[s]; else L.x_rem[e] = s32[s]; break;
-          }
-        }
-        __syncthreads();
-      }
-      nrun = nsurv;
+      compact(nfin);
     }
     t = t_end;
   }
