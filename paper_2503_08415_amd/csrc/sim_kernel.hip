@@ -168,9 +168,16 @@ __device__ __forceinline__ double rdl_f64(double v, int l) {
   return __builtin_bit_cast(double, (uint64_t)rdl64((int64_t)__builtin_bit_cast(uint64_t, v), l));
 }
 
+// This lane's operator coefficients (zero above lane 6), read from LDS on
+// use rather than held in registers across the whole simulation.
 struct LaneRoof {
-  double f, b0, b1, b2;  // this lane's operator coefficients (zero above lane 6)
+  const volatile double* tab;  // [4][8]: f, b0, b1, b2 per operator lane
+  int cl;                      // operator lane: min(lane, 7)
   bool is_attp, is_attd, is_lm;
+  __device__ double f() const { return tab[cl]; }
+  __device__ double b0() const { return tab[8 + cl]; }
+  __device__ double b1() const { return tab[16 + cl]; }
+  __device__ double b2() const { return tab[24 + cl]; }
 };
 
 // This lane's operator FLOPs F and bytes B for the batch sums (exact integers).
@@ -183,9 +190,9 @@ __device__ __forceinline__ void lane_work(const LaneRoof& c, int T, int TP, int6
   const double X = c.is_attp ? (double)AP : (double)xi;
   const double Y = (double)yi;
   const double Z = (double)zi;
-  const double b0 = (c.is_lm && R == 0) ? 0.0 : c.b0;  // no LM head without an emitter
-  *F = c.f * X;
-  *Bv = (b0 + c.b1 * Y) + c.b2 * Z;
+  const double b0 = (c.is_lm && R == 0) ? 0.0 : c.b0();  // no LM head without an emitter
+  *F = c.f() * X;
+  *Bv = (b0 + c.b1() * Y) + c.b2() * Z;
 }
 
 // Returns max(1, ceil(L * layer_sum + lm_head)) and the same value as a double.
@@ -582,8 +589,8 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
           const double dX = roofc.is_attp ? (double)((int64_t)q * q)
                                           : (roofc.is_attd ? (double)nDa : 0.0);
           const double dY = roofc.is_attp ? (double)q : (roofc.is_attd ? (double)nDa : 0.0);
-          dF = roofc.f * dX;
-          dB = roofc.b1 * dY;
+          dF = roofc.f() * dX;
+          dB = roofc.b1() * dY;
           // the constant operators' times, moved to lane 1 where the layer sum runs
           const double tl0 = __builtin_fmax(Fw * iF, Bw * iB);
           k_t0 = dpp_f64<0x111>(tl0);
@@ -1119,17 +1126,22 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
 // Persistent grid: each wave64 workgroup takes the next point from a ticket
 // counter until none is left.
 template <int NCH>
-__global__ __launch_bounds__(64) void sim_kernel(SimArgs A) {
+__global__ __launch_bounds__(64, 5) void sim_kernel(SimArgs A) {
   __shared__ SlotLds<NCH> L;
   const int lane = lane_id();
   QEntry* Q = A.queue + (size_t)blockIdx.x * kQueueCap;
   ReqTimes* RT = A.times + (size_t)blockIdx.x * (size_t)A.max_n;
+  __shared__ double coef[32];
+  if (lane < 8) {
+    coef[lane] = A.lc.f[lane];
+    coef[8 + lane] = A.lc.b0[lane];
+    coef[16 + lane] = A.lc.b1[lane];
+    coef[24 + lane] = A.lc.b2[lane];
+  }
+  __syncthreads();
   LaneRoof roofc;
-  const int cl = lane < 8 ? lane : 7;
-  roofc.f = A.lc.f[cl];
-  roofc.b0 = A.lc.b0[cl];
-  roofc.b1 = A.lc.b1[cl];
-  roofc.b2 = A.lc.b2[cl];
+  roofc.tab = coef;
+  roofc.cl = lane < 8 ? lane : 7;
   roofc.is_attp = lane == 1;
   roofc.is_attd = lane == 2;
   roofc.is_lm = lane == 6;
