@@ -10,20 +10,21 @@ The default workload is the largest sweep: 65536 design points x 10000
 requests (7B GQA model, chunked prefill 256..2048, long-context prompt
 mixture, bursty arrivals), generated from fixed seeds.
 
-roofline: the simulation is bound by VALU instruction issue (integer
-scheduling and a short fp64 roofline per iteration; no dense contraction,
-negligible HBM traffic).  ``achieved`` is the algorithmic instruction count
-of the dominant simulation kernel divided by its HIP-event duration:
-  per simulated iteration  U = 80 wave64 VALU instructions
-      (the roofline: 14 int->fp64 conversions, 14 fp64 multiplies, 7 maxes,
-       6 adds, 1 multiply, 1 add, 1 ceil, 1 fp64->int = 45; five batch sums
-       as 6-step wave reductions = 30; arrival compare and clock update = 5)
-  per request-iteration    S = 16/64 (16 lane operations on a 64-lane wave:
-       phase / block-boundary tests, budget share, sum contributions,
-       token / context / gap / clock updates, finish test)
-with request-iterations counted as decode tokens + one prefill iteration
-per finished request (a lower bound).  Peak = 256 CUs x 4 SIMDs x 2.4 GHz /
-4 cycles per wave64 instruction = 614.4 G instructions/s.
+roofline: the simulation is bound by instruction issue (integer scheduling
+and a short fp64 roofline per iteration; no dense contraction, negligible HBM
+traffic).  ``achieved`` is the algorithmic VALU instruction count of the
+dominant simulation kernel divided by its HIP-event duration, with
+  U = 21 wave64 VALU instructions per simulated iteration,
+the least work any implementation of the method does per iteration once the
+batch sums are stepped incrementally: the prefill- and decode-attention
+operators' FLOPs and bytes stepped by their integer increments (2, one lane
+each), divided by peak and bandwidth (2) and maxed (1), their times brought
+into one lane (2), the fixed-order layer sum (5), times layers plus the LM
+head (2), ceil and the 1 ns floor (2), the clock (1), the used-block time
+integral (2), the block-boundary and arrival tests (2).  Scheduling events
+(admissions, finishes, preemptions) are not counted, so the fraction is a
+lower bound.  Peak = 256 CUs x 4 SIMDs x 2.4 GHz / 4 cycles per wave64
+instruction = 614.4 G instructions/s.
 """
 from __future__ import annotations
 
@@ -41,8 +42,7 @@ if ROOT not in sys.path:
 
 METRIC = "simulated requests/sec across sweep on 1 MI355X; % VALU-issue peak"
 VALU_ISSUE_PEAK = 256 * 4 * 2.4e9 / 4.0   # wave64 VALU instructions per second
-U_ITER = 80.0
-S_REQ_ITER = 16.0 / 64.0
+U_ITER = 21.0
 KERNEL_NAMES = ("sim_kernel<1>", "sim_kernel<2>", "sim_kernel<4>")
 
 
@@ -88,8 +88,7 @@ def recorded_traffic(config, kernel):
 
 
 def algorithmic_instructions(out):
-    ri = out["decode_tokens"].astype(np.float64) + out["n_done"].astype(np.float64)
-    return U_ITER * out["n_iters"].astype(np.float64) + S_REQ_ITER * ri
+    return U_ITER * out["n_iters"].astype(np.float64)
 
 
 def kernel_class(max_batch):
