@@ -495,13 +495,21 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
     // stretch ends: tokens and the per-request gap by the iteration count,
     // block boundaries by a countdown per slot) and step the two attention
     // operators' FLOPs and bytes by exact integer increments; the other
-    // operators' times are constant.  Decodes that finish are recorded in
-    // place and leave holes, removed when the stretch ends; the sums are then
-    // re-derived for the next segment of the stretch.  The iteration that ends
-    // a segment (first finish, head prefill completion, iteration cap) is
-    // known when it starts.  The clock runs in fp64, exact below 2^53.
-    // Decodes hold slots [0, nD) and prefills the slots after them:
-    // prefills receive tokens in slot order, so they complete in slot order.
+    // operators' times are constant.  Within a stretch:
+    //   * decodes that finish are recorded in place and leave holes, removed
+    //     when the stretch ends;
+    //   * when the head prefill completes (its first one), it joins the
+    //     decodes, and the rest of the chunk budget may admit the next trace
+    //     request as the new head prefill, if that one does not complete in
+    //     the same iteration;
+    // after either event the sums are re-derived for the next segment.  The
+    // iteration that ends a segment (first finish, head prefill completion,
+    // iteration cap) is known when it starts.  The clock runs in fp64,
+    // exact below 2^53.  A decode joining at iteration g is stored shifted
+    // by g (tokens - g, remaining + g, room + g), so one iteration count
+    // advances every decode alike.  Decodes hold slots [0, nD) and prefills
+    // the slots after them: prefills receive tokens in slot order, so they
+    // complete in slot order.
     if (nrun > 0) {
       const int nch0 = ((nrun + 63) >> 6) < NCH ? ((nrun + 63) >> 6) : NCH;
       int nD = 0;
@@ -520,24 +528,26 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
           rr[j] = dec ? h.room : -0x40000000;
         }
       }
-      const int npf = nrun - nD;
+      int npf = nrun - nD;
       if (npf > 0 && unlimited) go = false;
-      int ctx_p = 0, tgt_p = 0;
+      int ctx_p = 0, tgt_p = 0, fl_p = 0;  // the head prefill (slot nD)
       if (go && npf > 0) {
         const int jp = nD >> 6, lp = nD & 63;
         if (NCH == 1 || jp == 0) {
           ctx_p = rdl(h0.ctx, lp);
           tgt_p = rdl(h0.tgt, lp);
+          fl_p = rdl(h0.fl, lp);
         } else {
           ctx_p = __builtin_amdgcn_readfirstlane(L.x_ctx[(jp - 1) * 64 + lp]);
           tgt_p = __builtin_amdgcn_readfirstlane(L.x_tgt[(jp - 1) * 64 + lp]);
+          fl_p = __builtin_amdgcn_readfirstlane(L.x_fl[(jp - 1) * 64 + lp]);
         }
         if (tgt_p - ctx_p <= K - nD) go = false;  // the head prefill completes now
       }
       constexpr int64_t kT52 = (int64_t)1 << 52;
       if (n_iters >= A.iter_cap || t >= kT52) go = false;
       if (A.time_limit_ticks != 0 && (n_iters & 255) == 0) go = false;  // watchdog below
-      const int nchd = (nD + 63) >> 6;
+      int nchd = (nD + 63) >> 6;
       int nDa = nD, nruna = nrun;  // alive decodes and running requests
       // an admission would find a free slot and token budget
       auto adm_open = [&]() { return nruna < M && (unlimited || (npf == 0 && K - nDa > 0)); };
@@ -561,7 +571,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
           const int wd = 256 - (int)(n_iters & 255);
           stop_fix = wd < stop_fix ? wd : stop_fix;
         }
-        int dG = 0, seg0 = 0, q = 0, fin_at = 0, stop = 0;
+        int dG = 0, seg0 = 0, q = 0, fin_at = 0, stop = 0, cd_seg = 0;
         double Fw = 0.0, Bw = 0.0, dF = 0.0, dB = 0.0;
         double k_t0 = 0.0, k_t3 = 0.0, k_t4 = 0.0, k_t5 = 0.0, k_lm = 0.0;
         // Segment set-up at iteration dG: the alive decodes' first finishing
@@ -582,10 +592,10 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
             }
           }
           fin_at = nDa > 0 ? 0x7fffffff - mx - 1 : 0x3fffffff;
-          const int cd = cs + nDa * dG;
+          cd_seg = cs + nDa * dG;
           q = npf > 0 ? K - nDa : 0;
           const int64_t AP0 = (int64_t)q * ctx_p + ((int64_t)q * (q + 1)) / 2;
-          lane_work(roofc, nDa + q, q, AP0, q > 0 ? ctx_p + q : 0, nDa, cd, nDa, &Fw, &Bw);
+          lane_work(roofc, nDa + q, q, AP0, q > 0 ? ctx_p + q : 0, nDa, cd_seg, nDa, &Fw, &Bw);
           const double dX = roofc.is_attp ? (double)((int64_t)q * q)
                                           : (roofc.is_attd ? (double)nDa : 0.0);
           const double dY = roofc.is_attp ? (double)q : (roofc.is_attd ? (double)nDa : 0.0);
@@ -605,105 +615,253 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
           }
           seg0 = dG;
         };
+        // a segment's token bookkeeping, through iteration dG - 1
+        auto close_segment = [&]() {
+          const int len = dG - seg0;
+          pf_tok += (int64_t)q * len;
+          dec_tok += (int64_t)nDa * len;
+          ctx_p += q * len;
+          if (NB - freeb > peak) peak = NB - freeb;
+          seg0 = dG;
+        };
         const double kT52d = 4503599627370496.0;
         double thr = next < N ? __builtin_fmin((double)rdl64(w_arr, next - wbase), kT52d) : kT52d;
         // lane 1 carries the clock, the block-time integral, the iteration
-        // time and the largest iteration time of the finished segments
+        // time and the largest iteration time since the decodes' gaps were
+        // last brought up to date
         double t_d = (double)t, ub = ubns, it = 0.0, em = 0.0;
         setup();
-        for (;;) {
-          if (nneed > 0) {
-            freeb -= nneed;
-#pragma unroll
-            for (int j = 0; j < NCH; ++j)
-              if (j < nchd) rr[j] += rr[j] == dG ? B : 0;
-          }
-          const double used_d = (double)(NB - freeb);
-          // prefill attention (lane 1) and decode attention (lane 2, moved
-          // to lane 1), then the layer sum in the fixed operator order
-          const double tl = __builtin_fmax(Fw * iF, Bw * iB);
-          const double t2 = dpp_f64<0x101>(tl);
-          double lay = k_t0 + tl;
-          lay = lay + t2;
-          lay = lay + k_t3;
-          lay = lay + k_t4;
-          lay = lay + k_t5;
-          double tot = A.n_layers * lay;
-          tot = tot + k_lm;
-          it = __builtin_fmax(ceil(tot), 1.0);
-          ub = ub + used_d * it;
-          t_d = t_d + it;
-          Fw = Fw + dF;
-          Bw = Bw + dB;
-          if (dG == fin_at) {
-            // Alive decodes emitting their last token finish at the end of
-            // this iteration.  Iteration times never fall within a segment,
-            // so the largest so far is the larger of em and this one.
-            em = __builtin_fmax(em, it);
-            const int64_t t_end = (int64_t)rdl_f64(t_d, 1);
-            const int64_t gx = (int64_t)rdl_f64(em, 1);
-            int nfin = 0, l_freed = 0;
-#pragma unroll
-            for (int j = 0; j < NCH; ++j) {
-              if (j < nchd) {
-                const int e = (j - 1) * 64 + lane;
-                const int rem0 = j == 0 ? h0.rem : L.x_rem[e];
-                const bool fin = rr[j] >= 0 && rem0 - 1 == dG;
-                const uint64_t fm = ballot(fin);
-                if (fm != 0) {
-                  const int ctx0 = j == 0 ? h0.ctx : L.x_ctx[e];
-                  const int64_t gap0 = j == 0 ? h0.gap : L.x_gap[e];
-                  record_done(fin, j * 64 + lane, t_end, gx > gap0 ? gx : gap0,
-                              n_done + nfin + rank_below(fm));
-                  l_freed += fin ? divB(ctx0 + rr[j]) : 0;  // held blocks
-                  rr[j] = fin ? -0x40000000 : rr[j];
-                  nfin += popc(fm);
-                }
-              }
-            }
-            // the segment's bookkeeping, through this iteration
-            const int len = dG + 1 - seg0;
-            pf_tok += (int64_t)q * len;
-            dec_tok += (int64_t)nDa * len;
-            ctx_p += q * len;
-            if (NB - freeb > peak) peak = NB - freeb;
-            freeb += wsum(l_freed);
-            n_done += nfin;
-            nDa -= nfin;
-            nruna -= nfin;
-            ++dG;
-            seg0 = dG;
-            if (nruna == 0) break;
-            if ((npre > 0 || nwait > 0) && adm_open() && !(head_need >= 0 && head_need > freeb))
-              break;  // the freed slot or blocks may admit
-            setup();
-          } else {
-            ++dG;
-          }
-          if (dG == stop) break;
-          // the next iteration: arrivals, then block boundaries
+        // the checks before iteration dG: arrivals, then block boundaries;
+        // false ends the stretch
+        auto next_ok = [&]() -> bool {
           if ((ballot(t_d >= thr) & 2ull) != 0) {
             t = (int64_t)rdl_f64(t_d, 1);
-            if (t >= kT52) break;
+            if (t >= kT52) return false;
             intake();
             thr = next < N ? __builtin_fmin((double)rdl64(w_arr, next - wbase), kT52d) : kT52d;
-            if ((npre > 0 || nwait > 0) && adm_open() && head_need < 0) break;  // a new head
+            if ((npre > 0 || nwait > 0) && adm_open() && head_need < 0) return false;  // a new head
           }
           nneed = 0;
 #pragma unroll
           for (int j = 0; j < NCH; ++j)
             if (j < nchd) nneed += popc(ballot(rr[j] == dG));
-          if (nneed > freeb) break;
+          return nneed <= freeb;
+        };
+        bool more = true;
+        while (more) {
+          // steady iterations up to the segment's last
+          while (dG != stop) {
+            if (nneed > 0) {
+              freeb -= nneed;
+#pragma unroll
+              for (int j = 0; j < NCH; ++j)
+                if (j < nchd) rr[j] += rr[j] == dG ? B : 0;
+            }
+            const double used_d = (double)(NB - freeb);
+            // prefill attention (lane 1) and decode attention (lane 2, moved
+            // to lane 1), then the layer sum in the fixed operator order
+            const double tl = __builtin_fmax(Fw * iF, Bw * iB);
+            const double t2 = dpp_f64<0x101>(tl);
+            double lay = k_t0 + tl;
+            lay = lay + t2;
+            lay = lay + k_t3;
+            lay = lay + k_t4;
+            lay = lay + k_t5;
+            double tot = A.n_layers * lay;
+            tot = tot + k_lm;
+            it = __builtin_fmax(ceil(tot), 1.0);
+            ub = ub + used_d * it;
+            t_d = t_d + it;
+            Fw = Fw + dF;
+            Bw = Bw + dB;
+            if (dG == fin_at) {
+              // Alive decodes emitting their last token finish at the end of
+              // this iteration.  Iteration times never fall within a
+              // segment, so the largest so far is the larger of em and this.
+              em = __builtin_fmax(em, it);
+              const int64_t t_end = (int64_t)rdl_f64(t_d, 1);
+              const int64_t gx = (int64_t)rdl_f64(em, 1);
+              int nfin = 0, l_freed = 0;
+#pragma unroll
+              for (int j = 0; j < NCH; ++j) {
+                if (j < nchd) {
+                  const int e = (j - 1) * 64 + lane;
+                  const int rem0 = j == 0 ? h0.rem : L.x_rem[e];
+                  const bool fin = rr[j] >= 0 && rem0 - 1 == dG;
+                  const uint64_t fm = ballot(fin);
+                  if (fm != 0) {
+                    const int ctx0 = j == 0 ? h0.ctx : L.x_ctx[e];
+                    const int64_t gap0 = j == 0 ? h0.gap : L.x_gap[e];
+                    record_done(fin, j * 64 + lane, t_end, gx > gap0 ? gx : gap0,
+                                n_done + nfin + rank_below(fm));
+                    l_freed += fin ? divB(ctx0 + rr[j]) : 0;  // held blocks
+                    rr[j] = fin ? -0x40000000 : rr[j];
+                    nfin += popc(fm);
+                  }
+                }
+              }
+              ++dG;
+              close_segment();
+              freeb += wsum(l_freed);
+              n_done += nfin;
+              nDa -= nfin;
+              nruna -= nfin;
+              if (nruna == 0 || ((npre > 0 || nwait > 0) && adm_open() &&
+                                 !(head_need >= 0 && head_need > freeb))) {
+                more = false;  // nothing runs, or the freed slot or blocks may admit
+                break;
+              }
+              setup();
+            } else {
+              ++dG;
+            }
+            if (!next_ok()) {
+              more = false;
+              break;
+            }
+          }
+          if (!more) break;
+            // The head prefill completes in this iteration (or the cap /
+            // watchdog is reached).  Its first completion, with no decode
+            // finishing here, is handled in place; everything else runs on
+            // the general path.
+            if (stop >= stop_fix || npf != 1 || dG == fin_at ||
+                (fl_p & (FL_FIRST | FL_STALE)) != 0)
+              break;
+            const int CD = cd_seg + nDa * (dG - seg0);  // decode keys at this iteration
+            close_segment();
+            const int left = tgt_p - ctx_p;
+            const int R1 = K - nDa - left;  // budget left after the completing prefill
+            int adm = 0, id_h = 0, tgt_h = 0, o_h = 0, need_h = 0;
+            if ((npre > 0 || nwait > 0) && nruna < M && R1 > 0) {
+              if (npre > 0 || nrun >= 64 * NCH) break;  // queue candidates, full slots
+              const TraceRec r = rec[next_new];
+              if (P.may_reject && (int64_t)r.prompt + (int64_t)r.output > cap_tok) break;
+              need_h = divB(r.prompt + B - 1);
+              if (need_h > freeb - nneed) {
+                head_need = need_h;  // the head waits for blocks
+              } else {
+                if (r.prompt <= R1) break;  // it would complete at once
+                adm = 1;
+                id_h = next_new;
+                tgt_h = r.prompt;
+                o_h = r.output;
+              }
+            }
+            // reserve, admit, price the iteration with both prefills
+            if (nneed > 0) {
+              freeb -= nneed;
+#pragma unroll
+              for (int j = 0; j < NCH; ++j)
+                if (j < nchd) rr[j] += rr[j] == dG ? B : 0;
+            }
+            if (adm) freeb -= need_h;
+            const int q_new = adm ? R1 : 0;
+            const int TP = left + q_new;
+            const int64_t AP = (int64_t)left * ctx_p + ((int64_t)left * (left + 1)) / 2 +
+                               ((int64_t)q_new * (q_new + 1)) / 2;
+            double iter_d;
+            const int64_t iter_ns = iteration_ns(roofc, A.n_layers, iF, iB, nDa + TP, TP, AP,
+                                                 tgt_p + q_new, nDa, CD, nDa + 1, &iter_d);
+            const int64_t t_beg = (int64_t)rdl_f64(t_d, 1);
+            const int64_t t_end = t_beg + iter_ns;
+            ub = ub + (double)(NB - freeb) * iter_d;
+            t_d = t_d + iter_d;
+            if (NB - freeb > peak) peak = NB - freeb;
+            pf_tok += TP;
+            dec_tok += nDa;
+            // the decodes' gaps include this iteration and the segment before
+            // it (whose largest time is its last, it); the new decode's do not
+            em = __builtin_fmax(__builtin_fmax(em, it), iter_d);
+            const int64_t gx = (int64_t)rdl_f64(em, 1);
+#pragma unroll
+            for (int j = 0; j < NCH; ++j) {
+              if (j < nchd) {
+                const bool al = rr[j] >= 0;
+                if (j == 0) {
+                  h0.gap = al && gx > h0.gap ? gx : h0.gap;
+                } else {
+                  const int e = (j - 1) * 64 + lane;
+                  const int64_t g = L.x_gap[e];
+                  L.x_gap[e] = al && gx > g ? gx : g;
+                }
+              }
+            }
+            em = 0.0;
+            it = 0.0;
+            // the completed prefill emits its first token and joins the
+            // decodes at iteration dG + 1
+            {
+              const int js = nD >> 6, ls = nD & 63, g1 = dG + 1;
+              int room_s, id_s;
+              if (NCH == 1 || js == 0) {
+                room_s = rdl(h0.room, ls);
+                id_s = L.id[nD];
+                h0.ctx = lane == ls ? tgt_p - g1 : h0.ctx;
+                h0.rem = lane == ls ? h0.rem + g1 : h0.rem;
+                h0.fl = lane == ls ? (h0.fl | FL_FIRST) : h0.fl;
+              } else {
+                const int e = (js - 1) * 64 + ls;
+                room_s = __builtin_amdgcn_readfirstlane(L.x_room[e]);
+                id_s = L.id[nD];
+                L.x_ctx[e] = tgt_p - g1;  // every lane stores the same values
+                L.x_rem[e] = L.x_rem[e] + g1;
+                L.x_fl[e] = L.x_fl[e] | FL_FIRST;
+              }
+              id_s = __builtin_amdgcn_readfirstlane(id_s);
+              RT[id_s].first = t_end;
+#pragma unroll
+              for (int j = 0; j < NCH; ++j)
+                if (j == js) rr[j] = lane == ls ? room_s + g1 : rr[j];
+              ++nD;
+              ++nDa;
+              nchd = (nD + 63) >> 6;
+            }
+            if (adm) {
+              // the admitted request becomes the head prefill in slot nrun
+              const int js = nrun >> 6, ls = nrun & 63;
+              if (NCH == 1 || js == 0) {
+                h0.ctx = lane == ls ? q_new : h0.ctx;
+                h0.tgt = lane == ls ? tgt_h : h0.tgt;
+                h0.rem = lane == ls ? o_h : h0.rem;
+                h0.room = lane == ls ? need_h * B - tgt_h : h0.room;
+                h0.fl = lane == ls ? 0 : h0.fl;
+                h0.q = lane == ls ? 0 : h0.q;
+                h0.gap = lane == ls ? 0 : h0.gap;
+              } else {
+                const int e = (js - 1) * 64 + ls;  // every lane stores the same values
+                L.x_ctx[e] = q_new;
+                L.x_tgt[e] = tgt_h;
+                L.x_rem[e] = o_h;
+                L.x_room[e] = need_h * B - tgt_h;
+                L.x_fl[e] = 0;
+                L.x_q[e] = 0;
+                L.x_gap[e] = 0;
+              }
+              L.id[nrun] = id_h;
+              L.npre[nrun] = 0;
+              RT[id_h].admit = t_beg;  // first admission
+              ++nrun;
+              ++nruna;
+              ++next_new;
+              if (--nwait == 0) next_new = next;
+              head_need = -1;
+              ctx_p = q_new;
+              tgt_p = tgt_h;
+              fl_p = 0;
+            } else {
+              npf = 0;
+            }
+            ++dG;
+            seg0 = dG;
+            if ((npre > 0 || nwait > 0) && adm_open() && !(head_need >= 0 && head_need > freeb))
+              break;  // the head may be admitted next
+            setup();
+          if (!next_ok()) break;
         }
         // the last segment's bookkeeping, the point's counters, the decodes
         // (finished ones get rem 0) and the head prefill, then close the holes
-        {
-          const int len = dG - seg0;
-          pf_tok += (int64_t)q * len;
-          dec_tok += (int64_t)nDa * len;
-          ctx_p += q * len;
-        }
-        if (NB - freeb > peak) peak = NB - freeb;
+        close_segment();
         em = __builtin_fmax(em, it);
         t = (int64_t)rdl_f64(t_d, 1);
         ubns = rdl_f64(ub, 1);
