@@ -129,7 +129,8 @@ LaneCoef lane_coef(const CostCoef& c) {
 
 // Upper bounds of every FLOP / byte count and of the iteration time for a
 // point whose requests hold at most max_po tokens.
-bool exact_and_bounded(const CostCoef& c, int64_t max_po, int M, int K, double iF, double iB) {
+bool exact_and_bounded(const CostCoef& c, int64_t max_po, int M, int K, double iF, double iB,
+                       int* lg_iter) {
   const double po = (double)max_po;
   const double T = K > 0 ? (double)K : (double)M * po;   // tokens per iteration
   const double AP = T * po;                             // sum q*(c0+q) >= causal pairs
@@ -148,7 +149,12 @@ bool exact_and_bounded(const CostCoef& c, int64_t max_po, int M, int K, double i
   }
   // per-lane int32 partial sums (tokens, keys) must not overflow either
   if (T * 4 > 2147483647.0 || CD * 4 > 2147483647.0) return false;
-  return tmax < 1125899906842624.0;  // 2^50 ns per iteration
+  if (!(tmax < 1125899906842624.0)) return false;  // 2^50 ns per iteration
+  // a power of two above twice the bound (ceil and rounding order add less)
+  int lg = 1;
+  while ((double)((int64_t)1 << lg) < 2.0 * (tmax + 2.0)) ++lg;
+  *lg_iter = lg;
+  return true;
 }
 
 // Longest-expected-first ordering key: a rough count of iterations.  Under
@@ -343,7 +349,7 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
     d.out_index = i;
     d.may_reject = ts.max_po > d.cap_tokens ? 1 : 0;
     if (!exact_and_bounded(coef, ts.max_po, p.max_batch, p.chunk_size, d.inv_flops_ns,
-                           d.inv_bw_ns))
+                           d.inv_bw_ns, &d.lg_iter))
       return TS_ERR_UNSUPPORTED;
     est[(size_t)i] = work_estimate(ts, d.n, p.max_batch, p.chunk_size, p.peak_flops, p.mem_bw,
                                    (double)weights);

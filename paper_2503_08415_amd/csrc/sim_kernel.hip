@@ -571,9 +571,13 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
           const int wd = 256 - (int)(n_iters & 255);
           stop_fix = wd < stop_fix ? wd : stop_fix;
         }
-        int dG = 0, seg0 = 0, q = 0, fin_at = 0, stop = 0, cd_seg = 0;
+        int dG = 0, seg0 = 0, q = 0, fin_at = 0, stop = 0, stop_hard = 0, cd_seg = 0;
+        bool watch = false;
         double Fw = 0.0, Bw = 0.0, dF = 0.0, dB = 0.0;
         double k_t0 = 0.0, k_t3 = 0.0, k_t4 = 0.0, k_t5 = 0.0, k_lm = 0.0;
+        const double kT52d = 4503599627370496.0;
+        double thr = next < N ? __builtin_fmin((double)rdl64(w_arr, next - wbase), kT52d) : kT52d;
+        double t_d = (double)t, ub = ubns, it = 0.0, em = 0.0;
         // Segment set-up at iteration dG: the alive decodes' first finishing
         // iteration and key sum, the head prefill's chunk, every operator's
         // work and its per-iteration step, and the segment's last iteration.
@@ -608,11 +612,17 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
           k_t4 = dpp_f64<0x103>(tl0);
           k_t5 = dpp_f64<0x104>(tl0);
           k_lm = dpp_f64<0x105>(tl0);
-          stop = stop_fix;
+          // every iteration is below 2^lg_iter ns: this many keep the fp64
+          // clock below 2^52
+          const int64_t ks = (kT52 - (int64_t)rdl_f64(t_d, 1)) >> P.lg_iter;
+          stop_hard = ks < (int64_t)(stop_fix - dG) ? dG + (ks > 0 ? (int)ks : 0) : stop_fix;
+          stop = stop_hard;
           if (q > 0) {  // the head prefill completes in iteration kc
             const int kc = dG + (tgt_p - ctx_p - 1) / q;
             stop = kc < stop ? kc : stop;
           }
+          // arrivals matter within the segment only if one could be admitted
+          watch = adm_open() && npre == 0 && nwait == 0;
           seg0 = dG;
         };
         // a segment's token bookkeeping, through iteration dG - 1
@@ -624,17 +634,11 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
           if (NB - freeb > peak) peak = NB - freeb;
           seg0 = dG;
         };
-        const double kT52d = 4503599627370496.0;
-        double thr = next < N ? __builtin_fmin((double)rdl64(w_arr, next - wbase), kT52d) : kT52d;
-        // lane 1 carries the clock, the block-time integral, the iteration
-        // time and the largest iteration time since the decodes' gaps were
-        // last brought up to date
-        double t_d = (double)t, ub = ubns, it = 0.0, em = 0.0;
         setup();
         // the checks before iteration dG: arrivals, then block boundaries;
         // false ends the stretch
         auto next_ok = [&]() -> bool {
-          if ((ballot(t_d >= thr) & 2ull) != 0) {
+          if (watch && (ballot(t_d >= thr) & 2ull) != 0) {
             t = (int64_t)rdl_f64(t_d, 1);
             if (t >= kT52) return false;
             intake();
@@ -651,12 +655,10 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
         while (more) {
           // steady iterations up to the segment's last
           while (dG != stop) {
-            if (nneed > 0) {
-              freeb -= nneed;
+            freeb -= nneed;
 #pragma unroll
-              for (int j = 0; j < NCH; ++j)
-                if (j < nchd) rr[j] += rr[j] == dG ? B : 0;
-            }
+            for (int j = 0; j < NCH; ++j)
+              if (j < nchd) rr[j] += rr[j] == dG ? B : 0;
             const double used_d = (double)(NB - freeb);
             // prefill attention (lane 1) and decode attention (lane 2, moved
             // to lane 1), then the layer sum in the fixed operator order
@@ -706,6 +708,9 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
               n_done += nfin;
               nDa -= nfin;
               nruna -= nfin;
+              t = (int64_t)rdl_f64(t_d, 1);  // arrivals up to the clock
+              intake();
+              thr = next < N ? __builtin_fmin((double)rdl64(w_arr, next - wbase), kT52d) : kT52d;
               if (nruna == 0 || ((npre > 0 || nwait > 0) && adm_open() &&
                                  !(head_need >= 0 && head_need > freeb))) {
                 more = false;  // nothing runs, or the freed slot or blocks may admit
@@ -725,11 +730,14 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
             // watchdog is reached).  Its first completion, with no decode
             // finishing here, is handled in place; everything else runs on
             // the general path.
-            if (stop >= stop_fix || npf != 1 || dG == fin_at ||
+            if (stop >= stop_hard || npf != 1 || dG == fin_at ||
                 (fl_p & (FL_FIRST | FL_STALE)) != 0)
               break;
             const int CD = cd_seg + nDa * (dG - seg0);  // decode keys at this iteration
             close_segment();
+            t = (int64_t)rdl_f64(t_d, 1);  // arrivals up to the clock
+            intake();
+            thr = next < N ? __builtin_fmin((double)rdl64(w_arr, next - wbase), kT52d) : kT52d;
             const int left = tgt_p - ctx_p;
             const int R1 = K - nDa - left;  // budget left after the completing prefill
             int adm = 0, id_h = 0, tgt_h = 0, o_h = 0, need_h = 0;
@@ -763,7 +771,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
             double iter_d;
             const int64_t iter_ns = iteration_ns(roofc, A.n_layers, iF, iB, nDa + TP, TP, AP,
                                                  tgt_p + q_new, nDa, CD, nDa + 1, &iter_d);
-            const int64_t t_beg = (int64_t)rdl_f64(t_d, 1);
+            const int64_t t_beg = t;
             const int64_t t_end = t_beg + iter_ns;
             ub = ub + (double)(NB - freeb) * iter_d;
             t_d = t_d + iter_d;

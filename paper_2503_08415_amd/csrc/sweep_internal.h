@@ -29,6 +29,7 @@ struct __attribute__((aligned(16))) DevPoint {
   int32_t n;            // requests in the trace
   int32_t out_index;    // index of the point's results
   int32_t may_reject;   // 1 if some request of the trace exceeds cap_tokens
+  int32_t lg_iter;      // every iteration takes less than 2^lg_iter ns
 };
 
 // Integer coefficients of the per-operator roofline (exact below 2^53):
