@@ -237,8 +237,11 @@ int tso_simulate_point(const tso_model *m, const tso_trace *tr, const tso_point 
   if (!m || !tr || !p || !out) return TSO_ERR_ARG;
   if (tr->n < 0 || (tr->n > 0 && (!tr->arrival_ns || !tr->prompt_len || !tr->output_len)))
     return TSO_ERR_ARG;
-  if (p->max_batch < 1 || p->block_size < 1 || p->policy != 0) return TSO_ERR_ARG;
+  if (p->max_batch < 1 || p->block_size < 1) return TSO_ERR_ARG;
+  if (p->policy < TSO_POLICY_MIXED || p->policy > TSO_POLICY_STATIC) return TSO_ERR_ARG;
   if (p->chunk_size != 0 && p->chunk_size < p->max_batch) return TSO_ERR_ARG;
+  if (p->policy == TSO_POLICY_PREFILL_FIRST && p->chunk_size != 0) return TSO_ERR_ARG;
+  if (p->admit_mem_permille < 0 || p->admit_mem_permille > 1000) return TSO_ERR_ARG;
   tso_derived dv;
   int rc = tso_derive(m, p, &dv);
   if (rc != TSO_OK) return rc;
@@ -256,6 +259,10 @@ int tso_simulate_point(const tso_model *m, const tso_trace *tr, const tso_point 
     if (i > 0 && arr[i] < arr[i - 1]) return TSO_ERR_ARG;
   }
   const int64_t NB = dv.num_blocks, b = p->block_size, M = p->max_batch, K = p->chunk_size;
+  const int policy = p->policy;
+  /* blocks a first admission may leave in use, and the reserve it may not touch */
+  const int64_t adm_cap = p->admit_mem_permille > 0 ? NB * p->admit_mem_permille / 1000 : NB;
+  const int64_t adm_reserve = NB - adm_cap;
   const double iF = dv.inv_flops_ns, iB = dv.inv_bw_ns;
 
   memset(out, 0, sizeof *out);
@@ -276,10 +283,12 @@ int tso_simulate_point(const tso_model *m, const tso_trace *tr, const tso_point 
   int64_t nlog = 0;
 
   /* A request that could not fit even alone is rejected up front: with
-   * recompute preemption it would otherwise never finish. */
+   * recompute preemption it would otherwise never finish.  So is one whose
+   * prompt alone exceeds what a first admission may use. */
   for (int32_t i = 0; i < N; i++) {
     rq *r = &rs[i];
-    r->phase = (NB == 0 || ceil_div((int64_t)plen[i] + olen[i], b) > NB) ? PH_REJECTED : PH_FUTURE;
+    r->phase = (NB == 0 || ceil_div((int64_t)plen[i] + olen[i], b) > NB ||
+                ceil_div(plen[i], b) > adm_cap) ? PH_REJECTED : PH_FUTURE;
     r->target = plen[i];
     r->admit = r->first = r->last = -1;
   }
@@ -311,13 +320,22 @@ int tso_simulate_point(const tso_model *m, const tso_trace *tr, const tso_point 
       break;
     }
 
+    /* Prefill-first: when the waiting head can be admitted now, the iteration
+     * admits and prefills only, and the decodes pause. */
+    int pf_iter = 0;
+    if (policy == TSO_POLICY_PREFILL_FIRST && wq.nw > 0 && nr < M) {
+      const rq *h = &rs[waiting[0]];
+      const int64_t room = h->admit < 0 ? free_blocks - adm_reserve : free_blocks;
+      pf_iter = ceil_div(h->target, b) <= room;
+    }
+
     /* 3. decode sequences whose next token starts a new block reserve it, in
      *    admission order; when no block is free the most recently admitted
      *    running request is preempted (recompute: its KV is dropped and it
      *    waits again, ordered by arrival) until the block fits. */
     int preempted = 0;
     int32_t n_pre_now = 0;
-    for (int32_t i = 0; i < nr; i++) {
+    for (int32_t i = 0; i < nr && !pf_iter; i++) {
       rq *r = &rs[running[i]];
       int need = (r->ctx >= r->target) && (r->ctx % b == 0);
       if (!need) continue;
@@ -355,7 +373,7 @@ int tso_simulate_point(const tso_model *m, const tso_trace *tr, const tso_point 
     for (int32_t i = 0; i < nr; i++) {
       rq *r = &rs[running[i]];
       if (r->ctx >= r->target) {
-        r->q = 1;
+        r->q = pf_iter ? 0 : 1;
       } else {
         int64_t left = r->target - r->ctx;
         int64_t q = unlimited ? left : (left < R ? left : R);
@@ -366,15 +384,20 @@ int tso_simulate_point(const tso_model *m, const tso_trace *tr, const tso_point 
 
     /* 5. FCFS admission (none in an iteration that preempted): the head of
      *    the waiting queue joins if its whole prefill target fits in free
-     *    blocks, the running set is below max batch and budget remains; no
-     *    skipping past a blocked head */
+     *    blocks (a first admission also leaves the reserve untouched), the
+     *    running set is below max batch and budget remains; no skipping past
+     *    a blocked head.  Static batching admits only into an empty running
+     *    set; prefill-first only in a prefill iteration. */
     int32_t n_adm = 0;
-    if (!preempted) {
+    int may_admit = !preempted;
+    if (policy == TSO_POLICY_STATIC && nr > 0) may_admit = 0;
+    if (policy == TSO_POLICY_PREFILL_FIRST && !pf_iter) may_admit = 0;
+    if (may_admit) {
       while (wq.nw > 0 && nr < M && (unlimited || R > 0)) {
         int32_t hidx = waiting[0];
         rq *r = &rs[hidx];
         int64_t need = ceil_div(r->target, b);
-        if (need > free_blocks) break;
+        if (need > (r->admit < 0 ? free_blocks - adm_reserve : free_blocks)) break;
         free_blocks -= need;
         r->alloc = (int32_t)need;
         int64_t q = unlimited ? r->target : (r->target < R ? r->target : R);
@@ -397,6 +420,7 @@ int tso_simulate_point(const tso_model *m, const tso_trace *tr, const tso_point 
       rq *r = &rs[running[i]];
       int64_t c0 = r->ctx;
       if (r->ctx >= r->target) {
+        if (r->q == 0) continue; /* paused by a prefill-first iteration */
         s.T += 1;
         s.n_D += 1;
         s.C_D += c0 + 1;
@@ -424,7 +448,7 @@ int tso_simulate_point(const tso_model *m, const tso_trace *tr, const tso_point 
     for (int32_t i = 0; i < nr; i++) {
       int32_t idx = running[i];
       rq *r = &rs[idx];
-      if (r->ctx >= r->target) {
+      if (r->ctx >= r->target && r->q > 0) {
         r->ctx += 1;
         r->gdone += 1;
         int64_t gap = t_end - r->last;
@@ -440,7 +464,7 @@ int tso_simulate_point(const tso_model *m, const tso_trace *tr, const tso_point 
           n_fin++;
           continue;
         }
-      } else if (r->q > 0) {
+      } else if (r->ctx < r->target && r->q > 0) {
         r->ctx += r->q;
         prefill_tokens += r->q;
         if (r->ctx == r->target && r->first < 0) {
@@ -521,6 +545,7 @@ int tso_simulate_point(const tso_model *m, const tso_trace *tr, const tso_point 
       if (ee > out->max_e2e_ns) out->max_e2e_ns = ee;
       if (r->last > out->last_finish_ns) out->last_finish_ns = r->last;
       if (tt <= slo_ttft && r->max_gap <= slo_tpot) out->slo_ok++;
+      if (r->max_gap <= slo_tpot) out->slo_tpot_ok++;
       if (check && r->gdone != olen[i]) nviol++;
     } else if (r->phase == PH_REJECTED) {
       rec.status = TSO_REQ_REJECTED;

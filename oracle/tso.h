@@ -38,6 +38,14 @@ extern "C" {
 enum { TSO_OK = 0, TSO_ERR_ARG = -1, TSO_ERR_UNSUPPORTED = -2, TSO_ERR_OOM = -3 };
 enum { TSO_POINT_OK = 0, TSO_POINT_NO_KV = 1, TSO_POINT_ITER_LIMIT = 2 };
 enum { TSO_REQ_PENDING = 0, TSO_REQ_DONE = 1, TSO_REQ_REJECTED = 2 };
+/* Scheduling policies (Sec. IV-A compares continuous with static batching;
+ * the prefill-first iteration is the validation target's default scheduler,
+ * Sec. III-C):
+ *   MIXED          continuous batching, prefill and decode in one iteration;
+ *   PREFILL_FIRST  an iteration either admits and prefills (decodes pause) or
+ *                  runs every decode; needs chunk_size 0;
+ *   STATIC         a batch is admitted only when nothing runs. */
+enum { TSO_POLICY_MIXED = 0, TSO_POLICY_PREFILL_FIRST = 1, TSO_POLICY_STATIC = 2 };
 
 typedef struct {
   int32_t n_layers, d_model, n_heads, n_kv_heads;
@@ -62,7 +70,12 @@ typedef struct {
   int32_t max_batch;
   int32_t chunk_size;          /* 0 = whole prompt in one iteration */
   int32_t trace_id;
-  int32_t policy;              /* 0 only */
+  int32_t policy;              /* TSO_POLICY_* */
+  int32_t admit_mem_permille;  /* 0 = off; else a first admission keeps used
+                                  blocks <= floor(num_blocks * this / 1000)
+                                  (Sec. IV-B, the maximum memory ratio for
+                                  new requests) */
+  int32_t pad;
 } tso_point;
 
 typedef struct {
@@ -78,6 +91,7 @@ typedef struct {
   int64_t p50_e2e_ns, p90_e2e_ns, p99_e2e_ns, p50_ttft_ns, p99_ttft_ns, slo_ok;
   double used_block_ns;
   uint64_t digest;
+  int64_t slo_tpot_ok;         /* finished with largest token gap <= the mTPOT SLO */
 } tso_point_out;
 
 typedef struct {

@@ -50,7 +50,8 @@ class Point(C.Structure):
     _fields_ = [("peak_flops", C.c_double), ("mem_bw", C.c_double),
                 ("capacity_bytes", C.c_int64), ("mem_util_permille", C.c_int32),
                 ("block_size", C.c_int32), ("max_batch", C.c_int32),
-                ("chunk_size", C.c_int32), ("trace_id", C.c_int32), ("policy", C.c_int32)]
+                ("chunk_size", C.c_int32), ("trace_id", C.c_int32), ("policy", C.c_int32),
+                ("admit_mem_permille", C.c_int32), ("pad", C.c_int32)]
 
 
 class Options(C.Structure):
@@ -76,7 +77,7 @@ POINT_OUT_DTYPE = np.dtype([
     ("sum_e2e_ns", "<i8"), ("max_e2e_ns", "<i8"), ("sum_tpot_num_ns", "<i8"),
     ("p50_e2e_ns", "<i8"), ("p90_e2e_ns", "<i8"), ("p99_e2e_ns", "<i8"),
     ("p50_ttft_ns", "<i8"), ("p99_ttft_ns", "<i8"), ("slo_ok", "<i8"),
-    ("used_block_ns", "<f8"), ("digest", "<u8")])
+    ("used_block_ns", "<f8"), ("digest", "<u8"), ("slo_tpot_ok", "<i8")])
 
 ITER_DTYPE = np.dtype([("t_start", "<i8"), ("iter_ns", "<i8"), ("n_decode", "<i4"),
                        ("n_prefill", "<i4"), ("tokens", "<i4"), ("used_blocks", "<i4"),
@@ -84,6 +85,7 @@ ITER_DTYPE = np.dtype([("t_start", "<i8"), ("iter_ns", "<i8"), ("n_decode", "<i4
                        ("n_finished", "<i4")])
 
 POINT_OK, POINT_NO_KV, POINT_ITER_LIMIT = 0, 1, 2
+POLICY_MIXED, POLICY_PREFILL_FIRST, POLICY_STATIC = 0, 1, 2
 REQ_PENDING, REQ_DONE, REQ_REJECTED = 0, 1, 2
 
 _lib = None
@@ -128,14 +130,15 @@ def _point(pts: dict, i: int) -> Point:
                  int(pts["capacity_bytes"][i]), int(pts["mem_util_permille"][i]),
                  int(pts["block_size"][i]), int(pts["max_batch"][i]),
                  int(pts["chunk_size"][i]), int(pts["trace_id"][i]),
-                 int(pts["policy"][i]) if "policy" in pts else 0)
+                 int(pts["policy"][i]) if "policy" in pts else 0,
+                 int(pts["admit_mem_permille"][i]) if "admit_mem_permille" in pts else 0, 0)
 
 
 def _single_point(p: dict) -> Point:
     return Point(float(p["peak_flops"]), float(p["mem_bw"]), int(p["capacity_bytes"]),
                  int(p.get("mem_util_permille", 1000)), int(p["block_size"]),
                  int(p["max_batch"]), int(p.get("chunk_size", 0)), int(p.get("trace_id", 0)),
-                 int(p.get("policy", 0)))
+                 int(p.get("policy", 0)), int(p.get("admit_mem_permille", 0)), 0)
 
 
 class _TraceKeep:

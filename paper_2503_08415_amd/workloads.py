@@ -70,7 +70,8 @@ BW_GRID8 = (1000000000000.0, 1389495494373.1377, 1930697728883.25,
 C4_CAPS = tuple(int(round(24e9 + i * 136e9 / 31)) for i in range(32))
 
 POINT_FIELDS = ("peak_flops", "mem_bw", "capacity_bytes", "mem_util_permille",
-                "block_size", "max_batch", "chunk_size", "trace_id", "policy")
+                "block_size", "max_batch", "chunk_size", "trace_id", "policy",
+                "admit_mem_permille")
 
 _NS = 1e9
 
@@ -167,6 +168,7 @@ def _points(rows):
         "chunk_size": np.asarray(pts["chunk_size"], dtype=np.int32),
         "trace_id": np.asarray(pts["trace_id"], dtype=np.int32),
         "policy": np.asarray(pts["policy"], dtype=np.int32),
+        "admit_mem_permille": np.asarray(pts["admit_mem_permille"], dtype=np.int32),
     }
 
 

@@ -22,12 +22,19 @@ def blocks(tokens, b):
     return -(-tokens // b)
 
 
-def brute(reqs, NB, b, M, K, cost):
-    """reqs: list of (arrival, p, o), sorted by arrival.  Returns records and counters."""
+def brute(reqs, NB, b, M, K, cost, policy=0, permille=0):
+    """reqs: list of (arrival, p, o), sorted by arrival.  Returns records and counters.
+
+    policy 0: mixed continuous batching; 1: prefill-first (an iteration that
+    can admit the waiting head only admits and prefills); 2: static batching
+    (admit only into an empty running set).  permille > 0 keeps first
+    admissions within floor(NB * permille / 1000) used blocks."""
     N = len(reqs)
+    cap = NB * permille // 1000 if permille else NB
+    reserve = NB - cap
     st = []
     for i, (a, p, o) in enumerate(reqs):
-        rej = NB == 0 or blocks(p + o, b) > NB
+        rej = NB == 0 or blocks(p + o, b) > NB or blocks(p, b) > cap
         st.append(dict(i=i, a=a, p=p, o=o, ph="rej" if rej else "future", ctx=0, tgt=p,
                        gd=0, seq=None, admit=-1, first=-1, last=-1, gap=0, npre=0, fin=-1))
     t, nxt, seq, iters = 0, 0, 0, 0
@@ -57,7 +64,14 @@ def brute(reqs, NB, b, M, K, cost):
             continue
         preempted = False
         grow = set()  # requests holding one extra (reserved) block this iteration
-        for r in running():
+
+        def room_for(h):
+            return free() - len(grow) - (reserve if h["admit"] < 0 else 0)
+
+        pf = False
+        if policy == 1 and waiting() and len(running()) < M:
+            pf = blocks(waiting()[0]["tgt"], b) <= room_for(waiting()[0])
+        for r in ([] if pf else running()):
             if r["ph"] != "run":
                 continue
             if not (r["ctx"] >= r["tgt"] and r["ctx"] % b == 0):
@@ -81,11 +95,17 @@ def brute(reqs, NB, b, M, K, cost):
                 q[r["i"]] = need if budget is None else min(need, budget)
                 if budget is not None:
                     budget -= q[r["i"]]
-        if not preempted:
+        paused = {r["i"] for r in run if pf and r["ctx"] >= r["tgt"]}
+        may = not preempted
+        if policy == 2 and run:
+            may = False
+        if policy == 1 and not pf:
+            may = False
+        if may:
             for h in waiting():
                 if len(running()) >= M or (budget is not None and budget <= 0):
                     break
-                if blocks(h["tgt"], b) > free() - len(grow):
+                if blocks(h["tgt"], b) > room_for(h):
                     break
                 seq += 1
                 h.update(ph="run", seq=seq)
@@ -98,6 +118,8 @@ def brute(reqs, NB, b, M, K, cost):
         used = NB - free() + len(grow)
         batch = []
         for r in run:
+            if r["i"] in paused:
+                continue
             if r["ctx"] >= r["tgt"]:
                 batch.append((1, r["ctx"], 0, 0))
             elif q[r["i"]] > 0:
@@ -107,6 +129,8 @@ def brute(reqs, NB, b, M, K, cost):
         t_end = t + dt
         iters += 1
         for r in run:
+            if r["i"] in paused:
+                continue
             if r["ctx"] >= r["tgt"]:
                 r["ctx"] += 1
                 r["gd"] += 1
@@ -140,11 +164,15 @@ def _random_case(rnd):
     M = rnd.choice([1, 2, 3, 5])
     K = rnd.choice([0, 0, M, M + 1, M + 4])
     NB = rnd.randint(1, 12)
+    policy = rnd.choice([0, 0, 1, 2])
+    if policy == 1:
+        K = 0
+    permille = rnd.choice([0, 0, 250, 500, 750, 1000])
     t, reqs = 0, []
     for _ in range(n):
         t += rnd.choice([0, 0, 1, 2, 5, 40])
         reqs.append((t, rnd.randint(1, 9), rnd.randint(1, 6)))
-    return reqs, NB, b, M, K
+    return reqs, NB, b, M, K, policy, permille
 
 
 @pytest.mark.parametrize("hw", ["unit", "roofline"])
@@ -154,19 +182,23 @@ def test_oracle_matches_brute_force(oracle, hw):
     iF, iB = 1e9 / F, 1e9 / BW
     cost = lambda batch: oracle.iter_ns(TOY, iF, iB, batch)
     n_pre_seen = 0
-    for case in range(400 if hw == "unit" else 150):
-        reqs, NB, b, M, K = _random_case(rnd)
+    seen = set()
+    for case in range(600 if hw == "unit" else 200):
+        reqs, NB, b, M, K, policy, permille = _random_case(rnd)
+        seen.add((policy, permille > 0))
         tr = {"arrival_ns": np.array([r[0] for r in reqs], np.int64),
               "prompt_len": np.array([r[1] for r in reqs], np.int32),
               "output_len": np.array([r[2] for r in reqs], np.int32)}
         pt = dict(peak_flops=F, mem_bw=BW, capacity_bytes=NB * b * 16, mem_util_permille=1000,
-                  block_size=b, max_batch=M, chunk_size=K)
+                  block_size=b, max_batch=M, chunk_size=K, policy=policy,
+                  admit_mem_permille=permille)
         out, req, _, viol = oracle.simulate_point(TOY, tr, pt)
         assert viol == 0
-        want, cnt = brute(reqs, NB, b, M, K, cost)
+        want, cnt = brute(reqs, NB, b, M, K, cost, policy, permille)
         got = [tuple(int(x) for x in r) for r in req]
-        assert got == want, (case, reqs, NB, b, M, K)
+        assert got == want, (case, reqs, NB, b, M, K, policy, permille)
         for k, v in cnt.items():
             assert out[k] == v, (k, case)
         n_pre_seen += cnt["n_preempt"]
     assert n_pre_seen > 20  # the random cases do exercise preemption
+    assert len(seen) == 6  # every policy, with and without the admission ratio

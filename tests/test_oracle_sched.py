@@ -38,7 +38,9 @@ def hand_point(case):
     nb, b = case["num_blocks"], case["block_size"]
     cap = nb * b * 16 if nb > 0 else 1   # the toy model stores 16 B of KV per token
     return dict(peak_flops=INF, mem_bw=INF, capacity_bytes=cap, mem_util_permille=1000,
-                block_size=b, max_batch=case["max_batch"], chunk_size=case["chunk_size"])
+                block_size=b, max_batch=case["max_batch"], chunk_size=case["chunk_size"],
+                policy=case.get("policy", 0),
+                admit_mem_permille=case.get("admit_mem_permille", 0))
 
 
 @pytest.mark.parametrize("case", HAND_CASES, ids=[c["name"] for c in HAND_CASES])
@@ -190,6 +192,15 @@ def test_statistics_definitions(oracle):
         assert out["sum_tpot_num_ns"] == int((req["finish_ns"][done] - req["first_token_ns"][done]).sum())
         ok = (ttft <= 2_000_000_000) & (req["max_gap_ns"][done] <= 60_000_000)
         assert out["slo_ok"] == int(ok.sum())
+        assert out["slo_tpot_ok"] == int((req["max_gap_ns"][done] <= 60_000_000).sum())
+        assert out["slo_ok"] <= out["slo_tpot_ok"] <= out["n_done"]
+        # a TTFT objective at the median separates the two counts
+        tight = int(np.median(ttft))
+        out2, _, _, _ = oracle.simulate_point(m, tr, p, slo_ttft_ns=tight,
+                                              slo_tpot_ns=60_000_000)
+        ok2 = (ttft <= tight) & (req["max_gap_ns"][done] <= 60_000_000)
+        assert out2["slo_ok"] == int(ok2.sum()) and out2["slo_tpot_ok"] == out["slo_tpot_ok"]
+        assert out2["slo_ok"] < out2["slo_tpot_ok"]
         assert out["last_finish_ns"] == int(req["finish_ns"][done].max())
         assert out["first_arrival_ns"] == int(tr["arrival_ns"][0])
 
@@ -238,7 +249,9 @@ def test_empty_trace_and_iteration_cap(oracle):
 
 def test_bad_arguments_rejected(oracle):
     tr = _trace([(0, 5, 5)])
-    for bad in (dict(A100, chunk_size=8), dict(A100, block_size=0), dict(A100, policy=1),
+    for bad in (dict(A100, chunk_size=8), dict(A100, block_size=0), dict(A100, policy=3),
+                dict(A100, policy=-1), dict(A100, policy=1, chunk_size=256),
+                dict(A100, admit_mem_permille=1001), dict(A100, admit_mem_permille=-1),
                 dict(A100, peak_flops=float("inf")), dict(A100, mem_util_permille=0)):
         with pytest.raises(oracle.OracleError):
             oracle.simulate_point(C1_MODEL, tr, bad)
