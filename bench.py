@@ -53,6 +53,11 @@ KERNEL_SOURCES = ("paper_2503_08415_amd/csrc/sim_kernel.hip",
                   "paper_2503_08415_amd/csrc/host.hip")
 
 
+def workloads_configs():
+    from paper_2503_08415_amd import workloads
+    return workloads.CONFIGS.keys()
+
+
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
@@ -128,7 +133,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--config", default="c5", choices=["c1", "c2", "c3", "c4", "c5"])
+    ap.add_argument("--config", default="c5", choices=sorted(workloads_configs()))
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="wall time budget of the oracle baseline sample (0 = skip)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",

@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define TS_ABI_VERSION 1
+#define TS_ABI_VERSION 2
 #define TS_MAX_BATCH 256 /* running-set cap per design point */
 
 /* call status */
@@ -76,6 +76,19 @@ extern "C" {
 #define TS_REQ_PENDING 0  /* not finished (iteration cap hit); other fields -1/0 */
 #define TS_REQ_DONE 1
 #define TS_REQ_REJECTED 2 /* could never fit; other fields -1/0 */
+
+/* ts_point.policy: how the local scheduler forms each iteration.
+ *   MIXED          continuous batching (Sec. II-B, Sec. IV-A): admissions join
+ *                  every iteration, prefills and decodes share it;
+ *   PREFILL_FIRST  an iteration either admits and prefills (running decodes
+ *                  pause) when the waiting head can be admitted, or runs
+ *                  every decode; the validation target's default scheduler
+ *                  (Sec. III-C).  Requires chunk_size 0;
+ *   STATIC         static batching (Sec. IV-A): a batch is admitted only into
+ *                  an empty running set and runs until every member ends. */
+#define TS_POLICY_MIXED 0
+#define TS_POLICY_PREFILL_FIRST 1
+#define TS_POLICY_STATIC 2
 
 /* ts_options.flags */
 #define TS_F_PER_REQUEST 1u /* also return per-request records */
@@ -116,7 +129,13 @@ typedef struct {
   int32_t chunk_size;         /* 0: prompts prefill in one iteration; else per-iteration
                                  token budget, max_batch <= chunk_size <= TS_MAX_TOKENS */
   int32_t trace_id;           /* index into the traces passed to create */
-  int32_t policy;             /* 0: FCFS continuous batching, recompute preemption */
+  int32_t policy;             /* TS_POLICY_*; FCFS order and recompute preemption in all */
+  int32_t admit_mem_permille; /* 0: off; 1..1000: a first admission keeps used blocks
+                                 <= floor(num_blocks * this / 1000), reserving the rest
+                                 for requests already admitted (Sec. IV-B's maximum
+                                 memory ratio for new requests); a request whose prompt
+                                 needs more than that is rejected */
+  int32_t reserved;           /* 0 */
 } ts_point;
 
 /* Per-request record (TS_F_PER_REQUEST): 40 bytes. */
@@ -129,10 +148,12 @@ typedef struct {
   int32_t status;         /* TS_REQ_* */
 } ts_req_result;
 
-/* Per-point result: 168 bytes.  Percentiles are nearest rank over finished
+/* Per-point result: 176 bytes.  Percentiles are nearest rank over finished
  * requests (-1 when none); TTFT = first_token - arrival, E2E = finish -
  * arrival, TPOT numerator = finish - first_token.  slo_ok counts finished
- * requests with TTFT <= slo_ttft_ns and max gap <= slo_tpot_ns.
+ * requests with TTFT <= slo_ttft_ns and max gap <= slo_tpot_ns; slo_tpot_ok
+ * those with max gap <= slo_tpot_ns (Sec. IV-B's two SLO throughputs are
+ * these counts over last_finish_ns - first_arrival_ns).
  * used_block_ns = sum over iterations of used blocks * iteration time (fp64).
  * digest = sum mod 2^64 of a 64-bit hash of every finished or rejected
  * request's record and index. */
@@ -144,6 +165,7 @@ typedef struct {
   int64_t p50_e2e_ns, p90_e2e_ns, p99_e2e_ns, p50_ttft_ns, p99_ttft_ns, slo_ok;
   double used_block_ns;
   uint64_t digest;
+  int64_t slo_tpot_ok;
 } ts_point_result;
 
 /* Options; pass NULL for all defaults. */

@@ -60,6 +60,7 @@ bool model_ok(const ts_model* m) {
 
 struct TraceStats {
   int64_t max_po = 0;     // largest prompt + output
+  int64_t max_p = 0;      // largest prompt
   double mean_p = 0, mean_o = 0, span_s = 0;
 };
 
@@ -292,6 +293,7 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
       if (a < 0 || (i > 0 && a < tr.arrival_ns[i - 1])) return TS_ERR_ARG;
       if (p < 1 || o < 1 || p > TS_MAX_TOKENS || o > TS_MAX_TOKENS) return TS_ERR_ARG;
       s.max_po = std::max<int64_t>(s.max_po, (int64_t)p + o);
+      s.max_p = std::max<int64_t>(s.max_p, p);
       sp += p;
       so += o;
     }
@@ -327,7 +329,10 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
     if (p.chunk_size != 0 && (p.chunk_size < p.max_batch || p.chunk_size > TS_MAX_TOKENS))
       return TS_ERR_ARG;
     if (p.trace_id < 0 || p.trace_id >= n_traces) return TS_ERR_ARG;
-    if (p.policy != 0) return TS_ERR_UNSUPPORTED;
+    if (p.policy < TS_POLICY_MIXED || p.policy > TS_POLICY_STATIC) return TS_ERR_UNSUPPORTED;
+    if (p.policy == TS_POLICY_PREFILL_FIRST && p.chunk_size != 0) return TS_ERR_ARG;
+    if (p.admit_mem_permille < 0 || p.admit_mem_permille > 1000 || p.reserved != 0)
+      return TS_ERR_ARG;
     // KV block budget: floor(capacity * util / 1000), minus the weights when
     // they share the memory, in whole blocks of block_size tokens
     const __int128 usable = ((__int128)p.capacity_bytes * p.mem_util_permille) / 1000;
@@ -347,7 +352,13 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
     d.trace_off = (int32_t)toff[(size_t)p.trace_id];
     d.n = traces[p.trace_id].n;
     d.out_index = i;
-    d.may_reject = ts.max_po > d.cap_tokens ? 1 : 0;
+    // blocks a first admission may leave in use; the rest is reserved
+    const int64_t adm_cap =
+        p.admit_mem_permille > 0 ? (int64_t)nb * p.admit_mem_permille / 1000 : (int64_t)nb;
+    d.policy = p.policy;
+    d.adm_reserve = (int32_t)((int64_t)nb - adm_cap);
+    d.cap_prompt = adm_cap * p.block_size;
+    d.may_reject = (ts.max_po > d.cap_tokens || ts.max_p > d.cap_prompt) ? 1 : 0;
     if (!exact_and_bounded(coef, ts.max_po, p.max_batch, p.chunk_size, d.inv_flops_ns,
                            d.inv_bw_ns, &d.lg_iter))
       return TS_ERR_UNSUPPORTED;

@@ -254,7 +254,7 @@ struct SlotLds {
   // finished-request statistics of the point, accumulated by LDS atomics
   unsigned long long sum_ttft, sum_e2e, sum_tpot, digest;
   long long max_e2e, last_fin;
-  unsigned int slo_ok;
+  unsigned int slo_ok, slo_tpot_ok;
   union {
     StageSlot stage[64];
     int64_t scratch[NCH * 64];
@@ -288,7 +288,13 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
   const TraceRec* __restrict__ rec = A.recs + P.trace_off;
   const int N = P.n, NB = P.num_blocks, B = P.block, M = P.max_batch, K = P.chunk;
   const bool unlimited = (K == 0);
-  const int64_t cap_tok = P.cap_tokens;
+  const int64_t cap_tok = P.cap_tokens, cap_prompt = P.cap_prompt;
+  const int policy = P.policy, adm_reserve = P.adm_reserve;
+  const bool pff = policy == TS_POLICY_PREFILL_FIRST;
+  // a request that could never fit, alone or within the admission ratio
+  auto rejected = [&](int32_t pr, int32_t ou) {
+    return (int64_t)pr + (int64_t)ou > cap_tok || (int64_t)pr > cap_prompt;
+  };
   const double iF = P.inv_flops_ns, iB = P.inv_bw_ns;
   const int oi = P.out_index;
   ts_req_result* RR = A.req ? A.req + (size_t)oi * (size_t)A.max_n : nullptr;
@@ -298,7 +304,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
   // statistics of finished / rejected requests: LDS accumulators, cleared
   // by every lane storing the same zeros (no lane-dependent branch)
   L.sum_ttft = 0; L.sum_e2e = 0; L.sum_tpot = 0; L.digest = 0;
-  L.max_e2e = -1; L.last_fin = -1; L.slo_ok = 0;
+  L.max_e2e = -1; L.last_fin = -1; L.slo_ok = 0; L.slo_tpot_ok = 0;
   __syncthreads();
   int n_rej = 0;
 
@@ -309,7 +315,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       bool rj = false;
       if (i < N) {
         const TraceRec r = rec[i];
-        rj = (int64_t)r.prompt + (int64_t)r.output > cap_tok;
+        rj = rejected(r.prompt, r.output);
       }
       if (rj) {
         atomicAdd(&L.digest, (unsigned long long)record_hash(i, -1, -1, -1, 0, 0, TS_REQ_REJECTED));
@@ -335,10 +341,10 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
 
   // arrival window: lane l holds record wbase + l
   int64_t w_arr = INT64_MAX;
-  int w_po = 0;
+  int w_rj = 0;  // 1: the record is rejected
   if (lane < N) {
     const TraceRec r = rec[lane];
-    w_arr = r.arrival_ns; w_po = r.prompt + r.output;
+    w_arr = r.arrival_ns; w_rj = rejected(r.prompt, r.output) ? 1 : 0;
   }
 
   Hot h0;  // chunk 0 in registers
@@ -355,7 +361,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       if (nn > next) {
         int add = nn - next;
         if (P.may_reject) {
-          const bool rj = lane >= next - wbase && lane < cnt && (int64_t)w_po > cap_tok;
+          const bool rj = lane >= next - wbase && lane < cnt && w_rj != 0;
           add -= popc(ballot(rj));
         }
         if (npre == 0 && nwait == 0) head_need = -1;
@@ -365,10 +371,10 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       if (cnt == 64 && nn < N) {
         wbase = nn;
         w_arr = INT64_MAX;
-        w_po = 0;
+        w_rj = 0;
         if (wbase + lane < N) {
           const TraceRec r = rec[wbase + lane];
-          w_arr = r.arrival_ns; w_po = r.prompt + r.output;
+          w_arr = r.arrival_ns; w_rj = rejected(r.prompt, r.output) ? 1 : 0;
         }
         continue;
       }
@@ -396,6 +402,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       atomicMax(&L.max_e2e, (long long)ee);
       atomicMax(&L.last_fin, (long long)t_end);
       if (tt <= A.slo_ttft_ns && gap <= A.slo_tpot_ns) atomicAdd(&L.slo_ok, 1u);
+      if (gap <= A.slo_tpot_ns) atomicAdd(&L.slo_tpot_ok, 1u);
       atomicAdd(&L.digest, (unsigned long long)record_hash(id, rt.admit, rt.first, t_end, gap,
                                                            npr, TS_REQ_DONE));
       if (RR) {
@@ -550,7 +557,14 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       int nchd = (nD + 63) >> 6;
       int nDa = nD, nruna = nrun;  // alive decodes and running requests
       // an admission would find a free slot and token budget
-      auto adm_open = [&]() { return nruna < M && (unlimited || (npf == 0 && K - nDa > 0)); };
+      auto adm_open = [&]() {
+        return policy != TS_POLICY_STATIC && nruna < M && (unlimited || (npf == 0 && K - nDa > 0));
+      };
+      // the waiting head is known not to fit in fb free blocks (a first
+      // admission also leaves the admission-ratio reserve)
+      auto head_blocked = [&](int fb) {
+        return head_need >= 0 && head_need > fb - (npre > 0 ? 0 : adm_reserve);
+      };
       int nneed = 0;
       if (go) {
         if (next < N && rdl64(w_arr, next - wbase) <= t) intake();
@@ -559,7 +573,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
           if (j < nchd) nneed += popc(ballot(rr[j] == 0));
         if (nneed > freeb) go = false;  // recompute preemption
         else if ((npre > 0 || nwait > 0) && adm_open() &&
-                 !(head_need >= 0 && head_need > freeb - nneed))
+                 !head_blocked(pff ? freeb : freeb - nneed))
           go = false;  // an admission may happen
       }
       if (go) {
@@ -711,8 +725,8 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
               t = (int64_t)rdl_f64(t_d, 1);  // arrivals up to the clock
               intake();
               thr = next < N ? __builtin_fmin((double)rdl64(w_arr, next - wbase), kT52d) : kT52d;
-              if (nruna == 0 || ((npre > 0 || nwait > 0) && adm_open() &&
-                                 !(head_need >= 0 && head_need > freeb))) {
+              if (nruna == 0 ||
+                  ((npre > 0 || nwait > 0) && adm_open() && !head_blocked(freeb))) {
                 more = false;  // nothing runs, or the freed slot or blocks may admit
                 break;
               }
@@ -741,12 +755,12 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
             const int left = tgt_p - ctx_p;
             const int R1 = K - nDa - left;  // budget left after the completing prefill
             int adm = 0, id_h = 0, tgt_h = 0, o_h = 0, need_h = 0;
-            if ((npre > 0 || nwait > 0) && nruna < M && R1 > 0) {
+            if (policy != TS_POLICY_STATIC && (npre > 0 || nwait > 0) && nruna < M && R1 > 0) {
               if (npre > 0 || nrun >= 64 * NCH) break;  // queue candidates, full slots
               const TraceRec r = rec[next_new];
-              if (P.may_reject && (int64_t)r.prompt + (int64_t)r.output > cap_tok) break;
+              if (P.may_reject && rejected(r.prompt, r.output)) break;
               need_h = divB(r.prompt + B - 1);
-              if (need_h > freeb - nneed) {
+              if (need_h > freeb - nneed - adm_reserve) {
                 head_need = need_h;  // the head waits for blocks
               } else {
                 if (r.prompt <= R1) break;  // it would complete at once
@@ -862,7 +876,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
             }
             ++dG;
             seg0 = dG;
-            if ((npre > 0 || nwait > 0) && adm_open() && !(head_need >= 0 && head_need > freeb))
+            if ((npre > 0 || nwait > 0) && adm_open() && !head_blocked(freeb))
               break;  // the head may be admitted next
             setup();
           if (!next_ok()) break;
@@ -927,12 +941,29 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       break;
     }
 
+    // Prefill-first: when the waiting head can be admitted now the
+    // iteration admits and prefills only and the decodes pause; otherwise it
+    // runs every decode and admits nothing.
+    bool pf_iter = false;
+    if (pff && (npre > 0 || nwait > 0) && nrun < M) {
+      int tgt_h;
+      if (npre > 0) {
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+        tgt_h = Q[qhead].target;
+      } else {
+        int i = next_new;  // the first candidate that is not rejected
+        while (P.may_reject && i < next - 1 && rejected(rec[i].prompt, rec[i].output)) ++i;
+        tgt_h = rec[i].prompt;
+      }
+      pf_iter = divB(tgt_h + B - 1) <= freeb - (npre > 0 ? 0 : adm_reserve);
+    }
+
     // ---- 3. reserve a block for decodes crossing a block boundary
     int nch = (nrun + 63) >> 6;
     nch = nch < NCH ? nch : NCH;
     int nneed = 0;
 #pragma nounroll
-    for (int j = 0; j < nch; ++j) {
+    for (int j = 0; j < nch && !pf_iter; ++j) {
       const Hot h = load_chunk<NCH>(L, h0, j, lane);
       const bool act = (j * 64 + lane) < nrun;
       nneed += popc(ballot(act && h.ctx >= h.tgt && h.room == 0));
@@ -1054,11 +1085,14 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       }
     }
 
-    // ---- 5. FCFS admission over 64-candidate windows (none after preemption)
-    if (!preempted) {
+    // ---- 5. FCFS admission over 64-candidate windows (none after
+    // preemption; static batching only into an empty running set;
+    // prefill-first only in a prefill iteration).  A first admission leaves
+    // the admission-ratio reserve free.
+    if (!preempted && (!pff || pf_iter) && (policy != TS_POLICY_STATIC || nrun == 0)) {
       int guard = M + N / 64 + 4;  // each pass admits or advances a window
       while (nrun < M && (unlimited || R > 0) && (npre > 0 || nwait > 0) && --guard >= 0) {
-        if (head_need >= 0 && head_need > freeb) break;
+        if (head_need >= 0 && head_need > freeb - (npre > 0 ? 0 : adm_reserve)) break;
         const bool fromq = npre > 0;
         bool valid;
         int c_id, c_tgt, c_rem, c_npre, c_fl;
@@ -1081,7 +1115,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
             const TraceRec r = rec[idx];
             c_tgt = r.prompt;
             c_rem = r.output;
-            if (P.may_reject && (int64_t)r.prompt + (int64_t)r.output > cap_tok) valid = false;
+            if (P.may_reject && rejected(r.prompt, r.output)) valid = false;
           }
         }
         const uint64_t vm = ballot(valid);
@@ -1101,7 +1135,8 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
         const int tq = valid ? c_tgt : 0;
         const int ET = scan_i32(tq) - tq;
         const int slots_left = M - nrun;
-        const bool adm = valid && rank < slots_left && SN <= freeb && (unlimited || ET < R);
+        const bool adm = valid && rank < slots_left && SN <= freeb - (fromq ? 0 : adm_reserve) &&
+                         (unlimited || ET < R);
         const uint64_t am = ballot(adm);
         const int a = popc(am);
         if (a == 0) {
@@ -1153,7 +1188,9 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       nch = nch < NCH ? nch : NCH;
     }
 
-    // ---- 6. batch sums and the roofline iteration time
+    // ---- 6. batch sums and the roofline iteration time (paused decodes of a
+    // prefill-first iteration take no part)
+    if (pf_iter) nD = 0;
     int l_cd = 0, l_tp = 0, l_cp = 0, TP = 0, CP = 0, Rc = 0;
     int64_t l_ap = 0, AP = 0;
     bool wide = false;  // some chunk has more than two prefills: reduce by DPP
@@ -1161,7 +1198,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
     for (int j = 0; j < nch; ++j) {
       const Hot h = load_chunk<NCH>(L, h0, j, lane);
       const bool act = (j * 64 + lane) < nrun;
-      const bool dec = act && h.ctx >= h.tgt;
+      const bool dec = act && h.ctx >= h.tgt && !pf_iter;
       const bool pf = act && !dec && h.q > 0;
       if (dec) l_cd += h.ctx + 1;
       uint64_t m = ballot(pf);
@@ -1210,8 +1247,13 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       Hot h = load_chunk<NCH>(L, h0, j, lane);
       const int s = j * 64 + lane;
       const bool act = s < nrun;
-      const bool dec = act && h.ctx >= h.tgt;
+      const bool dec = act && h.ctx >= h.tgt && !pf_iter;
       bool fin = false;
+      if (pf_iter && act && h.ctx >= h.tgt && !(h.fl & FL_STALE)) {
+        // a paused decode: its last token ended the previous iteration
+        RT[L.id[s]].last = t;
+        h.fl |= FL_STALE;
+      }
       if (dec) {
         h.ctx += 1;
         h.rem -= 1;
@@ -1256,6 +1298,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
   const int64_t sum_e2e = (int64_t)L.sum_e2e;
   const int64_t sum_tpot = (int64_t)L.sum_tpot;
   const int slo_ok = (int)L.slo_ok;
+  const int slo_tpot_ok = (int)L.slo_tpot_ok;
   const int64_t max_e2e = L.max_e2e;
   const int64_t last_fin = L.last_fin;
   const uint64_t digest = L.digest;
@@ -1285,6 +1328,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
     o.slo_ok = slo_ok;
     o.used_block_ns = ubns;
     o.digest = digest;
+    o.slo_tpot_ok = slo_tpot_ok;
     A.res[oi] = o;
   }
 }
@@ -1292,7 +1336,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
 // Persistent grid: each wave64 workgroup takes the next point from a ticket
 // counter until none is left.
 template <int NCH>
-__global__ __launch_bounds__(64, 5) void sim_kernel(SimArgs A) {
+__global__ __launch_bounds__(64, NCH == 4 ? 4 : 5) void sim_kernel(SimArgs A) {
   __shared__ SlotLds<NCH> L;
   const int lane = lane_id();
   QEntry* Q = A.queue + (size_t)blockIdx.x * kQueueCap;

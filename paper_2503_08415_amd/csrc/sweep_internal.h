@@ -28,8 +28,11 @@ struct __attribute__((aligned(16))) DevPoint {
   int32_t trace_off;    // first record of the point's trace
   int32_t n;            // requests in the trace
   int32_t out_index;    // index of the point's results
-  int32_t may_reject;   // 1 if some request of the trace exceeds cap_tokens
+  int32_t may_reject;   // 1 if some request of the trace is rejected
   int32_t lg_iter;      // every iteration takes less than 2^lg_iter ns
+  int64_t cap_prompt;   // a prompt above this many tokens is rejected (admission ratio)
+  int32_t policy;       // TS_POLICY_*
+  int32_t adm_reserve;  // blocks a first admission must leave free
 };
 
 // Integer coefficients of the per-operator roofline (exact below 2^53):

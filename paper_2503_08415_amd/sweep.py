@@ -21,6 +21,7 @@ TS_OK, TS_ERR_ARG, TS_ERR_UNSUPPORTED, TS_ERR_OOM, TS_ERR_DEVICE, TS_ERR_STATE =
 POINT_OK, POINT_NO_KV, POINT_ITER_LIMIT, POINT_TIME_LIMIT = 0, 1, 2, 3
 REQ_PENDING, REQ_DONE, REQ_REJECTED = 0, 1, 2
 F_PER_REQUEST = 1
+POLICY_MIXED, POLICY_PREFILL_FIRST, POLICY_STATIC = 0, 1, 2
 MAX_BATCH = 256
 
 
@@ -39,7 +40,8 @@ class Point(C.Structure):
     _fields_ = [("peak_flops", C.c_double), ("mem_bw", C.c_double),
                 ("capacity_bytes", C.c_int64), ("mem_util_permille", C.c_int32),
                 ("block_size", C.c_int32), ("max_batch", C.c_int32),
-                ("chunk_size", C.c_int32), ("trace_id", C.c_int32), ("policy", C.c_int32)]
+                ("chunk_size", C.c_int32), ("trace_id", C.c_int32), ("policy", C.c_int32),
+                ("admit_mem_permille", C.c_int32), ("reserved", C.c_int32)]
 
 
 class Options(C.Structure):
@@ -59,7 +61,7 @@ POINT_DTYPE = np.dtype([
     ("sum_e2e_ns", "<i8"), ("max_e2e_ns", "<i8"), ("sum_tpot_num_ns", "<i8"),
     ("p50_e2e_ns", "<i8"), ("p90_e2e_ns", "<i8"), ("p99_e2e_ns", "<i8"),
     ("p50_ttft_ns", "<i8"), ("p99_ttft_ns", "<i8"), ("slo_ok", "<i8"),
-    ("used_block_ns", "<f8"), ("digest", "<u8")])
+    ("used_block_ns", "<f8"), ("digest", "<u8"), ("slo_tpot_ok", "<i8")])
 
 # every entry point declared in include/ts_sweep.h
 EXPORTS = ("ts_sweep_create", "ts_sweep_run", "ts_sweep_results", "ts_sweep_shape",
@@ -120,12 +122,14 @@ def points_array(points: dict):
     n = len(points["peak_flops"])
     arr = (Point * max(n, 1))()
     pol = points.get("policy")
+    adm = points.get("admit_mem_permille")
     for i in range(n):
         arr[i] = Point(float(points["peak_flops"][i]), float(points["mem_bw"][i]),
                        int(points["capacity_bytes"][i]), int(points["mem_util_permille"][i]),
                        int(points["block_size"][i]), int(points["max_batch"][i]),
                        int(points["chunk_size"][i]), int(points["trace_id"][i]),
-                       int(pol[i]) if pol is not None else 0)
+                       int(pol[i]) if pol is not None else 0,
+                       int(adm[i]) if adm is not None else 0, 0)
     return arr, n
 
 

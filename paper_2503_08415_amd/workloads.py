@@ -264,6 +264,27 @@ def _c5(n_req):
     return "gqa-7b", traces, rows
 
 
+def _c6(n_req):
+    """Scheduling policies and the admission memory ratio under memory
+    pressure (the studies of Sec. IV-A and Sec. IV-B): 16 arrival rates x
+    3 policies x 4 ratios x 2 small capacities, 7B model, unchunked."""
+    traces = []
+    for r in range(16):
+        spec = {"arrival": ("poisson", float(r + 1)), "prompt": _LN_P_C2,
+                "output": _LN_O_C2}
+        traces.append(make_trace(spec, n_req, _seed(6, 0, r)))
+    rows = []
+    for r in range(16):
+        for policy in (0, 1, 2):
+            for ratio in (0, 600, 800, 950):
+                for cap in (24_000_000_000, 40_000_000_000):
+                    rows.append(dict(peak_flops=312e12, mem_bw=2e12, capacity_bytes=cap,
+                                     mem_util_permille=900, block_size=16, max_batch=64,
+                                     chunk_size=0, trace_id=r, policy=policy,
+                                     admit_mem_permille=ratio))
+    return "llama2-7b", traces, rows
+
+
 # name -> (builder, default requests per trace, description)
 CONFIGS = {
     "c1": (_c1, 64, "1 point x 64 requests, 7B MHA, 312 TF / 2 TB/s / 80 GB, "
@@ -276,6 +297,8 @@ CONFIGS = {
                       "24-160 GB, 8 rates x 32 caps x 8 FLOP/s x 8 BW, max batch 256"),
     "c5": (_c5, 10000, "65536 points x 10000 requests, 7B GQA, chunked prefill "
                        "{256..2048}, long-context mixture, bursty arrivals"),
+    "c6": (_c6, 2000, "384 points x 2000 requests, 7B MHA, 16 rates x {mixed, prefill-first, "
+                      "static} x admission ratio {off, 60%, 80%, 95%} x {24, 40} GB"),
 }
 
 

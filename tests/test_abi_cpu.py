@@ -39,12 +39,13 @@ def test_exports_every_declared_symbol(L):
 def test_struct_layouts():
     assert C.sizeof(S.Model) == 40
     assert C.sizeof(S.Trace) == 32
-    assert C.sizeof(S.Point) == 48
+    assert C.sizeof(S.Point) == 56
     assert C.sizeof(S.Options) == 48
     assert S.REQ_DTYPE.itemsize == 40
-    assert S.POINT_DTYPE.itemsize == 168
+    assert S.POINT_DTYPE.itemsize == 176
     src = open(HEADER).read()
-    assert "Per-point result: 168 bytes" in src and "40 bytes" in src
+    assert "Per-point result: 176 bytes" in src and "40 bytes" in src
+    assert "#define TS_ABI_VERSION 2" in src
 
 
 def test_status_strings(L):
@@ -90,14 +91,13 @@ def test_invalid_arguments_fail_before_device(L):
     for kw in (dict(block_size=0), dict(max_batch=0), dict(chunk_size=8),
                dict(trace_id=3), dict(mem_util_permille=0), dict(mem_util_permille=1001),
                dict(capacity_bytes=0), dict(peak_flops=float("nan")),
-               dict(mem_bw=float("inf")), dict(peak_flops=-1.0)):
+               dict(mem_bw=float("inf")), dict(peak_flops=-1.0),
+               dict(policy=S.POLICY_PREFILL_FIRST, chunk_size=64),
+               dict(admit_mem_permille=-1), dict(admit_mem_permille=1001)):
         rc, h = _create(L, m, traces, _mod_points(pts, **kw))
         assert rc == S.TS_ERR_ARG, kw
-    for kw in (dict(max_batch=257), dict(policy=1)):
-        q = _mod_points(pts, **({} if "policy" in kw else kw))
-        if "policy" in kw:
-            q["policy"] = np.ones(1, np.int32)
-        rc, h = _create(L, m, traces, q)
+    for kw in (dict(max_batch=257), dict(policy=3), dict(policy=-1)):
+        rc, h = _create(L, m, traces, _mod_points(pts, **kw))
         assert rc == S.TS_ERR_UNSUPPORTED, kw
     unsorted = dict(traces[0])
     unsorted["arrival_ns"] = traces[0]["arrival_ns"][::-1].copy()

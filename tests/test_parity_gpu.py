@@ -89,7 +89,8 @@ def hand_sweep():
         rows.append(dict(peak_flops=1e300, mem_bw=1e300,
                          capacity_bytes=nb * b * 16 if nb > 0 else 1, mem_util_permille=1000,
                          block_size=b, max_batch=c["max_batch"], chunk_size=c["chunk_size"],
-                         trace_id=k))
+                         trace_id=k, policy=c.get("policy", 0),
+                         admit_mem_permille=c.get("admit_mem_permille", 0)))
     pts = {k: np.array([r[k] for r in rows]) for k in rows[0]}
     pts = {k: (v.astype(np.float64) if k in ("peak_flops", "mem_bw") else
                v.astype(np.int64) if k == "capacity_bytes" else v.astype(np.int32))
@@ -139,16 +140,22 @@ def _fuzz_case(rng, n_pts):
         K = int(rng.choice([0, 0, M, M + int(rng.integers(0, 9))]))
         nb = int(rng.integers(0, 21)) if M < 64 else int(rng.integers(0, 400))
         fast = rng.random() < 0.5
+        policy = int(rng.choice([0, 0, 0, 1, 2]))  # mixed, prefill-first, static
+        if policy == 1:
+            K = 0
+        permille = int(rng.choice([0, 0, 0, 250, 500, 1000]))
         rows.append(dict(peak_flops=1e300 if fast else float(rng.choice([1e9, 3e9])),
                          mem_bw=1e300 if fast else float(rng.choice([1e8, 7e8])),
                          capacity_bytes=max(1, nb * b * 16), mem_util_permille=1000,
-                         block_size=b, max_batch=M, chunk_size=K, trace_id=k))
+                         block_size=b, max_batch=M, chunk_size=K, trace_id=k,
+                         policy=policy, admit_mem_permille=permille))
     pts = {
         "peak_flops": np.array([r["peak_flops"] for r in rows], np.float64),
         "mem_bw": np.array([r["mem_bw"] for r in rows], np.float64),
         "capacity_bytes": np.array([r["capacity_bytes"] for r in rows], np.int64),
         **{f: np.array([r[f] for r in rows], np.int32)
-           for f in ("mem_util_permille", "block_size", "max_batch", "chunk_size", "trace_id")}}
+           for f in ("mem_util_permille", "block_size", "max_batch", "chunk_size", "trace_id",
+                     "policy", "admit_mem_permille")}}
     return traces, pts
 
 
@@ -169,6 +176,22 @@ def test_fuzz_tiny_points(S, oracle):
         compare_requests(req, o_req, "fuzz%d" % rnd)
         total_pre += int(o_out["n_preempt"].sum())
     assert total_pre > 100
+
+
+def test_full_c6_policies(S, oracle):
+    """Static batching, prefill-first iterations and the admission memory
+    ratio under memory pressure: every point, per request on a subset."""
+    m, traces, pts = W.make_config("c6")
+    t0 = time.time()
+    o_out, o_req = oracle.run_points(m, traces, pts, per_request=True)
+    say("c6: oracle %.1fs, preemptions %d" % (time.time() - t0, int(o_out["n_preempt"].sum())))
+    out, req = gpu_run(S, m, traces, pts, per_request=True, iter_cap=cap_from(o_out))
+    compare_points(out, o_out, "c6")
+    compare_requests(req, o_req, "c6")
+    assert (out["status"] == 0).all()
+    # the ratio keeps memory for running requests: fewer preemptions
+    ratio = pts["admit_mem_permille"]
+    assert out["n_preempt"][ratio == 600].sum() < out["n_preempt"][ratio == 0].sum()
 
 
 def test_full_c3_points(S, oracle):
