@@ -39,6 +39,7 @@ typedef struct {
   int32_t q;       /* tokens scheduled this iteration */
   int64_t admit, first, last, max_gap;
   int32_t n_pre;
+  int32_t swapped; /* preempted by swap: its KV waits in host memory */
 } rq;
 
 #define DEFAULT_ITER_CAP (1LL << 40)
@@ -109,7 +110,8 @@ static double op_time(int64_t flops, int64_t bytes, double iF, double iB) {
   return tf > tb ? tf : tb;
 }
 
-static int64_t cost_from_sums(const tso_model *m, double iF, double iB, const batch_sums *s) {
+/* The iteration's compute time in ns before quantisation. */
+static double compute_total(const tso_model *m, double iF, double iB, const batch_sums *s) {
   const int64_t L = m->n_layers, d = m->d_model, h = m->n_heads, hkv = m->n_kv_heads;
   const int64_t dh = d / h, dkv = hkv * dh;
   const int64_t f = m->ffn_dim, g = 1 + (m->ffn_gated != 0), V = m->vocab;
@@ -142,12 +144,25 @@ static int64_t cost_from_sums(const tso_model *m, double iF, double iB, const ba
   layer = layer + t6;
   double total = (double)L * layer;
   total = total + t7;
+  return total;
+}
+
+static int64_t cost_from_sums_x(const tso_model *m, double iF, double iB, const batch_sums *s,
+                                double xfer, int overlap) {
+  double total = compute_total(m, iF, iB, s);
+  if (xfer > 0.0) total = overlap ? (xfer > total ? xfer : total) : total + xfer;
   int64_t ns = (int64_t)ceil(total);
   return ns < 1 ? 1 : ns;
 }
 
-int64_t tso_iter_ns(const tso_model *m, double iF, double iB, int32_t n, const int32_t *q,
-                    const int32_t *c0, const int32_t *is_prefill, const int32_t *completes) {
+/* xfer: swap transfer time of the iteration in ns (0 when none); overlap:
+ * the transfer runs beside the compute instead of after it */
+static int64_t cost_from_sums(const tso_model *m, double iF, double iB, const batch_sums *s) {
+  return cost_from_sums_x(m, iF, iB, s, 0.0, 0);
+}
+
+static void sums_of(int32_t n, const int32_t *q, const int32_t *c0, const int32_t *is_prefill,
+                    const int32_t *completes, batch_sums *out) {
   batch_sums s;
   memset(&s, 0, sizeof s);
   for (int32_t i = 0; i < n; i++) {
@@ -165,7 +180,21 @@ int64_t tso_iter_ns(const tso_model *m, double iF, double iB, int32_t n, const i
       s.R_lm += 1;
     }
   }
+  *out = s;
+}
+
+int64_t tso_iter_ns(const tso_model *m, double iF, double iB, int32_t n, const int32_t *q,
+                    const int32_t *c0, const int32_t *is_prefill, const int32_t *completes) {
+  batch_sums s;
+  sums_of(n, q, c0, is_prefill, completes, &s);
   return cost_from_sums(m, iF, iB, &s);
+}
+
+double tso_iter_total(const tso_model *m, double iF, double iB, int32_t n, const int32_t *q,
+                      const int32_t *c0, const int32_t *is_prefill, const int32_t *completes) {
+  batch_sums s;
+  sums_of(n, q, c0, is_prefill, completes, &s);
+  return compute_total(m, iF, iB, &s);
 }
 
 /* ------------------------------------------------------------ record hash
@@ -242,6 +271,8 @@ int tso_simulate_point(const tso_model *m, const tso_trace *tr, const tso_point 
   if (p->chunk_size != 0 && p->chunk_size < p->max_batch) return TSO_ERR_ARG;
   if (p->policy == TSO_POLICY_PREFILL_FIRST && p->chunk_size != 0) return TSO_ERR_ARG;
   if (p->admit_mem_permille < 0 || p->admit_mem_permille > 1000) return TSO_ERR_ARG;
+  if (!(p->swap_bw >= 0.0) || !isfinite(p->swap_bw)) return TSO_ERR_ARG;
+  if (p->swap_overlap != 0 && p->swap_overlap != 1) return TSO_ERR_ARG;
   tso_derived dv;
   int rc = tso_derive(m, p, &dv);
   if (rc != TSO_OK) return rc;
@@ -263,6 +294,11 @@ int tso_simulate_point(const tso_model *m, const tso_trace *tr, const tso_point 
   /* blocks a first admission may leave in use, and the reserve it may not touch */
   const int64_t adm_cap = p->admit_mem_permille > 0 ? NB * p->admit_mem_permille / 1000 : NB;
   const int64_t adm_reserve = NB - adm_cap;
+  /* swap preemption: KV bytes per block and ns per byte of the host link */
+  const int swap = p->swap_bw > 0.0;
+  const int64_t block_bytes = b * dv.kv_bytes_per_token;
+  const double inv_link_ns = swap ? 1e9 / p->swap_bw : 0.0;
+  if (swap && NB * block_bytes >= (1LL << 53)) return TSO_ERR_UNSUPPORTED;
   const double iF = dv.inv_flops_ns, iB = dv.inv_bw_ns;
 
   memset(out, 0, sizeof *out);
@@ -326,7 +362,8 @@ int tso_simulate_point(const tso_model *m, const tso_trace *tr, const tso_point 
     if (policy == TSO_POLICY_PREFILL_FIRST && wq.nw > 0 && nr < M) {
       const rq *h = &rs[waiting[0]];
       const int64_t room = h->admit < 0 ? free_blocks - adm_reserve : free_blocks;
-      pf_iter = ceil_div(h->target, b) <= room;
+      const int64_t top = h->ctx > h->target ? h->ctx : h->target;
+      pf_iter = ceil_div(h->swapped ? top : h->target, b) <= room;
     }
 
     /* 3. decode sequences whose next token starts a new block reserve it, in
@@ -335,6 +372,7 @@ int tso_simulate_point(const tso_model *m, const tso_trace *tr, const tso_point 
      *    waits again, ordered by arrival) until the block fits. */
     int preempted = 0;
     int32_t n_pre_now = 0;
+    int64_t xfer_blocks = 0; /* blocks swapped out or in this iteration */
     for (int32_t i = 0; i < nr && !pf_iter; i++) {
       rq *r = &rs[running[i]];
       int need = (r->ctx >= r->target) && (r->ctx % b == 0);
@@ -343,9 +381,16 @@ int tso_simulate_point(const tso_model *m, const tso_trace *tr, const tso_point 
         int32_t v = running[--nr];
         rq *pv = &rs[v];
         free_blocks += pv->alloc;
+        if (swap) {
+          /* swap: the KV moves to host memory and comes back on re-admission */
+          xfer_blocks += pv->alloc;
+          pv->swapped = 1;
+        } else {
+          /* recompute: the KV is dropped and refilled from the tokens so far */
+          pv->ctx = 0;
+          pv->target = plen[v] + pv->gdone;
+        }
         pv->alloc = 0;
-        pv->ctx = 0;
-        pv->target = plen[v] + pv->gdone;
         pv->n_pre += 1;
         pv->phase = PH_WAITING;
         waiting_insert(&wq, v);
@@ -393,16 +438,26 @@ int tso_simulate_point(const tso_model *m, const tso_trace *tr, const tso_point 
     if (policy == TSO_POLICY_STATIC && nr > 0) may_admit = 0;
     if (policy == TSO_POLICY_PREFILL_FIRST && !pf_iter) may_admit = 0;
     if (may_admit) {
-      while (wq.nw > 0 && nr < M && (unlimited || R > 0)) {
+      while (wq.nw > 0 && nr < M) {
         int32_t hidx = waiting[0];
         rq *r = &rs[hidx];
-        int64_t need = ceil_div(r->target, b);
+        /* a swapped request brings back the blocks it held and works from
+         * the next iteration on; any other needs budget for its prefill */
+        if (!r->swapped && !unlimited && R <= 0) break;
+        int64_t top = r->ctx > r->target ? r->ctx : r->target;
+        int64_t need = ceil_div(r->swapped ? top : r->target, b);
         if (need > (r->admit < 0 ? free_blocks - adm_reserve : free_blocks)) break;
         free_blocks -= need;
         r->alloc = (int32_t)need;
-        int64_t q = unlimited ? r->target : (r->target < R ? r->target : R);
-        r->q = (int32_t)q;
-        if (!unlimited) R -= q;
+        if (r->swapped) {
+          xfer_blocks += need;
+          r->swapped = 0;
+          r->q = 0;
+        } else {
+          int64_t q = unlimited ? r->target : (r->target < R ? r->target : R);
+          r->q = (int32_t)q;
+          if (!unlimited) R -= q;
+        }
         if (r->admit < 0) r->admit = t;
         r->phase = PH_RUNNING;
         memmove(&waiting[0], &waiting[1], (size_t)(wq.nw - 1) * sizeof(int32_t));
@@ -420,7 +475,7 @@ int tso_simulate_point(const tso_model *m, const tso_trace *tr, const tso_point 
       rq *r = &rs[running[i]];
       int64_t c0 = r->ctx;
       if (r->ctx >= r->target) {
-        if (r->q == 0) continue; /* paused by a prefill-first iteration */
+        if (r->q == 0) continue; /* paused, or swapped in this iteration */
         s.T += 1;
         s.n_D += 1;
         s.C_D += c0 + 1;
@@ -436,7 +491,9 @@ int tso_simulate_point(const tso_model *m, const tso_trace *tr, const tso_point 
         n_pf++;
       }
     }
-    const int64_t iter_ns = cost_from_sums(m, iF, iB, &s);
+    /* swap transfers of the iteration, priced by the communication model */
+    const double xfer = (double)(xfer_blocks * block_bytes) * inv_link_ns;
+    const int64_t iter_ns = cost_from_sums_x(m, iF, iB, &s, xfer, p->swap_overlap);
 
     /* 7. advance the clock and every scheduled request */
     const int64_t t_end = t + iter_ns;

@@ -75,7 +75,14 @@ typedef struct {
                                   blocks <= floor(num_blocks * this / 1000)
                                   (Sec. IV-B, the maximum memory ratio for
                                   new requests) */
+  int32_t swap_overlap;        /* swap transfers: 0 add to the iteration,
+                                  1 overlap with its compute (Sec. III-B) */
   int32_t pad;
+  double swap_bw;              /* B/s of the host link; 0 = recompute
+                                  preemption, else preempted requests swap
+                                  their KV blocks to host memory (Sec. IV-B)
+                                  and back, priced by the communication model
+                                  (Sec. III-B) */
 } tso_point;
 
 typedef struct {
@@ -128,6 +135,11 @@ int tso_derive(const tso_model *m, const tso_point *p, tso_derived *out);
 int64_t tso_iter_ns(const tso_model *m, double inv_flops_ns, double inv_bw_ns,
                     int32_t n, const int32_t *q, const int32_t *c0,
                     const int32_t *is_prefill, const int32_t *completes);
+
+/* The same batch's compute time in ns before quantisation (no transfer). */
+double tso_iter_total(const tso_model *m, double inv_flops_ns, double inv_bw_ns,
+                      int32_t n, const int32_t *q, const int32_t *c0,
+                      const int32_t *is_prefill, const int32_t *completes);
 
 /* Simulate one design point.  out_req: trace.n records (may be NULL);
  * log: up to log_cap iteration records (may be NULL); *n_log receives the

@@ -51,7 +51,8 @@ class Point(C.Structure):
                 ("capacity_bytes", C.c_int64), ("mem_util_permille", C.c_int32),
                 ("block_size", C.c_int32), ("max_batch", C.c_int32),
                 ("chunk_size", C.c_int32), ("trace_id", C.c_int32), ("policy", C.c_int32),
-                ("admit_mem_permille", C.c_int32), ("pad", C.c_int32)]
+                ("admit_mem_permille", C.c_int32), ("swap_overlap", C.c_int32),
+                ("pad", C.c_int32), ("swap_bw", C.c_double)]
 
 
 class Options(C.Structure):
@@ -100,6 +101,8 @@ def lib():
         L.tso_iter_ns.argtypes = [C.POINTER(Model), C.c_double, C.c_double, C.c_int32,
                                   C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
         L.tso_iter_ns.restype = C.c_int64
+        L.tso_iter_total.argtypes = L.tso_iter_ns.argtypes
+        L.tso_iter_total.restype = C.c_double
         L.tso_simulate_point.argtypes = [
             C.POINTER(Model), C.POINTER(Trace), C.POINTER(Point), C.POINTER(Options),
             C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64, C.POINTER(C.c_int64),
@@ -131,14 +134,17 @@ def _point(pts: dict, i: int) -> Point:
                  int(pts["block_size"][i]), int(pts["max_batch"][i]),
                  int(pts["chunk_size"][i]), int(pts["trace_id"][i]),
                  int(pts["policy"][i]) if "policy" in pts else 0,
-                 int(pts["admit_mem_permille"][i]) if "admit_mem_permille" in pts else 0, 0)
+                 int(pts["admit_mem_permille"][i]) if "admit_mem_permille" in pts else 0,
+                 int(pts["swap_overlap"][i]) if "swap_overlap" in pts else 0, 0,
+                 float(pts["swap_bw"][i]) if "swap_bw" in pts else 0.0)
 
 
 def _single_point(p: dict) -> Point:
     return Point(float(p["peak_flops"]), float(p["mem_bw"]), int(p["capacity_bytes"]),
                  int(p.get("mem_util_permille", 1000)), int(p["block_size"]),
                  int(p["max_batch"]), int(p.get("chunk_size", 0)), int(p.get("trace_id", 0)),
-                 int(p.get("policy", 0)), int(p.get("admit_mem_permille", 0)), 0)
+                 int(p.get("policy", 0)), int(p.get("admit_mem_permille", 0)),
+                 int(p.get("swap_overlap", 0)), 0, float(p.get("swap_bw", 0.0)))
 
 
 class _TraceKeep:
@@ -176,6 +182,14 @@ def iter_ns(model: dict, inv_flops_ns: float, inv_bw_ns: float, batch) -> int:
     cols = [np.ascontiguousarray([b[k] for b in batch] or [0], dtype=np.int32) for k in range(4)]
     return int(lib().tso_iter_ns(C.byref(_model(model)), float(inv_flops_ns), float(inv_bw_ns),
                                  n, *[c.ctypes.data for c in cols]))
+
+
+def iter_total(model: dict, inv_flops_ns: float, inv_bw_ns: float, batch) -> float:
+    """The same batch's compute time in ns before quantisation."""
+    n = len(batch)
+    cols = [np.ascontiguousarray([b[k] for b in batch] or [0], dtype=np.int32) for k in range(4)]
+    return float(lib().tso_iter_total(C.byref(_model(model)), float(inv_flops_ns),
+                                      float(inv_bw_ns), n, *[c.ctypes.data for c in cols]))
 
 
 def simulate_point(model: dict, trace: dict, point: dict, *, iter_cap=0, slo_ttft_ns=0,

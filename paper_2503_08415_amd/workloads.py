@@ -71,7 +71,7 @@ C4_CAPS = tuple(int(round(24e9 + i * 136e9 / 31)) for i in range(32))
 
 POINT_FIELDS = ("peak_flops", "mem_bw", "capacity_bytes", "mem_util_permille",
                 "block_size", "max_batch", "chunk_size", "trace_id", "policy",
-                "admit_mem_permille")
+                "admit_mem_permille", "swap_overlap", "swap_bw")
 
 _NS = 1e9
 
@@ -169,6 +169,8 @@ def _points(rows):
         "trace_id": np.asarray(pts["trace_id"], dtype=np.int32),
         "policy": np.asarray(pts["policy"], dtype=np.int32),
         "admit_mem_permille": np.asarray(pts["admit_mem_permille"], dtype=np.int32),
+        "swap_overlap": np.asarray(pts["swap_overlap"], dtype=np.int32),
+        "swap_bw": np.asarray(pts["swap_bw"], dtype=np.float64),
     }
 
 

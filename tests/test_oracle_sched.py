@@ -40,7 +40,8 @@ def hand_point(case):
     return dict(peak_flops=INF, mem_bw=INF, capacity_bytes=cap, mem_util_permille=1000,
                 block_size=b, max_batch=case["max_batch"], chunk_size=case["chunk_size"],
                 policy=case.get("policy", 0),
-                admit_mem_permille=case.get("admit_mem_permille", 0))
+                admit_mem_permille=case.get("admit_mem_permille", 0),
+                swap_bw=case.get("swap_bw", 0.0), swap_overlap=case.get("swap_overlap", 0))
 
 
 @pytest.mark.parametrize("case", HAND_CASES, ids=[c["name"] for c in HAND_CASES])

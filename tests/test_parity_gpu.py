@@ -90,9 +90,10 @@ def hand_sweep():
                          capacity_bytes=nb * b * 16 if nb > 0 else 1, mem_util_permille=1000,
                          block_size=b, max_batch=c["max_batch"], chunk_size=c["chunk_size"],
                          trace_id=k, policy=c.get("policy", 0),
-                         admit_mem_permille=c.get("admit_mem_permille", 0)))
+                         admit_mem_permille=c.get("admit_mem_permille", 0),
+                         swap_bw=c.get("swap_bw", 0.0), swap_overlap=c.get("swap_overlap", 0)))
     pts = {k: np.array([r[k] for r in rows]) for k in rows[0]}
-    pts = {k: (v.astype(np.float64) if k in ("peak_flops", "mem_bw") else
+    pts = {k: (v.astype(np.float64) if k in ("peak_flops", "mem_bw", "swap_bw") else
                v.astype(np.int64) if k == "capacity_bytes" else v.astype(np.int32))
            for k, v in pts.items()}
     return g["model"], traces, pts, g["cases"]
@@ -278,7 +279,7 @@ def test_edge_cases(S, oracle):
     keys = ("peak_flops", "mem_bw", "capacity_bytes", "mem_util_permille", "block_size",
             "max_batch", "chunk_size", "trace_id")
     pts = {k: np.array([r[i] for r in rows]) for i, k in enumerate(keys)}
-    pts = {k: (v.astype(np.float64) if k in ("peak_flops", "mem_bw") else
+    pts = {k: (v.astype(np.float64) if k in ("peak_flops", "mem_bw", "swap_bw") else
                v.astype(np.int64) if k == "capacity_bytes" else v.astype(np.int32))
            for k, v in pts.items()}
     o_out, o_req = oracle.run_points(m, traces, pts, per_request=True)
