@@ -21,8 +21,9 @@
  *      next arrival;
  *   2. reserve: each running decode whose next token starts a new KV block
  *      takes one, in admission order; when none is free the most recently
- *      admitted running request is preempted by recompute (its blocks are
- *      freed, it waits again with target = prompt + tokens decoded);
+ *      admitted running request is preempted (its blocks are freed and it
+ *      waits again): by recompute, with target = prompt + tokens decoded and
+ *      no KV, or by swap (swap_bw > 0), keeping its KV in host memory;
  *   3. budget: with chunk_size > 0, decodes take one token each and running
  *      prefills share what is left of chunk_size in admission order;
  *   4. admit (not in an iteration that preempted): FCFS, no skipping; the
@@ -55,7 +56,7 @@
 extern "C" {
 #endif
 
-#define TS_ABI_VERSION 2
+#define TS_ABI_VERSION 3
 #define TS_MAX_BATCH 256 /* running-set cap per design point */
 
 /* call status */
@@ -129,13 +130,22 @@ typedef struct {
   int32_t chunk_size;         /* 0: prompts prefill in one iteration; else per-iteration
                                  token budget, max_batch <= chunk_size <= TS_MAX_TOKENS */
   int32_t trace_id;           /* index into the traces passed to create */
-  int32_t policy;             /* TS_POLICY_*; FCFS order and recompute preemption in all */
+  int32_t policy;             /* TS_POLICY_*; FCFS order in all */
   int32_t admit_mem_permille; /* 0: off; 1..1000: a first admission keeps used blocks
                                  <= floor(num_blocks * this / 1000), reserving the rest
                                  for requests already admitted (Sec. IV-B's maximum
                                  memory ratio for new requests); a request whose prompt
                                  needs more than that is rejected */
-  int32_t reserved;           /* 0 */
+  int32_t swap_overlap;       /* swap transfers: 0 add to the iteration's compute time,
+                                 1 overlap with it (the longer of the two) */
+  double swap_bw;             /* 0: preemption by recompute.  > 0 (finite): preemption
+                                 by swap over a host link of this many bytes/s
+                                 (Sec. IV-B; priced by the communication model,
+                                 Sec. III-B): the victim's blocks move to host memory
+                                 and it keeps its tokens; re-admission moves them back
+                                 (no re-prefill, no token budget) and the request works
+                                 again from the next iteration.  An iteration's
+                                 transfers take blocks * block bytes / swap_bw ns */
 } ts_point;
 
 /* Per-request record (TS_F_PER_REQUEST): 40 bytes. */
@@ -185,7 +195,8 @@ typedef struct {
  * memory, copied).  The selected sub-range of points becomes the handle's
  * points, numbered from 0.  Every argument is checked before any device
  * call: TS_ERR_ARG for invalid input, TS_ERR_UNSUPPORTED when a cost-model
- * integer could exceed 2^53 (exact fp64) or a block count exceeds 2^30.
+ * integer (a point's KV bytes, with swap) could exceed 2^53 (exact fp64) or a
+ * block count exceeds 2^30.
  * On success *out receives the handle; on failure *out is NULL. */
 int ts_sweep_create(const ts_model *model, const ts_trace *traces, int32_t n_traces,
                     const ts_point *points, int32_t n_points, const ts_options *opt,

@@ -131,7 +131,7 @@ LaneCoef lane_coef(const CostCoef& c) {
 // Upper bounds of every FLOP / byte count and of the iteration time for a
 // point whose requests hold at most max_po tokens.
 bool exact_and_bounded(const CostCoef& c, int64_t max_po, int M, int K, double iF, double iB,
-                       int* lg_iter) {
+                       double xfer_max, int* lg_iter) {
   const double po = (double)max_po;
   const double T = K > 0 ? (double)K : (double)M * po;   // tokens per iteration
   const double AP = T * po;                             // sum q*(c0+q) >= causal pairs
@@ -148,6 +148,7 @@ bool exact_and_bounded(const CostCoef& c, int64_t max_po, int M, int K, double i
     const double t = std::max(F[i] * iF, Bv[i] * iB);
     tmax += i < 6 ? c.n_layers * t : t;
   }
+  tmax += xfer_max;  // swap transfers of one iteration
   // per-lane int32 partial sums (tokens, keys) must not overflow either
   if (T * 4 > 2147483647.0 || CD * 4 > 2147483647.0) return false;
   if (!(tmax < 1125899906842624.0)) return false;  // 2^50 ns per iteration
@@ -331,8 +332,9 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
     if (p.trace_id < 0 || p.trace_id >= n_traces) return TS_ERR_ARG;
     if (p.policy < TS_POLICY_MIXED || p.policy > TS_POLICY_STATIC) return TS_ERR_UNSUPPORTED;
     if (p.policy == TS_POLICY_PREFILL_FIRST && p.chunk_size != 0) return TS_ERR_ARG;
-    if (p.admit_mem_permille < 0 || p.admit_mem_permille > 1000 || p.reserved != 0)
-      return TS_ERR_ARG;
+    if (p.admit_mem_permille < 0 || p.admit_mem_permille > 1000) return TS_ERR_ARG;
+    if (!std::isfinite(p.swap_bw) || !(p.swap_bw >= 0.0)) return TS_ERR_ARG;
+    if (p.swap_overlap != 0 && p.swap_overlap != 1) return TS_ERR_ARG;
     // KV block budget: floor(capacity * util / 1000), minus the weights when
     // they share the memory, in whole blocks of block_size tokens
     const __int128 usable = ((__int128)p.capacity_bytes * p.mem_util_permille) / 1000;
@@ -359,8 +361,16 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
     d.adm_reserve = (int32_t)((int64_t)nb - adm_cap);
     d.cap_prompt = adm_cap * p.block_size;
     d.may_reject = (ts.max_po > d.cap_tokens || ts.max_p > d.cap_prompt) ? 1 : 0;
+    // swap preemption: an iteration moves at most every block once (out, or
+    // in after an iteration that preempted nothing), exactly in int64 and fp64
+    d.swap = p.swap_bw > 0.0 ? 1 : 0;
+    d.swap_overlap = p.swap_overlap;
+    d.block_bytes = (int64_t)p.block_size * kv_tok;
+    d.inv_link_ns = d.swap ? 1e9 / p.swap_bw : 0.0;
+    if (d.swap && (__int128)nb * d.block_bytes >= ((__int128)1 << 53)) return TS_ERR_UNSUPPORTED;
+    const double xfer_max = (double)((int64_t)nb * d.block_bytes) * d.inv_link_ns;
     if (!exact_and_bounded(coef, ts.max_po, p.max_batch, p.chunk_size, d.inv_flops_ns,
-                           d.inv_bw_ns, &d.lg_iter))
+                           d.inv_bw_ns, xfer_max, &d.lg_iter))
       return TS_ERR_UNSUPPORTED;
     est[(size_t)i] = work_estimate(ts, d.n, p.max_batch, p.chunk_size, p.peak_flops, p.mem_bw,
                                    (double)weights);

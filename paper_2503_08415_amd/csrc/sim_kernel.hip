@@ -195,10 +195,13 @@ __device__ __forceinline__ void lane_work(const LaneRoof& c, int T, int TP, int6
   *Bv = (b0 + c.b1() * Y) + c.b2() * Z;
 }
 
-// Returns max(1, ceil(L * layer_sum + lm_head)) and the same value as a double.
+// Returns max(1, ceil(total)) and the same value as a double, where total is
+// L * layer_sum + lm_head, and with swap transfers of xfer ns in the iteration
+// (xfer > 0) total + xfer, or max(total, xfer) when they overlap the compute.
 __device__ __forceinline__ int64_t iteration_ns(const LaneRoof& c, double n_layers, double iF,
                                                 double iB, int T, int TP, int64_t AP, int CP,
-                                                int nD, int CD, int R, double* iter_d) {
+                                                int nD, int CD, int R, double xfer,
+                                                bool overlap, double* iter_d) {
   double F, Bv;
   lane_work(c, T, TP, AP, CP, nD, CD, R, &F, &Bv);
   const double tf = F * iF;
@@ -214,6 +217,7 @@ __device__ __forceinline__ int64_t iteration_ns(const LaneRoof& c, double n_laye
   const double lm = rdl_f64(t, 6);
   double total = n_layers * layer;
   total = total + lm;
+  if (xfer > 0.0) total = overlap ? __builtin_fmax(total, xfer) : total + xfer;
   const double it = __builtin_fmax(ceil(total), 1.0);
   *iter_d = it;
   return (int64_t)it;
@@ -226,11 +230,12 @@ __device__ __forceinline__ int64_t iteration_ns(const LaneRoof& c, double n_laye
 //   ctx   KV tokens resident          tgt  prefill target (prompt + decoded)
 //   rem   decode iterations left      room free token slots in held blocks
 //   fl    FL_FIRST: first token emitted; FL_STALE: the last token is older
-//         than the previous iteration (set on re-admission after preemption)
+//         than the previous iteration (set on re-admission after preemption);
+//         FL_IDLE: swapped in this iteration, takes no part in it
 //   q     tokens scheduled this iteration (prefill slots)
 //   gap   largest interval between consecutive tokens so far
 // Held blocks are (max(ctx, tgt) + room) / block and are never stored.
-enum : int { FL_FIRST = 1, FL_STALE = 2 };
+enum : int { FL_FIRST = 1, FL_STALE = 2, FL_IDLE = 4 };
 
 struct Hot {
   int ctx, tgt, rem, room, fl, q;
@@ -239,7 +244,7 @@ struct Hot {
 
 // Admission staging: one entry per admitted candidate of a window.
 struct StageSlot {
-  int32_t id, tgt, rem, npre, fl, q, room, pad;
+  int32_t id, tgt, rem, npre, fl, q, room, ctx;
   int64_t gap;
 };
 
@@ -291,6 +296,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
   const int64_t cap_tok = P.cap_tokens, cap_prompt = P.cap_prompt;
   const int policy = P.policy, adm_reserve = P.adm_reserve;
   const bool pff = policy == TS_POLICY_PREFILL_FIRST;
+  const bool swap = P.swap != 0;  // preemption by swap instead of recompute
   // a request that could never fit, alone or within the admission ratio
   auto rejected = [&](int32_t pr, int32_t ou) {
     return (int64_t)pr + (int64_t)ou > cap_tok || (int64_t)pr > cap_prompt;
@@ -524,14 +530,22 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       // alive decode slots: room + B * (blocks taken in this stretch), >= 0;
       // every other lane (prefills, unused, finished) holds a negative value
       int rr[NCH];
+      bool short_chunk = false;  // a chunk before this one holds a non-decode slot
 #pragma unroll
       for (int j = 0; j < NCH; ++j) {
         rr[j] = -0x40000000;
         if (j < nch0) {
           const Hot h = load_chunk<NCH>(L, h0, j, lane);
           const bool dec = (j * 64 + lane) < nrun && h.ctx >= h.tgt;
-          nD += popc(ballot(dec));
+          const uint64_t dm = ballot(dec);
+          nD += popc(dm);
           if (ballot(dec && ((h.fl & FL_STALE) != 0 || h.rem == 1)) != 0) go = false;
+          if (swap) {
+            // a request swapped in behind a prefill can finish its prefill
+            // later than a newer one: the decodes may not form a slot prefix
+            if ((dm & (dm + 1)) != 0 || (short_chunk && dm != 0)) go = false;
+            short_chunk = short_chunk || dm != ~0ull;
+          }
           rr[j] = dec ? h.room : -0x40000000;
         }
       }
@@ -556,9 +570,11 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       if (A.time_limit_ticks != 0 && (n_iters & 255) == 0) go = false;  // watchdog below
       int nchd = (nD + 63) >> 6;
       int nDa = nD, nruna = nrun;  // alive decodes and running requests
-      // an admission would find a free slot and token budget
+      // an admission would find a free slot and token budget (a swapped
+      // request needs no budget)
       auto adm_open = [&]() {
-        return policy != TS_POLICY_STATIC && nruna < M && (unlimited || (npf == 0 && K - nDa > 0));
+        return policy != TS_POLICY_STATIC && nruna < M &&
+               (unlimited || (npf == 0 && K - nDa > 0) || (swap && npre > 0));
       };
       // the waiting head is known not to fit in fb free blocks (a first
       // admission also leaves the admission-ratio reserve)
@@ -755,7 +771,8 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
             const int left = tgt_p - ctx_p;
             const int R1 = K - nDa - left;  // budget left after the completing prefill
             int adm = 0, id_h = 0, tgt_h = 0, o_h = 0, need_h = 0;
-            if (policy != TS_POLICY_STATIC && (npre > 0 || nwait > 0) && nruna < M && R1 > 0) {
+            if (policy != TS_POLICY_STATIC && (npre > 0 || nwait > 0) && nruna < M &&
+                (R1 > 0 || (swap && npre > 0))) {
               if (npre > 0 || nrun >= 64 * NCH) break;  // queue candidates, full slots
               const TraceRec r = rec[next_new];
               if (P.may_reject && rejected(r.prompt, r.output)) break;
@@ -784,7 +801,8 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
                                ((int64_t)q_new * (q_new + 1)) / 2;
             double iter_d;
             const int64_t iter_ns = iteration_ns(roofc, A.n_layers, iF, iB, nDa + TP, TP, AP,
-                                                 tgt_p + q_new, nDa, CD, nDa + 1, &iter_d);
+                                                 tgt_p + q_new, nDa, CD, nDa + 1, 0.0, false,
+                                                 &iter_d);
             const int64_t t_beg = t;
             const int64_t t_end = t_beg + iter_ns;
             ub = ub + (double)(NB - freeb) * iter_d;
@@ -946,10 +964,11 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
     // runs every decode and admits nothing.
     bool pf_iter = false;
     if (pff && (npre > 0 || nwait > 0) && nrun < M) {
-      int tgt_h;
+      int tgt_h;  // tokens whose blocks the head needs
       if (npre > 0) {
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-        tgt_h = Q[qhead].target;
+        const int qc = Q[qhead].ctx, qt = Q[qhead].target;
+        tgt_h = qc > qt ? qc : qt;
       } else {
         int i = next_new;  // the first candidate that is not rejected
         while (P.may_reject && i < next - 1 && rejected(rec[i].prompt, rec[i].output)) ++i;
@@ -969,6 +988,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       nneed += popc(ballot(act && h.ctx >= h.tgt && h.room == 0));
     }
     bool preempted = false;
+    int xblk = 0;  // blocks swapped out or in this iteration
     if (nneed <= freeb) {
       freeb -= nneed;
       if (nneed > 0) {
@@ -984,9 +1004,9 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
         }
       }
     } else {
-      // Recompute preemption from the tail: keep the longest prefix of slots
-      // whose held + needed blocks fit in the whole budget.
-      int carry = 0, k = 0, kept = 0;
+      // Preemption from the tail: keep the longest prefix of slots whose
+      // held + needed blocks fit in the whole budget.
+      int carry = 0, k = 0, kept = 0, kneed = 0;
 #pragma nounroll
       for (int j = 0; j < nch; ++j) {
         const Hot h = load_chunk<NCH>(L, h0, j, lane);
@@ -997,9 +1017,12 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
         const int S = scan_i32(v) + carry;
         const bool keep = act && S <= NB;
         k += popc(ballot(keep));
+        kneed += popc(ballot(keep && need != 0));
         kept += wsum(keep ? v : 0);
         carry = rdl(S, 63);
       }
+      // swap moves the victims' held blocks: all held blocks but the kept ones
+      if (swap) xblk = NB - freeb - (kept - kneed);
       freeb = NB - kept;
       const int nv = nrun - k;
       qhead = (qhead - nv) & (kQueueCap - 1);
@@ -1021,11 +1044,16 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
           }
           QEntry e;
           e.id = id;
-          e.target = h.ctx > h.tgt ? h.ctx : h.tgt;  // prompt + tokens decoded
+          if (swap) {  // the KV goes to host memory and comes back as it was
+            e.target = h.tgt;
+            e.ctx = h.ctx;
+          } else {  // recompute: prefill again over prompt + tokens decoded
+            e.target = h.ctx > h.tgt ? h.ctx : h.tgt;
+            e.ctx = 0;
+          }
           e.rem = h.rem;
           e.n_pre = L.npre[s] + 1;
           e.flags = fl;
-          e.pad = 0;
           e.gap = h.gap;
           Q[(qhead + s - k) & (kQueueCap - 1)] = e;
         }
@@ -1091,11 +1119,13 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
     // the admission-ratio reserve free.
     if (!preempted && (!pff || pf_iter) && (policy != TS_POLICY_STATIC || nrun == 0)) {
       int guard = M + N / 64 + 4;  // each pass admits or advances a window
-      while (nrun < M && (unlimited || R > 0) && (npre > 0 || nwait > 0) && --guard >= 0) {
+      while (nrun < M && (unlimited || R > 0 || (swap && npre > 0)) && (npre > 0 || nwait > 0) &&
+             --guard >= 0) {
         if (head_need >= 0 && head_need > freeb - (npre > 0 ? 0 : adm_reserve)) break;
         const bool fromq = npre > 0;
+        const bool swin = fromq && swap;  // swapped requests: blocks only, no budget
         bool valid;
-        int c_id, c_tgt, c_rem, c_npre, c_fl;
+        int c_id, c_tgt, c_rem, c_npre, c_fl, c_ctx = 0;
         int64_t c_gap;
         if (fromq) {
           valid = lane < npre;
@@ -1103,7 +1133,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
           if (valid) {
             const QEntry e = Q[(qhead + lane) & (kQueueCap - 1)];
             c_id = e.id; c_tgt = e.target; c_rem = e.rem; c_npre = e.n_pre; c_fl = e.flags;
-            c_gap = e.gap;
+            c_gap = e.gap; c_ctx = e.ctx;
           } else {
             c_id = 0; c_tgt = 1; c_rem = 1; c_npre = 0; c_fl = 0; c_gap = 0;
           }
@@ -1130,13 +1160,14 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
           continue;
         }
         const int rank = rank_below(vm);
-        const int need = valid ? divB(c_tgt + B - 1) : 0;
+        const int c_top = c_ctx > c_tgt ? c_ctx : c_tgt;  // tokens held in blocks
+        const int need = valid ? divB(c_top + B - 1) : 0;
         const int SN = scan_i32(need);
         const int tq = valid ? c_tgt : 0;
         const int ET = scan_i32(tq) - tq;
         const int slots_left = M - nrun;
         const bool adm = valid && rank < slots_left && SN <= freeb - (fromq ? 0 : adm_reserve) &&
-                         (unlimited || ET < R);
+                         (unlimited || swin || ET < R);
         const uint64_t am = ballot(adm);
         const int a = popc(am);
         if (a == 0) {
@@ -1144,14 +1175,17 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
           break;
         }
         const int last_lane = 63 - (int)__builtin_clzll(am);
-        const int qv = unlimited ? c_tgt : (c_tgt < R - ET ? c_tgt : R - ET);
-        freeb -= rdl(SN, last_lane);
+        const int qv = swin ? 0 : (unlimited ? c_tgt : (c_tgt < R - ET ? c_tgt : R - ET));
+        const int taken = rdl(SN, last_lane);
+        freeb -= taken;
+        if (swin) xblk += taken;
         if (!unlimited) R -= wsum(adm ? qv : 0);
         if (adm) {
           if (!fromq) RT[c_id].admit = t;  // first admission
           StageSlot st;
-          st.id = c_id; st.tgt = c_tgt; st.rem = c_rem; st.npre = c_npre; st.fl = c_fl;
-          st.q = qv; st.room = need * B - c_tgt; st.pad = 0; st.gap = c_gap;
+          st.id = c_id; st.tgt = c_tgt; st.rem = c_rem; st.npre = c_npre;
+          st.fl = swin ? (c_fl | FL_IDLE) : c_fl;
+          st.q = qv; st.room = need * B - c_top; st.ctx = c_ctx; st.gap = c_gap;
           L.u.stage[rank] = st;
         }
         __syncthreads();
@@ -1161,7 +1195,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
           if (s >= nrun && s < nrun + a) {
             const StageSlot st = L.u.stage[s - nrun];
             Hot h;
-            h.ctx = 0; h.tgt = st.tgt; h.rem = st.rem; h.room = st.room; h.fl = st.fl;
+            h.ctx = st.ctx; h.tgt = st.tgt; h.rem = st.rem; h.room = st.room; h.fl = st.fl;
             h.q = st.q; h.gap = st.gap;
             store_chunk<NCH>(L, h0, j, lane, h);
             L.id[s] = st.id;
@@ -1189,7 +1223,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
     }
 
     // ---- 6. batch sums and the roofline iteration time (paused decodes of a
-    // prefill-first iteration take no part)
+    // prefill-first iteration and requests swapped in now take no part)
     if (pf_iter) nD = 0;
     int l_cd = 0, l_tp = 0, l_cp = 0, TP = 0, CP = 0, Rc = 0;
     int64_t l_ap = 0, AP = 0;
@@ -1198,7 +1232,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
     for (int j = 0; j < nch; ++j) {
       const Hot h = load_chunk<NCH>(L, h0, j, lane);
       const bool act = (j * 64 + lane) < nrun;
-      const bool dec = act && h.ctx >= h.tgt && !pf_iter;
+      const bool dec = act && h.ctx >= h.tgt && !pf_iter && !(h.fl & FL_IDLE);
       const bool pf = act && !dec && h.q > 0;
       if (dec) l_cd += h.ctx + 1;
       uint64_t m = ballot(pf);
@@ -1228,9 +1262,11 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       CP += wsum(l_cp);
       AP += wsum64(l_ap);
     }
+    // swap transfers, priced by the host link's bandwidth
+    const double xfer = (double)((int64_t)xblk * P.block_bytes) * P.inv_link_ns;
     double iter_d;
     const int64_t iter_ns = iteration_ns(roofc, A.n_layers, iF, iB, nD + TP, TP, AP, CP, nD,
-                                         CD, nD + Rc, &iter_d);
+                                         CD, nD + Rc, xfer, P.swap_overlap != 0, &iter_d);
 
     // ---- 7. advance the clock and every scheduled request
     const int64_t t_end = t + iter_ns;
@@ -1247,7 +1283,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       Hot h = load_chunk<NCH>(L, h0, j, lane);
       const int s = j * 64 + lane;
       const bool act = s < nrun;
-      const bool dec = act && h.ctx >= h.tgt && !pf_iter;
+      const bool dec = act && h.ctx >= h.tgt && !pf_iter && !(h.fl & FL_IDLE);
       bool fin = false;
       if (pf_iter && act && h.ctx >= h.tgt && !(h.fl & FL_STALE)) {
         // a paused decode: its last token ended the previous iteration
@@ -1275,6 +1311,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
         }
         h.q = 0;
       }
+      h.fl &= ~FL_IDLE;
       store_chunk<NCH>(L, h0, j, lane, h);
       const uint64_t fm = ballot(fin);
       if (fm != 0) {

@@ -33,6 +33,10 @@ struct __attribute__((aligned(16))) DevPoint {
   int64_t cap_prompt;   // a prompt above this many tokens is rejected (admission ratio)
   int32_t policy;       // TS_POLICY_*
   int32_t adm_reserve;  // blocks a first admission must leave free
+  double inv_link_ns;   // swap preemption: 1e9 / host link bytes per second
+  int64_t block_bytes;  // KV bytes of one block
+  int32_t swap;         // 1: preemption by swap, 0: by recompute
+  int32_t swap_overlap; // 1: transfers overlap the iteration's compute
 };
 
 // Integer coefficients of the per-operator roofline (exact below 2^53):
@@ -50,9 +54,11 @@ struct CostCoef {
   double n_layers;
 };
 
-// A request waiting after recompute preemption, 32 bytes.
+// A preempted request waiting for re-admission, 32 bytes.  After recompute
+// preemption ctx is 0 and target covers prompt and decoded tokens; after swap
+// preemption both keep the values the request had when it left.
 struct __attribute__((aligned(16))) QEntry {
-  int32_t id, target, rem, n_pre, flags, pad;
+  int32_t id, target, rem, n_pre, flags, ctx;
   int64_t gap;
 };
 

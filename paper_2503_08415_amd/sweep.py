@@ -41,7 +41,8 @@ class Point(C.Structure):
                 ("capacity_bytes", C.c_int64), ("mem_util_permille", C.c_int32),
                 ("block_size", C.c_int32), ("max_batch", C.c_int32),
                 ("chunk_size", C.c_int32), ("trace_id", C.c_int32), ("policy", C.c_int32),
-                ("admit_mem_permille", C.c_int32), ("reserved", C.c_int32)]
+                ("admit_mem_permille", C.c_int32), ("swap_overlap", C.c_int32),
+                ("swap_bw", C.c_double)]
 
 
 class Options(C.Structure):
@@ -123,13 +124,17 @@ def points_array(points: dict):
     arr = (Point * max(n, 1))()
     pol = points.get("policy")
     adm = points.get("admit_mem_permille")
+    sov = points.get("swap_overlap")
+    sbw = points.get("swap_bw")
     for i in range(n):
         arr[i] = Point(float(points["peak_flops"][i]), float(points["mem_bw"][i]),
                        int(points["capacity_bytes"][i]), int(points["mem_util_permille"][i]),
                        int(points["block_size"][i]), int(points["max_batch"][i]),
                        int(points["chunk_size"][i]), int(points["trace_id"][i]),
                        int(pol[i]) if pol is not None else 0,
-                       int(adm[i]) if adm is not None else 0, 0)
+                       int(adm[i]) if adm is not None else 0,
+                       int(sov[i]) if sov is not None else 0,
+                       float(sbw[i]) if sbw is not None else 0.0)
     return arr, n
 
 

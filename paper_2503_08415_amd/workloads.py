@@ -287,6 +287,29 @@ def _c6(n_req):
     return "llama2-7b", traces, rows
 
 
+def _c7(n_req):
+    """Preemption by recompute against preemption by swap (Sec. IV-B; the
+    transfer priced by the communication model of Sec. III-B) under memory
+    pressure: 16 arrival rates x {recompute, swap over 16 / 32 / 64 GB/s
+    after the compute, swap over 64 GB/s overlapping it} x {20, 24} GB x
+    {unchunked, chunk 512}, 7B model."""
+    traces = []
+    for r in range(16):
+        spec = {"arrival": ("poisson", float(r + 1)), "prompt": _LN_P_C2,
+                "output": _LN_O_C2}
+        traces.append(make_trace(spec, n_req, _seed(7, 0, r)))
+    rows = []
+    for r in range(16):
+        for bw, overlap in ((0.0, 0), (16e9, 0), (32e9, 0), (64e9, 0), (64e9, 1)):
+            for cap in (20_000_000_000, 24_000_000_000):
+                for chunk in (0, 512):
+                    rows.append(dict(peak_flops=312e12, mem_bw=2e12, capacity_bytes=cap,
+                                     mem_util_permille=900, block_size=16, max_batch=64,
+                                     chunk_size=chunk, trace_id=r, swap_bw=bw,
+                                     swap_overlap=overlap))
+    return "llama2-7b", traces, rows
+
+
 # name -> (builder, default requests per trace, description)
 CONFIGS = {
     "c1": (_c1, 64, "1 point x 64 requests, 7B MHA, 312 TF / 2 TB/s / 80 GB, "
@@ -301,6 +324,8 @@ CONFIGS = {
                        "{256..2048}, long-context mixture, bursty arrivals"),
     "c6": (_c6, 2000, "384 points x 2000 requests, 7B MHA, 16 rates x {mixed, prefill-first, "
                       "static} x admission ratio {off, 60%, 80%, 95%} x {24, 40} GB"),
+    "c7": (_c7, 2000, "320 points x 2000 requests, 7B MHA, 16 rates x {recompute, swap "
+                      "16/32/64 GB/s, swap 64 GB/s overlapped} x {20, 24} GB x {no chunk, 512}"),
 }
 
 

@@ -39,13 +39,47 @@ def test_exports_every_declared_symbol(L):
 def test_struct_layouts():
     assert C.sizeof(S.Model) == 40
     assert C.sizeof(S.Trace) == 32
-    assert C.sizeof(S.Point) == 56
+    assert C.sizeof(S.Point) == 64
     assert C.sizeof(S.Options) == 48
     assert S.REQ_DTYPE.itemsize == 40
     assert S.POINT_DTYPE.itemsize == 176
     src = open(HEADER).read()
     assert "Per-point result: 176 bytes" in src and "40 bytes" in src
-    assert "#define TS_ABI_VERSION 2" in src
+    assert "#define TS_ABI_VERSION 3" in src
+
+
+def test_header_layout_matches_binding(tmp_path):
+    """Every field offset and struct size the C compiler derives from the
+    header equals the one the Python binding declares."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no host C compiler")
+    structs = [("ts_model", S.Model), ("ts_trace", S.Trace), ("ts_point", S.Point),
+               ("ts_options", S.Options), ("ts_point_result", S.POINT_DTYPE),
+               ("ts_req_result", S.REQ_DTYPE)]
+    want, lines = [], []
+    for cname, py in structs:
+        if isinstance(py, np.dtype):
+            fields = [(n, py.fields[n][1]) for n in py.names]
+            size = py.itemsize
+        else:
+            fields = [(f[0], getattr(py, f[0]).offset) for f in py._fields_]
+            size = C.sizeof(py)
+        want.append("%s %d" % (cname, size))
+        lines.append('printf("%s %%zu\\n", sizeof(%s));' % (cname, cname))
+        for n, off in fields:
+            want.append("%s.%s %d" % (cname, n, off))
+            lines.append('printf("%s.%s %%zu\\n", offsetof(%s, %s));' % (cname, n, cname, n))
+    src = tmp_path / "layout.c"
+    src.write_text("#include <stddef.h>\n#include <stdio.h>\n#include \"ts_sweep.h\"\n"
+                   "int main(void) {\n" + "\n".join(lines) + "\nreturn 0;\n}\n")
+    exe = tmp_path / "layout"
+    subprocess.run([cc, "-std=c99", "-I", os.path.join(ROOT, "include"), str(src), "-o",
+                    str(exe)], check=True)
+    got = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n")
+    assert [g for g in got if g] == want
 
 
 def test_status_strings(L):
@@ -93,7 +127,8 @@ def test_invalid_arguments_fail_before_device(L):
                dict(capacity_bytes=0), dict(peak_flops=float("nan")),
                dict(mem_bw=float("inf")), dict(peak_flops=-1.0),
                dict(policy=S.POLICY_PREFILL_FIRST, chunk_size=64),
-               dict(admit_mem_permille=-1), dict(admit_mem_permille=1001)):
+               dict(admit_mem_permille=-1), dict(admit_mem_permille=1001),
+               dict(swap_bw=-1.0), dict(swap_bw=float("inf")), dict(swap_overlap=2)):
         rc, h = _create(L, m, traces, _mod_points(pts, **kw))
         assert rc == S.TS_ERR_ARG, kw
     for kw in (dict(max_batch=257), dict(policy=3), dict(policy=-1)):

@@ -145,18 +145,22 @@ def _fuzz_case(rng, n_pts):
         if policy == 1:
             K = 0
         permille = int(rng.choice([0, 0, 0, 250, 500, 1000]))
+        # swap preemption over a link moving a 16-byte token in 16, 0.5 or 0.016 ns
+        swap_bw = float(rng.choice([0.0, 0.0, 0.0, 1e9, 3.2e10, 1e12]))
         rows.append(dict(peak_flops=1e300 if fast else float(rng.choice([1e9, 3e9])),
                          mem_bw=1e300 if fast else float(rng.choice([1e8, 7e8])),
                          capacity_bytes=max(1, nb * b * 16), mem_util_permille=1000,
                          block_size=b, max_batch=M, chunk_size=K, trace_id=k,
-                         policy=policy, admit_mem_permille=permille))
+                         policy=policy, admit_mem_permille=permille, swap_bw=swap_bw,
+                         swap_overlap=int(rng.integers(0, 2))))
     pts = {
         "peak_flops": np.array([r["peak_flops"] for r in rows], np.float64),
         "mem_bw": np.array([r["mem_bw"] for r in rows], np.float64),
         "capacity_bytes": np.array([r["capacity_bytes"] for r in rows], np.int64),
+        "swap_bw": np.array([r["swap_bw"] for r in rows], np.float64),
         **{f: np.array([r[f] for r in rows], np.int32)
            for f in ("mem_util_permille", "block_size", "max_batch", "chunk_size", "trace_id",
-                     "policy", "admit_mem_permille")}}
+                     "policy", "admit_mem_permille", "swap_overlap")}}
     return traces, pts
 
 
@@ -193,6 +197,27 @@ def test_full_c6_policies(S, oracle):
     # the ratio keeps memory for running requests: fewer preemptions
     ratio = pts["admit_mem_permille"]
     assert out["n_preempt"][ratio == 600].sum() < out["n_preempt"][ratio == 0].sum()
+
+
+def test_full_c7_swap(S, oracle):
+    """Preemption by swap (transfers after the compute or overlapping it)
+    against preemption by recompute under memory pressure: every point and
+    every request."""
+    m, traces, pts = W.make_config("c7")
+    t0 = time.time()
+    o_out, o_req = oracle.run_points(m, traces, pts, per_request=True)
+    say("c7: oracle %.1fs, preemptions %d" % (time.time() - t0, int(o_out["n_preempt"].sum())))
+    out, req = gpu_run(S, m, traces, pts, per_request=True, iter_cap=cap_from(o_out))
+    compare_points(out, o_out, "c7")
+    compare_requests(req, o_req, "c7")
+    assert (out["status"] == 0).all()
+    swap = pts["swap_bw"] > 0
+    assert out["n_preempt"][swap].sum() > 1000 and out["n_preempt"][~swap].sum() > 1000
+    # transfers that overlap the compute never lengthen an iteration beyond
+    # the sequential ones at the same bandwidth: lower mean latency overall
+    fast = pts["swap_bw"] == 64e9
+    ov, sq = fast & (pts["swap_overlap"] == 1), fast & (pts["swap_overlap"] == 0)
+    assert out["sum_e2e_ns"][ov].sum() < out["sum_e2e_ns"][sq].sum()
 
 
 def test_full_c3_points(S, oracle):
