@@ -40,6 +40,7 @@ typedef struct {
   int64_t admit, first, last, max_gap;
   int32_t n_pre;
   int32_t swapped; /* preempted by swap: its KV waits in host memory */
+  int32_t fresh;   /* not yet admitted on this worker */
 } rq;
 
 #define DEFAULT_ITER_CAP (1LL << 40)
@@ -224,7 +225,7 @@ uint64_t tso_record_hash(int64_t index, const tso_req *r) {
 
 /* ------------------------------------------------------------ simulation */
 typedef struct {
-  const tso_trace *tr;
+  const int64_t *arr;
   rq *rs;
   int32_t *waiting;
   int32_t nw;
@@ -232,7 +233,7 @@ typedef struct {
 
 /* waiting is ordered by (arrival, index): FCFS */
 static void waiting_insert(waitq *w, int32_t idx) {
-  const int64_t *arr = w->tr->arrival_ns;
+  const int64_t *arr = w->arr;
   int32_t pos = w->nw;
   while (pos > 0) {
     int32_t o = w->waiting[pos - 1];
@@ -259,77 +260,78 @@ static int64_t nearest_rank(const int64_t *sorted, int64_t n, int pct) {
 
 static int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-int tso_simulate_point(const tso_model *m, const tso_trace *tr, const tso_point *p,
-                       const tso_options *opt, tso_point_out *out, tso_req *out_req,
-                       tso_iter_rec *log, int64_t log_cap, int64_t *n_log,
-                       int64_t *violations) {
-  if (!m || !tr || !p || !out) return TSO_ERR_ARG;
-  if (tr->n < 0 || (tr->n > 0 && (!tr->arrival_ns || !tr->prompt_len || !tr->output_len)))
-    return TSO_ERR_ARG;
-  if (p->max_batch < 1 || p->block_size < 1) return TSO_ERR_ARG;
-  if (p->policy < TSO_POLICY_MIXED || p->policy > TSO_POLICY_STATIC) return TSO_ERR_ARG;
-  if (p->chunk_size != 0 && p->chunk_size < p->max_batch) return TSO_ERR_ARG;
-  if (p->policy == TSO_POLICY_PREFILL_FIRST && p->chunk_size != 0) return TSO_ERR_ARG;
-  if (p->admit_mem_permille < 0 || p->admit_mem_permille > 1000) return TSO_ERR_ARG;
-  if (!(p->swap_bw >= 0.0) || !isfinite(p->swap_bw)) return TSO_ERR_ARG;
-  if (p->swap_overlap != 0 && p->swap_overlap != 1) return TSO_ERR_ARG;
-  tso_derived dv;
-  int rc = tso_derive(m, p, &dv);
-  if (rc != TSO_OK) return rc;
+/* ------------------------------------------------------------ one worker */
+/* What a worker does with the requests that reach it:
+ *   WM_FULL     the whole request: prefill, first token, output decodes
+ *               (a design point with one worker);
+ *   WM_PREFILL  a prefill device of a disaggregated deployment (Sec. II-B;
+ *               breakpoints after the first iteration, Sec. III-A): the
+ *               request leaves when its prefill completes, and its KV
+ *               crosses the device's link to a decode device;
+ *   WM_DECODE   a decode device: the request arrives with its prompt's KV and
+ *               first token, and runs its output decodes. */
+enum { WM_FULL = 0, WM_PREFILL = 1, WM_DECODE = 2 };
 
-  const int64_t iter_cap = (opt && opt->iter_cap > 0) ? opt->iter_cap : DEFAULT_ITER_CAP;
-  const int64_t slo_ttft = (opt && opt->slo_ttft_ns > 0) ? opt->slo_ttft_ns : DEFAULT_SLO_TTFT;
-  const int64_t slo_tpot = (opt && opt->slo_tpot_ns > 0) ? opt->slo_tpot_ns : DEFAULT_SLO_TPOT;
-  const int check = opt ? opt->check_invariants : 0;
+typedef struct {
+  int64_t n_iters, n_preempt, prefill_tokens, decode_tokens, peak_used;
+  double used_block_ns;
+  int32_t status;
+  int64_t nviol, nlog;
+} worker_out;
 
-  const int32_t N = tr->n;
-  const int64_t *arr = tr->arrival_ns;
-  const int32_t *plen = tr->prompt_len, *olen = tr->output_len;
-  for (int32_t i = 0; i < N; i++) {
-    if (plen[i] < 1 || olen[i] < 1 || arr[i] < 0) return TSO_ERR_ARG;
-    if (i > 0 && arr[i] < arr[i - 1]) return TSO_ERR_ARG;
-  }
-  const int64_t NB = dv.num_blocks, b = p->block_size, M = p->max_batch, K = p->chunk_size;
+/* The KV link out of a prefill device.  Transfers run one after another in
+ * the order the prefills complete: the sequential default of the
+ * communication model (Sec. III-B), which prices a transfer as bytes over
+ * bandwidth. */
+typedef struct {
+  int64_t kv_bytes_per_token;
+  double inv_link_ns;  /* ns per byte; 0 = instant */
+  int64_t free_at;     /* the link is busy until then */
+  int64_t *arrive;     /* per request: when its KV reaches the decode device */
+} kv_link;
+
+/* ceil(prompt KV bytes * ns per byte), whole ns */
+static int64_t kv_transfer_ns(const kv_link *lk, int32_t prompt) {
+  if (lk->inv_link_ns == 0.0) return 0;
+  return (int64_t)ceil((double)((int64_t)prompt * lk->kv_bytes_per_token) * lk->inv_link_ns);
+}
+
+/* Blocks a waiting request takes when admitted: a swapped request gets back
+ * what it held; one that arrives ready to decode holds its KV plus the slot
+ * of the token it decodes next; any other holds its whole prefill target. */
+static int64_t admission_blocks(const rq *r, int64_t b) {
+  const int64_t top = r->ctx > r->target ? r->ctx : r->target;
+  if (r->swapped) return ceil_div(top, b);
+  if (r->ctx >= r->target) return ceil_div((int64_t)r->ctx + 1, b);
+  return ceil_div(r->target, b);
+}
+
+/* Run one worker (hardware and scheduler p, derived constants dv) over N
+ * requests with arrival times arr (sorted), whose state rs the caller has
+ * initialised (PH_FUTURE or PH_REJECTED, target, ctx, times). */
+static int worker_loop(const tso_model *m, const tso_point *p, const tso_derived *dv, int wmode,
+                       int32_t N, const int64_t *arr, const int32_t *plen, const int32_t *olen,
+                       rq *rs, int64_t iter_cap, int check, kv_link *lk, tso_iter_rec *log,
+                       int64_t log_cap, worker_out *wo) {
+  const int64_t NB = dv->num_blocks, b = p->block_size, M = p->max_batch, K = p->chunk_size;
   const int policy = p->policy;
   /* blocks a first admission may leave in use, and the reserve it may not touch */
   const int64_t adm_cap = p->admit_mem_permille > 0 ? NB * p->admit_mem_permille / 1000 : NB;
   const int64_t adm_reserve = NB - adm_cap;
   /* swap preemption: KV bytes per block and ns per byte of the host link */
   const int swap = p->swap_bw > 0.0;
-  const int64_t block_bytes = b * dv.kv_bytes_per_token;
+  const int64_t block_bytes = b * dv->kv_bytes_per_token;
   const double inv_link_ns = swap ? 1e9 / p->swap_bw : 0.0;
-  if (swap && NB * block_bytes >= (1LL << 53)) return TSO_ERR_UNSUPPORTED;
-  const double iF = dv.inv_flops_ns, iB = dv.inv_bw_ns;
-
-  memset(out, 0, sizeof *out);
-  out->num_blocks = (int32_t)NB;
-  out->first_arrival_ns = N > 0 ? arr[0] : -1;
-  out->last_finish_ns = -1;
-
-  rq *rs = (rq *)calloc((size_t)(N > 0 ? N : 1), sizeof(rq));
+  const double iF = dv->inv_flops_ns, iB = dv->inv_bw_ns;
   int32_t *running = (int32_t *)malloc((size_t)M * sizeof(int32_t));
   int32_t *waiting = (int32_t *)malloc((size_t)(N > 0 ? N : 1) * sizeof(int32_t));
-  int64_t *e2e = (int64_t *)malloc((size_t)(N > 0 ? N : 1) * sizeof(int64_t));
-  int64_t *ttft = (int64_t *)malloc((size_t)(N > 0 ? N : 1) * sizeof(int64_t));
-  if (!rs || !running || !waiting || !e2e || !ttft) {
-    free(rs); free(running); free(waiting); free(e2e); free(ttft);
+  if (!running || !waiting) {
+    free(running); free(waiting);
     return TSO_ERR_OOM;
   }
-  int64_t nviol = 0;
-  int64_t nlog = 0;
+  int64_t nviol = 0, nlog = 0;
 
-  /* A request that could not fit even alone is rejected up front: with
-   * recompute preemption it would otherwise never finish.  So is one whose
-   * prompt alone exceeds what a first admission may use. */
-  for (int32_t i = 0; i < N; i++) {
-    rq *r = &rs[i];
-    r->phase = (NB == 0 || ceil_div((int64_t)plen[i] + olen[i], b) > NB ||
-                ceil_div(plen[i], b) > adm_cap) ? PH_REJECTED : PH_FUTURE;
-    r->target = plen[i];
-    r->admit = r->first = r->last = -1;
-  }
-
-  waitq wq = {tr, rs, waiting, 0};
+  waitq wq = {arr, rs, waiting, 0};
   int64_t t = 0, free_blocks = NB;
   int32_t next = 0, nr = 0;
   int64_t n_iters = 0, n_preempt = 0, prefill_tokens = 0, decode_tokens = 0, peak_used = 0;
@@ -361,9 +363,8 @@ int tso_simulate_point(const tso_model *m, const tso_trace *tr, const tso_point 
     int pf_iter = 0;
     if (policy == TSO_POLICY_PREFILL_FIRST && wq.nw > 0 && nr < M) {
       const rq *h = &rs[waiting[0]];
-      const int64_t room = h->admit < 0 ? free_blocks - adm_reserve : free_blocks;
-      const int64_t top = h->ctx > h->target ? h->ctx : h->target;
-      pf_iter = ceil_div(h->swapped ? top : h->target, b) <= room;
+      const int64_t room = h->fresh ? free_blocks - adm_reserve : free_blocks;
+      pf_iter = admission_blocks(h, b) <= room;
     }
 
     /* 3. decode sequences whose next token starts a new block reserve it, in
@@ -442,23 +443,28 @@ int tso_simulate_point(const tso_model *m, const tso_trace *tr, const tso_point 
         int32_t hidx = waiting[0];
         rq *r = &rs[hidx];
         /* a swapped request brings back the blocks it held and works from
-         * the next iteration on; any other needs budget for its prefill */
+         * the next iteration on; any other needs budget for its prefill, or
+         * one token when it arrives ready to decode */
         if (!r->swapped && !unlimited && R <= 0) break;
-        int64_t top = r->ctx > r->target ? r->ctx : r->target;
-        int64_t need = ceil_div(r->swapped ? top : r->target, b);
-        if (need > (r->admit < 0 ? free_blocks - adm_reserve : free_blocks)) break;
+        int64_t need = admission_blocks(r, b);
+        if (need > (r->fresh ? free_blocks - adm_reserve : free_blocks)) break;
         free_blocks -= need;
         r->alloc = (int32_t)need;
         if (r->swapped) {
           xfer_blocks += need;
           r->swapped = 0;
           r->q = 0;
+        } else if (r->ctx >= r->target) {
+          /* its KV came from a prefill device: it decodes in this iteration */
+          r->q = 1;
+          if (!unlimited) R -= 1;
         } else {
           int64_t q = unlimited ? r->target : (r->target < R ? r->target : R);
           r->q = (int32_t)q;
           if (!unlimited) R -= q;
         }
         if (r->admit < 0) r->admit = t;
+        r->fresh = 0;
         r->phase = PH_RUNNING;
         memmove(&waiting[0], &waiting[1], (size_t)(wq.nw - 1) * sizeof(int32_t));
         wq.nw--;
@@ -527,6 +533,19 @@ int tso_simulate_point(const tso_model *m, const tso_trace *tr, const tso_point 
         if (r->ctx == r->target && r->first < 0) {
           r->first = t_end; /* the full prefill emits the first token */
           r->last = t_end;
+          if (wmode == WM_PREFILL) {
+            /* a prefill device is done with the request: its blocks are
+             * released and its KV queues for the device's link */
+            r->phase = PH_DONE;
+            free_blocks += r->alloc;
+            r->alloc = 0;
+            r->q = 0;
+            const int64_t start = t_end > lk->free_at ? t_end : lk->free_at;
+            lk->free_at = start + kv_transfer_ns(lk, plen[idx]);
+            lk->arrive[idx] = lk->free_at;
+            n_fin++;
+            continue;
+          }
         }
       }
       running[j++] = idx;
@@ -559,7 +578,7 @@ int tso_simulate_point(const tso_model *m, const tso_trace *tr, const tso_point 
         held += r->alloc;
         int64_t top = r->ctx > r->target ? r->ctx : r->target;
         if (r->alloc != ceil_div(top, b)) nviol++;
-        if (r->admit < arr[idx]) nviol++;
+        if (wmode != WM_DECODE && r->admit < arr[idx]) nviol++;
         if (r->first >= 0 && r->first <= r->admit) nviol++;
         if (r->ctx >= r->target && r->ctx != plen[idx] + r->gdone) nviol++;
         if (r->ctx < r->target && r->target != plen[idx] + r->gdone) nviol++;
@@ -573,11 +592,42 @@ int tso_simulate_point(const tso_model *m, const tso_trace *tr, const tso_point 
     }
   }
 
+
+  if (check && status == TSO_POINT_OK && wmode != WM_PREFILL) {
+    int64_t want = 0;
+    for (int32_t i = 0; i < N; i++)
+      if (rs[i].phase == PH_DONE) want += olen[i];
+    if (want != decode_tokens) nviol++;
+  }
+  wo->n_iters = n_iters;
+  wo->n_preempt = n_preempt;
+  wo->prefill_tokens = prefill_tokens;
+  wo->decode_tokens = decode_tokens;
+  wo->peak_used = peak_used;
+  wo->used_block_ns = used_block_ns;
+  wo->status = status;
+  wo->nviol = nviol;
+  wo->nlog = nlog;
+  free(running); free(waiting);
+  return TSO_OK;
+}
+
+/* Per-request records, latency statistics and the digest of one point, from
+ * every request's final state (arr: the trace's arrival times). */
+static int point_stats(int32_t N, const int64_t *arr, const int32_t *olen, const rq *rs,
+                       int64_t slo_ttft, int64_t slo_tpot, int check, tso_point_out *out,
+                       tso_req *out_req, int64_t *nviol) {
+  int64_t *e2e = (int64_t *)malloc((size_t)(N > 0 ? N : 1) * sizeof(int64_t));
+  int64_t *ttft = (int64_t *)malloc((size_t)(N > 0 ? N : 1) * sizeof(int64_t));
+  if (!e2e || !ttft) {
+    free(e2e); free(ttft);
+    return TSO_ERR_OOM;
+  }
   /* per-request records and per-point statistics */
   int64_t n_done = 0, n_rej = 0;
   uint64_t digest = 0;
   for (int32_t i = 0; i < N; i++) {
-    rq *r = &rs[i];
+    const rq *r = &rs[i];
     tso_req rec;
     rec.admit_ns = -1;
     rec.first_token_ns = -1;
@@ -603,7 +653,7 @@ int tso_simulate_point(const tso_model *m, const tso_trace *tr, const tso_point 
       if (r->last > out->last_finish_ns) out->last_finish_ns = r->last;
       if (tt <= slo_ttft && r->max_gap <= slo_tpot) out->slo_ok++;
       if (r->max_gap <= slo_tpot) out->slo_tpot_ok++;
-      if (check && r->gdone != olen[i]) nviol++;
+      if (check && r->gdone != olen[i]) (*nviol)++;
     } else if (r->phase == PH_REJECTED) {
       rec.status = TSO_REQ_REJECTED;
       n_rej++;
@@ -619,27 +669,297 @@ int tso_simulate_point(const tso_model *m, const tso_trace *tr, const tso_point 
   out->p50_ttft_ns = nearest_rank(ttft, n_done, 50);
   out->p99_ttft_ns = nearest_rank(ttft, n_done, 99);
   if (n_done == 0) out->max_e2e_ns = -1;
-
-  out->status = status;
   out->n_done = (int32_t)n_done;
   out->n_rejected = (int32_t)n_rej;
-  out->n_iters = n_iters;
-  out->n_preempt = n_preempt;
-  out->prefill_tokens = prefill_tokens;
-  out->decode_tokens = decode_tokens;
-  out->peak_used_blocks = peak_used;
-  out->used_block_ns = used_block_ns;
   out->digest = digest;
-  if (check && status == TSO_POINT_OK) {
-    int64_t want = 0;
-    for (int32_t i = 0; i < N; i++)
-      if (rs[i].phase == PH_DONE) want += olen[i];
-    if (want != decode_tokens) nviol++;
+  free(e2e); free(ttft);
+  return TSO_OK;
+}
+
+/* ------------------------------------------------------------ disaggregated */
+typedef struct {
+  int64_t key;  /* when the request's KV reaches its decode device */
+  int32_t idx;
+} arrival_key;
+
+static int cmp_arrival(const void *a, const void *b) {
+  const arrival_key *x = (const arrival_key *)a, *y = (const arrival_key *)b;
+  if (x->key != y->key) return (x->key > y->key) - (x->key < y->key);
+  return (x->idx > y->idx) - (x->idx < y->idx);
+}
+
+/* A disaggregated design point (Sec. II-B; validated against DistServe in
+ * Sec. III-C; device ratios and prefill-device hardware studied in Sec. V):
+ * n_prefill prefill devices with hardware p_*, and n_decode decode devices
+ * with the point's hardware and memory policy.  Readings:
+ *   - the global scheduler sends request i to prefill device i mod n_prefill
+ *     and then to decode device i mod n_decode (round robin in arrival
+ *     order);
+ *   - a prefill device runs continuous batching over prefills only; the
+ *     iteration that completes a prompt emits the first token and frees the
+ *     request's blocks; the prompt's KV then crosses the device's link
+ *     (WM_PREFILL, kv_link);
+ *   - the request reaches its decode device when that transfer ends, waits
+ *     there in (arrival, index) order, and runs its output decodes as on a
+ *     single worker (WM_DECODE), preemption included;
+ *   - a request is rejected up front when its prompt does not fit a prefill
+ *     device, or it could never fit a decode device.
+ * Point totals: iterations, tokens and the used-block integral summed over
+ * devices (prefill devices first, then decode devices, in index order), the
+ * block peak of the busiest decode device, the decode devices' block count. */
+static int simulate_pd(const tso_model *m, const tso_trace *tr, const tso_point *p,
+                       const tso_options *opt, tso_point_out *out, tso_req *out_req,
+                       int64_t *violations) {
+  if (p->n_prefill < 1 || p->n_prefill > TSO_MAX_DEVICES || p->n_decode < 1 ||
+      p->n_decode > TSO_MAX_DEVICES)
+    return TSO_ERR_ARG;
+  if (p->policy != TSO_POLICY_MIXED) return TSO_ERR_ARG;
+  if (!isfinite(p->p_peak_flops) || !(p->p_peak_flops > 0) || !isfinite(p->p_mem_bw) ||
+      !(p->p_mem_bw > 0) || p->p_capacity_bytes <= 0)
+    return TSO_ERR_ARG;
+  if (!isfinite(p->kv_link_bw) || !(p->kv_link_bw >= 0.0)) return TSO_ERR_ARG;
+  /* a prefill device: its own hardware, continuous batching, nothing else */
+  tso_point pp = *p;
+  pp.peak_flops = p->p_peak_flops;
+  pp.mem_bw = p->p_mem_bw;
+  pp.capacity_bytes = p->p_capacity_bytes;
+  pp.admit_mem_permille = 0;
+  pp.swap_bw = 0.0;
+  pp.swap_overlap = 0;
+  tso_derived dvp, dvd;
+  int rc = tso_derive(m, &pp, &dvp);
+  if (rc != TSO_OK) return rc;
+  rc = tso_derive(m, p, &dvd);
+  if (rc != TSO_OK) return rc;
+  const int64_t iter_cap = (opt && opt->iter_cap > 0) ? opt->iter_cap : DEFAULT_ITER_CAP;
+  const int64_t slo_ttft = (opt && opt->slo_ttft_ns > 0) ? opt->slo_ttft_ns : DEFAULT_SLO_TTFT;
+  const int64_t slo_tpot = (opt && opt->slo_tpot_ns > 0) ? opt->slo_tpot_ns : DEFAULT_SLO_TPOT;
+  const int check = opt ? opt->check_invariants : 0;
+
+  const int32_t N = tr->n;
+  const int64_t *arr = tr->arrival_ns;
+  const int32_t *plen = tr->prompt_len, *olen = tr->output_len;
+  for (int32_t i = 0; i < N; i++) {
+    if (plen[i] < 1 || olen[i] < 1 || arr[i] < 0) return TSO_ERR_ARG;
+    if (i > 0 && arr[i] < arr[i - 1]) return TSO_ERR_ARG;
+  }
+  const int64_t NBp = dvp.num_blocks, NBd = dvd.num_blocks, b = p->block_size;
+  const int64_t adm_cap = p->admit_mem_permille > 0 ? NBd * p->admit_mem_permille / 1000 : NBd;
+  if (p->swap_bw > 0.0 && NBd * b * dvd.kv_bytes_per_token >= (1LL << 53))
+    return TSO_ERR_UNSUPPORTED;
+
+  memset(out, 0, sizeof *out);
+  out->num_blocks = (int32_t)NBd;
+  out->first_arrival_ns = N > 0 ? arr[0] : -1;
+  out->last_finish_ns = -1;
+
+  const size_t n1 = (size_t)(N > 0 ? N : 1);
+  rq *g = (rq *)calloc(n1, sizeof(rq));        /* every request's final state */
+  rq *rw = (rq *)calloc(n1, sizeof(rq));       /* one device's requests */
+  int64_t *a2 = (int64_t *)malloc(n1 * sizeof(int64_t));
+  int32_t *ids = (int32_t *)malloc(n1 * sizeof(int32_t));
+  int64_t *arr_w = (int64_t *)malloc(n1 * sizeof(int64_t));
+  int32_t *plen_w = (int32_t *)malloc(n1 * sizeof(int32_t));
+  int32_t *olen_w = (int32_t *)malloc(n1 * sizeof(int32_t));
+  int64_t *arrive_w = (int64_t *)malloc(n1 * sizeof(int64_t));
+  arrival_key *keys = (arrival_key *)malloc(n1 * sizeof(arrival_key));
+  int32_t *prefilled = (int32_t *)calloc(n1, sizeof(int32_t));
+  if (!g || !rw || !a2 || !ids || !arr_w || !plen_w || !olen_w || !arrive_w || !keys ||
+      !prefilled) {
+    rc = TSO_ERR_OOM;
+    goto done;
+  }
+  for (int32_t i = 0; i < N; i++) {
+    rq *r = &g[i];
+    r->phase = (NBp == 0 || NBd == 0 || ceil_div(plen[i], b) > NBp ||
+                ceil_div((int64_t)plen[i] + olen[i], b) > NBd ||
+                ceil_div((int64_t)plen[i] + 1, b) > adm_cap) ? PH_REJECTED : PH_FUTURE;
+    r->target = plen[i];
+    r->admit = r->first = r->last = -1;
+  }
+  int32_t status = (NBp == 0 || NBd == 0) ? TSO_POINT_NO_KV : TSO_POINT_OK;
+  int64_t nviol = 0;
+  double ubns = 0.0;
+  const int32_t np = p->n_prefill, nd = p->n_decode;
+  for (int32_t w = 0; w < np && NBp > 0 && NBd > 0; w++) {
+    int32_t n = 0;
+    for (int32_t i = w; i < N; i += np) {
+      ids[n] = i;
+      arr_w[n] = arr[i];
+      plen_w[n] = plen[i];
+      olen_w[n] = olen[i];
+      memset(&rw[n], 0, sizeof(rq));
+      rw[n].phase = g[i].phase;
+      rw[n].target = plen[i];
+      rw[n].admit = rw[n].first = rw[n].last = -1;
+      rw[n].fresh = 1;
+      n++;
+    }
+    kv_link lk = {dvp.kv_bytes_per_token, p->kv_link_bw > 0.0 ? 1e9 / p->kv_link_bw : 0.0, 0,
+                  arrive_w};
+    worker_out wo;
+    rc = worker_loop(m, &pp, &dvp, WM_PREFILL, n, arr_w, plen_w, olen_w, rw, iter_cap, check,
+                     &lk, NULL, 0, &wo);
+    if (rc != TSO_OK) goto done;
+    if (wo.status > status) status = wo.status;
+    out->n_iters += wo.n_iters;
+    out->prefill_tokens += wo.prefill_tokens;
+    ubns = ubns + wo.used_block_ns;
+    nviol += wo.nviol;
+    for (int32_t k = 0; k < n; k++) {
+      if (rw[k].phase != PH_DONE) continue;
+      const int32_t i = ids[k];
+      g[i].admit = rw[k].admit;
+      g[i].first = rw[k].first;
+      a2[i] = arrive_w[k];
+      prefilled[i] = 1;
+    }
+  }
+  for (int32_t v = 0; v < nd && NBp > 0 && NBd > 0; v++) {
+    int32_t n = 0;
+    for (int32_t i = v; i < N; i += nd)
+      if (prefilled[i]) {
+        keys[n].key = a2[i];
+        keys[n].idx = i;
+        n++;
+      }
+    qsort(keys, (size_t)n, sizeof(arrival_key), cmp_arrival);
+    for (int32_t k = 0; k < n; k++) {
+      const int32_t i = keys[k].idx;
+      ids[k] = i;
+      arr_w[k] = a2[i];
+      plen_w[k] = plen[i];
+      olen_w[k] = olen[i];
+      memset(&rw[k], 0, sizeof(rq));
+      rw[k].phase = PH_FUTURE;
+      rw[k].ctx = plen[i];  /* the prompt's KV came over the link */
+      rw[k].target = plen[i];
+      rw[k].admit = g[i].admit;
+      rw[k].first = g[i].first;
+      rw[k].last = g[i].first;
+      rw[k].fresh = 1;
+    }
+    worker_out wo;
+    rc = worker_loop(m, p, &dvd, WM_DECODE, n, arr_w, plen_w, olen_w, rw, iter_cap, check, NULL,
+                     NULL, 0, &wo);
+    if (rc != TSO_OK) goto done;
+    if (wo.status > status) status = wo.status;
+    out->n_iters += wo.n_iters;
+    out->n_preempt += wo.n_preempt;
+    out->prefill_tokens += wo.prefill_tokens;
+    out->decode_tokens += wo.decode_tokens;
+    if (wo.peak_used > out->peak_used_blocks) out->peak_used_blocks = wo.peak_used;
+    ubns = ubns + wo.used_block_ns;
+    nviol += wo.nviol;
+    for (int32_t k = 0; k < n; k++) {
+      const int32_t i = ids[k];
+      g[i].phase = rw[k].phase == PH_DONE ? PH_DONE : PH_RUNNING;
+      g[i].last = rw[k].last;
+      g[i].max_gap = rw[k].max_gap;
+      g[i].n_pre = rw[k].n_pre;
+      g[i].gdone = rw[k].gdone;
+    }
+  }
+  {
+    int64_t iters = out->n_iters, npre = out->n_preempt, pft = out->prefill_tokens,
+            dct = out->decode_tokens, peak = out->peak_used_blocks;
+    rc = point_stats(N, arr, olen, g, slo_ttft, slo_tpot, check, out, out_req, &nviol);
+    out->n_iters = iters;
+    out->n_preempt = npre;
+    out->prefill_tokens = pft;
+    out->decode_tokens = dct;
+    out->peak_used_blocks = peak;
+  }
+  out->status = status;
+  out->used_block_ns = ubns;
+  if (violations) *violations = nviol;
+done:
+  free(g); free(rw); free(a2); free(ids); free(arr_w); free(plen_w); free(olen_w);
+  free(arrive_w); free(keys); free(prefilled);
+  return rc;
+}
+
+int tso_simulate_point(const tso_model *m, const tso_trace *tr, const tso_point *p,
+                       const tso_options *opt, tso_point_out *out, tso_req *out_req,
+                       tso_iter_rec *log, int64_t log_cap, int64_t *n_log,
+                       int64_t *violations) {
+  if (!m || !tr || !p || !out) return TSO_ERR_ARG;
+  if (tr->n < 0 || (tr->n > 0 && (!tr->arrival_ns || !tr->prompt_len || !tr->output_len)))
+    return TSO_ERR_ARG;
+  if ((p->n_prefill != 0 || p->n_decode != 0) && log && log_cap > 0)
+    return TSO_ERR_ARG;  /* iteration logs: one-worker points only */
+  if (p->max_batch < 1 || p->block_size < 1) return TSO_ERR_ARG;
+  if (p->policy < TSO_POLICY_MIXED || p->policy > TSO_POLICY_STATIC) return TSO_ERR_ARG;
+  if (p->chunk_size != 0 && p->chunk_size < p->max_batch) return TSO_ERR_ARG;
+  if (p->policy == TSO_POLICY_PREFILL_FIRST && p->chunk_size != 0) return TSO_ERR_ARG;
+  if (p->admit_mem_permille < 0 || p->admit_mem_permille > 1000) return TSO_ERR_ARG;
+  if (!(p->swap_bw >= 0.0) || !isfinite(p->swap_bw)) return TSO_ERR_ARG;
+  if (p->swap_overlap != 0 && p->swap_overlap != 1) return TSO_ERR_ARG;
+  if (p->n_prefill != 0 || p->n_decode != 0) {
+    int64_t nv = 0;
+    int rc = simulate_pd(m, tr, p, opt, out, out_req, &nv);
+    if (n_log) *n_log = 0;
+    if (violations) *violations = nv;
+    return rc;
+  }
+  tso_derived dv;
+  int rc = tso_derive(m, p, &dv);
+  if (rc != TSO_OK) return rc;
+
+  const int64_t iter_cap = (opt && opt->iter_cap > 0) ? opt->iter_cap : DEFAULT_ITER_CAP;
+  const int64_t slo_ttft = (opt && opt->slo_ttft_ns > 0) ? opt->slo_ttft_ns : DEFAULT_SLO_TTFT;
+  const int64_t slo_tpot = (opt && opt->slo_tpot_ns > 0) ? opt->slo_tpot_ns : DEFAULT_SLO_TPOT;
+  const int check = opt ? opt->check_invariants : 0;
+
+  const int32_t N = tr->n;
+  const int64_t *arr = tr->arrival_ns;
+  const int32_t *plen = tr->prompt_len, *olen = tr->output_len;
+  for (int32_t i = 0; i < N; i++) {
+    if (plen[i] < 1 || olen[i] < 1 || arr[i] < 0) return TSO_ERR_ARG;
+    if (i > 0 && arr[i] < arr[i - 1]) return TSO_ERR_ARG;
+  }
+  const int64_t NB = dv.num_blocks, b = p->block_size;
+  const int64_t adm_cap = p->admit_mem_permille > 0 ? NB * p->admit_mem_permille / 1000 : NB;
+  if (p->swap_bw > 0.0 && NB * b * dv.kv_bytes_per_token >= (1LL << 53))
+    return TSO_ERR_UNSUPPORTED;
+
+  memset(out, 0, sizeof *out);
+  out->num_blocks = (int32_t)NB;
+  out->first_arrival_ns = N > 0 ? arr[0] : -1;
+  out->last_finish_ns = -1;
+
+  rq *rs = (rq *)calloc((size_t)(N > 0 ? N : 1), sizeof(rq));
+  if (!rs) return TSO_ERR_OOM;
+
+  /* A request that could not fit even alone is rejected up front: with
+   * recompute preemption it would otherwise never finish.  So is one whose
+   * prompt alone exceeds what a first admission may use. */
+  for (int32_t i = 0; i < N; i++) {
+    rq *r = &rs[i];
+    r->phase = (NB == 0 || ceil_div((int64_t)plen[i] + olen[i], b) > NB ||
+                ceil_div(plen[i], b) > adm_cap) ? PH_REJECTED : PH_FUTURE;
+    r->target = plen[i];
+    r->admit = r->first = r->last = -1;
+    r->fresh = 1;
   }
 
-  if (n_log) *n_log = nlog;
-  if (violations) *violations = nviol;
-  free(rs); free(running); free(waiting); free(e2e); free(ttft);
+  worker_out wo;
+  int64_t nviol = 0;
+  rc = worker_loop(m, p, &dv, WM_FULL, N, arr, plen, olen, rs, iter_cap, check, NULL, log,
+                   log_cap, &wo);
+  if (rc == TSO_OK)
+    rc = point_stats(N, arr, olen, rs, slo_ttft, slo_tpot, check, out, out_req, &nviol);
+  free(rs);
+  if (rc != TSO_OK) return rc;
+  out->status = wo.status;
+  out->n_iters = wo.n_iters;
+  out->n_preempt = wo.n_preempt;
+  out->prefill_tokens = wo.prefill_tokens;
+  out->decode_tokens = wo.decode_tokens;
+  out->peak_used_blocks = wo.peak_used;
+  out->used_block_ns = wo.used_block_ns;
+  if (n_log) *n_log = wo.nlog;
+  if (violations) *violations = nviol + wo.nviol;
   return TSO_OK;
 }
 

@@ -46,6 +46,8 @@ enum { TSO_REQ_PENDING = 0, TSO_REQ_DONE = 1, TSO_REQ_REJECTED = 2 };
  *                  runs every decode; needs chunk_size 0;
  *   STATIC         a batch is admitted only when nothing runs. */
 enum { TSO_POLICY_MIXED = 0, TSO_POLICY_PREFILL_FIRST = 1, TSO_POLICY_STATIC = 2 };
+/* largest number of prefill, and of decode, devices of a disaggregated point */
+enum { TSO_MAX_DEVICES = 16 };
 
 typedef struct {
   int32_t n_layers, d_model, n_heads, n_kv_heads;
@@ -83,6 +85,17 @@ typedef struct {
                                   their KV blocks to host memory (Sec. IV-B)
                                   and back, priced by the communication model
                                   (Sec. III-B) */
+  /* Disaggregated prefill and decode (Sec. II-B; Sec. III-C, Sec. V): with
+   * n_prefill > 0 the point is n_prefill prefill devices with hardware p_*
+   * and n_decode decode devices with the hardware and memory policy above
+   * (policy MIXED only); each prefill device sends a prompt's KV over its
+   * own link of kv_link_bw B/s (0 = instant) to the request's decode device. */
+  int32_t n_prefill;           /* 0 = one worker; else 1..TSO_MAX_DEVICES */
+  int32_t n_decode;            /* 1..TSO_MAX_DEVICES with n_prefill > 0, else 0 */
+  double p_peak_flops;
+  double p_mem_bw;
+  int64_t p_capacity_bytes;
+  double kv_link_bw;
 } tso_point;
 
 typedef struct {
@@ -141,10 +154,11 @@ double tso_iter_total(const tso_model *m, double inv_flops_ns, double inv_bw_ns,
                       int32_t n, const int32_t *q, const int32_t *c0,
                       const int32_t *is_prefill, const int32_t *completes);
 
-/* Simulate one design point.  out_req: trace.n records (may be NULL);
+/* Simulate one design point, disaggregated or not.  out_req: trace.n
+ * records (may be NULL);
  * log: up to log_cap iteration records (may be NULL); *n_log receives the
- * number of iterations logged; *violations (may be NULL) the number of
- * invariant violations when opt->check_invariants is set. */
+ * number of iterations logged (one-worker points only); *violations (may be
+ * NULL) the number of invariant violations when opt->check_invariants is set. */
 int tso_simulate_point(const tso_model *m, const tso_trace *tr, const tso_point *p,
                        const tso_options *opt, tso_point_out *out, tso_req *out_req,
                        tso_iter_rec *log, int64_t log_cap, int64_t *n_log,

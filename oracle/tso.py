@@ -52,7 +52,24 @@ class Point(C.Structure):
                 ("block_size", C.c_int32), ("max_batch", C.c_int32),
                 ("chunk_size", C.c_int32), ("trace_id", C.c_int32), ("policy", C.c_int32),
                 ("admit_mem_permille", C.c_int32), ("swap_overlap", C.c_int32),
-                ("pad", C.c_int32), ("swap_bw", C.c_double)]
+                ("pad", C.c_int32), ("swap_bw", C.c_double),
+                ("n_prefill", C.c_int32), ("n_decode", C.c_int32),
+                ("p_peak_flops", C.c_double), ("p_mem_bw", C.c_double),
+                ("p_capacity_bytes", C.c_int64), ("kv_link_bw", C.c_double)]
+
+# optional point fields and their defaults (a missing key means the default)
+_OPTIONAL = {"mem_util_permille": 1000, "chunk_size": 0, "trace_id": 0, "policy": 0,
+             "admit_mem_permille": 0, "swap_overlap": 0, "pad": 0, "swap_bw": 0.0,
+             "n_prefill": 0, "n_decode": 0, "p_peak_flops": 0.0, "p_mem_bw": 0.0,
+             "p_capacity_bytes": 0, "kv_link_bw": 0.0}
+
+
+def _make_point(get) -> "Point":
+    vals = []
+    for name, ty in Point._fields_:
+        v = get(name)
+        vals.append(float(v) if ty is C.c_double else int(v))
+    return Point(*vals)
 
 
 class Options(C.Structure):
@@ -129,22 +146,11 @@ def _model(m: dict) -> Model:
 
 
 def _point(pts: dict, i: int) -> Point:
-    return Point(float(pts["peak_flops"][i]), float(pts["mem_bw"][i]),
-                 int(pts["capacity_bytes"][i]), int(pts["mem_util_permille"][i]),
-                 int(pts["block_size"][i]), int(pts["max_batch"][i]),
-                 int(pts["chunk_size"][i]), int(pts["trace_id"][i]),
-                 int(pts["policy"][i]) if "policy" in pts else 0,
-                 int(pts["admit_mem_permille"][i]) if "admit_mem_permille" in pts else 0,
-                 int(pts["swap_overlap"][i]) if "swap_overlap" in pts else 0, 0,
-                 float(pts["swap_bw"][i]) if "swap_bw" in pts else 0.0)
+    return _make_point(lambda f: pts[f][i] if f in pts else _OPTIONAL[f])
 
 
 def _single_point(p: dict) -> Point:
-    return Point(float(p["peak_flops"]), float(p["mem_bw"]), int(p["capacity_bytes"]),
-                 int(p.get("mem_util_permille", 1000)), int(p["block_size"]),
-                 int(p["max_batch"]), int(p.get("chunk_size", 0)), int(p.get("trace_id", 0)),
-                 int(p.get("policy", 0)), int(p.get("admit_mem_permille", 0)),
-                 int(p.get("swap_overlap", 0)), 0, float(p.get("swap_bw", 0.0)))
+    return _make_point(lambda f: p[f] if f in p else _OPTIONAL[f])
 
 
 class _TraceKeep:

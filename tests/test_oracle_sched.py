@@ -37,17 +37,23 @@ HAND_MODEL, HAND_CASES = _hand_cases()
 def hand_point(case):
     nb, b = case["num_blocks"], case["block_size"]
     cap = nb * b * 16 if nb > 0 else 1   # the toy model stores 16 B of KV per token
-    return dict(peak_flops=INF, mem_bw=INF, capacity_bytes=cap, mem_util_permille=1000,
-                block_size=b, max_batch=case["max_batch"], chunk_size=case["chunk_size"],
-                policy=case.get("policy", 0),
-                admit_mem_permille=case.get("admit_mem_permille", 0),
-                swap_bw=case.get("swap_bw", 0.0), swap_overlap=case.get("swap_overlap", 0))
+    pt = dict(peak_flops=INF, mem_bw=INF, capacity_bytes=cap, mem_util_permille=1000,
+              block_size=b, max_batch=case["max_batch"], chunk_size=case["chunk_size"],
+              policy=case.get("policy", 0),
+              admit_mem_permille=case.get("admit_mem_permille", 0),
+              swap_bw=case.get("swap_bw", 0.0), swap_overlap=case.get("swap_overlap", 0))
+    if case.get("n_prefill", 0) > 0:  # disaggregated: prefill devices as fast, own memory
+        pt.update(n_prefill=case["n_prefill"], n_decode=case["n_decode"], p_peak_flops=INF,
+                  p_mem_bw=INF, p_capacity_bytes=max(1, case["prefill_blocks"] * b * 16),
+                  kv_link_bw=case["kv_link_bw"])
+    return pt
 
 
 @pytest.mark.parametrize("case", HAND_CASES, ids=[c["name"] for c in HAND_CASES])
 def test_hand_traced_schedules(oracle, case):
+    log_cap = 0 if case.get("n_prefill", 0) > 0 else 1000
     out, req, log, viol = oracle.simulate_point(HAND_MODEL, _trace(case["requests"]),
-                                                hand_point(case), log_cap=1000)
+                                                hand_point(case), log_cap=log_cap)
     assert viol == 0
     got = [[int(r["admit_ns"]), int(r["first_token_ns"]), int(r["finish_ns"]),
             int(r["max_gap_ns"]), int(r["n_preempt"]), int(r["status"])] for r in req]

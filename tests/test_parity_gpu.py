@@ -80,6 +80,8 @@ def hand_sweep():
     with open(os.path.join(GOLD, "hand_traces.json")) as f:
         g = json.load(f)
     traces, rows = [], []
+    # disaggregated cases join once the kernels run them
+    g["cases"] = [c for c in g["cases"] if c.get("n_prefill", 0) == 0]
     for k, c in enumerate(g["cases"]):
         r = c["requests"]
         traces.append({"arrival_ns": np.array([x[0] for x in r], np.int64),
