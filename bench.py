@@ -43,7 +43,10 @@ if ROOT not in sys.path:
 METRIC = "simulated requests/sec across sweep on 1 MI355X; % VALU-issue peak"
 VALU_ISSUE_PEAK = 256 * 4 * 2.4e9 / 4.0   # wave64 VALU instructions per second
 U_ITER = 21.0
-KERNEL_NAMES = ("sim_kernel<1>", "sim_kernel<2>", "sim_kernel<4>")
+# simulation launches, 3 * stage + class (stages: one-worker points, prefill
+# devices, decode devices of disaggregated points; register-chunk classes
+# 1, 2, 4), named as rocprofv3 names the kernels
+KERNEL_NAMES = tuple("sim_kernel<%d,%d>" % (c, st) for st in range(3) for c in (1, 2, 4))
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "sim_kernel_traffic_c5.md")
@@ -199,18 +202,23 @@ def main():
     value = n_req / (total_s / args.steps)
     status = np.bincount(out["status"], minlength=4).tolist()
 
-    # roofline of the dominant simulation kernel (longest mean duration)
+    # roofline of the dominant simulation kernel (longest mean duration); a
+    # disaggregated point's iterations are spread over its devices' launches,
+    # so with any such point the figure covers all simulation launches
     kmean = np.mean(np.array(kms), axis=0)
+    disagg = "n_prefill" in points and bool((np.asarray(points["n_prefill"]) > 0).any())
     cls = kernel_class(points["max_batch"])
     w = algorithmic_instructions(out)
-    k = int(np.argmax(kmean))
-    w_k = float(w[cls == k].sum())
-    achieved = w_k / (kmean[k] * 1e-3)
+    if disagg:
+        name, w_k, k_ms, traffic = "all simulation launches", float(w.sum()), float(kmean.sum()), None
+    else:
+        k = int(np.argmax(kmean))
+        name, w_k, k_ms = KERNEL_NAMES[k], float(w[cls == k].sum()), float(kmean[k])
+        traffic = recorded_traffic(args.config, name)
+    achieved = w_k / (k_ms * 1e-3)
     roofline = {"bound": "alu", "achieved": achieved / 1e9, "peak": VALU_ISSUE_PEAK / 1e9,
                 "unit": "G wave64 VALU instr/s", "frac": achieved / VALU_ISSUE_PEAK,
-                "traffic": recorded_traffic(args.config, KERNEL_NAMES[k]),
-                "kernel": KERNEL_NAMES[k],
-                "algorithmic_instr": w_k, "kernel_ms": float(kmean[k])}
+                "traffic": traffic, "kernel": name, "algorithmic_instr": w_k, "kernel_ms": k_ms}
 
     line = {
         "metric": METRIC, "value": value, "unit": "simulated requests/s", "n_gpus": 1,
@@ -222,12 +230,14 @@ def main():
                    "model": "none (simulated transformer shape)",
                    "parallelism": "one wave64 workgroup per design point"},
         "roofline": roofline,
-        "kernels_ms": {KERNEL_NAMES[i]: float(kmean[i]) for i in range(3) if kmean[i] > 0},
+        "kernels_ms": {KERNEL_NAMES[i]: float(kmean[i]) for i in range(len(kmean))
+                       if kmean[i] > 0},
         "simulation_phase_ms": float(np.mean(sim_ms)), "statistics_ms": float(np.mean(stats_ms)),
         "results_copy_ms": 1e3 * results_s,
         "simulated_iterations": int(out["n_iters"].sum()),
-        "simulated_iterations_by_kernel": {KERNEL_NAMES[i]: int(out["n_iters"][cls == i].sum())
-                                           for i in range(3) if (cls == i).any()},
+        "simulated_iterations_by_kernel": (
+            {} if disagg else {KERNEL_NAMES[i]: int(out["n_iters"][cls == i].sum())
+                               for i in range(3) if (cls == i).any()}),
         "point_status_counts": status,
     }
     if args.cpu_seconds > 0:

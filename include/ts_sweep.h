@@ -56,8 +56,9 @@
 extern "C" {
 #endif
 
-#define TS_ABI_VERSION 3
+#define TS_ABI_VERSION 4
 #define TS_MAX_BATCH 256 /* running-set cap per design point */
+#define TS_MAX_DEVICES 16 /* prefill, and decode, devices of a disaggregated point */
 
 /* call status */
 #define TS_OK 0
@@ -146,6 +147,28 @@ typedef struct {
                                  (no re-prefill, no token budget) and the request works
                                  again from the next iteration.  An iteration's
                                  transfers take blocks * block bytes / swap_bw ns */
+  /* Disaggregated prefill and decode (Sec. II-B; breakpoints and a global
+   * scheduler, Sec. III-A; validated against DistServe, Sec. III-C; device
+   * ratios and prefill hardware, Sec. V).  n_prefill = n_decode = 0: one
+   * worker.  Otherwise the point is n_prefill prefill devices with hardware
+   * p_* (same memory utilisation, block size, max_batch and chunk_size;
+   * continuous batching over prefills only) and n_decode decode devices
+   * with the hardware and memory policy above (policy MIXED only).  Request
+   * i goes to prefill device i % n_prefill, which frees its blocks when its
+   * prefill completes (the first token); its prompt's KV then crosses that
+   * device's link, one transfer after another in completion order, each
+   * ceil(prompt * KV bytes per token * 1e9 / kv_link_bw) ns (0 = instant).
+   * At the transfer's end it reaches decode device i % n_decode and waits
+   * in (arrival there, index) order; admission takes blocks for its KV and
+   * the next token plus one token of budget, and it decodes at once.  A
+   * request is rejected up front when its prompt does not fit a prefill
+   * device or it could never fit a decode device. */
+  int32_t n_prefill;          /* 0, or 1..TS_MAX_DEVICES */
+  int32_t n_decode;           /* 0 with n_prefill 0, else 1..TS_MAX_DEVICES */
+  double p_peak_flops;        /* prefill devices: FLOP/s, finite, > 0 */
+  double p_mem_bw;            /* prefill devices: bytes/s, finite, > 0 */
+  int64_t p_capacity_bytes;   /* prefill devices: > 0 */
+  double kv_link_bw;          /* bytes/s of each prefill device's KV link, finite, >= 0 */
 } ts_point;
 
 /* Per-request record (TS_F_PER_REQUEST): 40 bytes. */
@@ -225,13 +248,15 @@ int ts_sweep_shape(const ts_sweep *h, int32_t *n_points, int32_t *max_n);
 int ts_sweep_timing(ts_sweep *h, float *sim_ms, float *stats_ms);
 
 /* Per-kernel device time of the last run.  The points are simulated by up
- * to TS_N_SIM_KERNELS kernels, one per register-chunk class (max_batch
- * <= 64, <= 128, <= 256), launched one after another on the run's stream.
- * ms[k] receives kernel k's duration in milliseconds from HIP events
- * recorded around it on that stream (0 when the class has no points) and
- * n_points[k] its number of points.  Waits for the run.  TS_ERR_STATE
- * before the first run. */
-#define TS_N_SIM_KERNELS 3
+ * to TS_N_SIM_KERNELS kernel launches, one per stage and register-chunk
+ * class, launched one after another on the run's stream: index
+ * 3 * stage + class, stage 0 for one-worker points, 1 for the prefill
+ * devices and 2 for the decode devices of disaggregated points, class 0, 1,
+ * 2 for max_batch <= 64, <= 128, <= 256.  ms[k] receives launch k's duration
+ * in milliseconds from HIP events recorded around it on that stream (0 when
+ * it has no work) and n_points[k] its number of simulated workers.  Waits
+ * for the run.  TS_ERR_STATE before the first run. */
+#define TS_N_SIM_KERNELS 9
 int ts_sweep_kernel_timing(ts_sweep *h, float *ms, int32_t *n_points);
 
 /* Release the handle and its device memory; NULL is accepted. */

@@ -13,6 +13,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <map>
 #include <new>
 #include <numeric>
 #include <vector>
@@ -20,8 +21,13 @@
 #include "sweep_internal.h"
 
 namespace tsw {
-template <int NCH>
+template <int NCH, int MODE>
 __global__ void sim_kernel(SimArgs A);
+__global__ void pd_merge_kernel(const PdAux* aux, int n_aux, const int64_t* sub_a2,
+                                const int32_t* sub_gid, TraceRec* recs, int32_t* gids,
+                                DevPoint* units);
+__global__ void pd_combine_kernel(const PdAux* aux, int n_aux, ts_point_result* res,
+                                  const TraceRec* recs, int64_t* e2e, int64_t* ttft, int max_n);
 __global__ void stats_kernel(const int64_t* e2e, const int64_t* ttft, ts_point_result* res,
                              int max_n, int n_points);
 __global__ void fill_pending_kernel(ts_req_result* r, size_t n);
@@ -36,6 +42,23 @@ thread_local char g_err[256];
 
 constexpr int kClasses = 3;                 // register chunks per lane: 1, 2, 4
 constexpr int kClassChunks[kClasses] = {1, 2, 4};
+constexpr int kLaunches = kStages * kClasses;  // launch 3 * stage + class
+static_assert(kLaunches == TS_N_SIM_KERNELS, "one timing entry per launch");
+
+const void* sim_kernel_fn(int launch) {
+  const int st = launch / kClasses, c = launch % kClasses;
+  switch (st * 8 + kClassChunks[c]) {
+    case 0 * 8 + 1: return (const void*)sim_kernel<1, kStageOne>;
+    case 0 * 8 + 2: return (const void*)sim_kernel<2, kStageOne>;
+    case 0 * 8 + 4: return (const void*)sim_kernel<4, kStageOne>;
+    case 1 * 8 + 1: return (const void*)sim_kernel<1, kStagePrefill>;
+    case 1 * 8 + 2: return (const void*)sim_kernel<2, kStagePrefill>;
+    case 1 * 8 + 4: return (const void*)sim_kernel<4, kStagePrefill>;
+    case 2 * 8 + 1: return (const void*)sim_kernel<1, kStageDecode>;
+    case 2 * 8 + 2: return (const void*)sim_kernel<2, kStageDecode>;
+    default: return (const void*)sim_kernel<4, kStageDecode>;
+  }
+}
 
 int class_of(int max_batch) { return max_batch <= 64 ? 0 : (max_batch <= 128 ? 1 : 2); }
 
@@ -186,7 +209,7 @@ struct ts_sweep {
   LaneCoef lc{};
   TraceRec* d_recs = nullptr;
   DevPoint* d_points = nullptr;
-  int32_t* d_order = nullptr;       // all classes, concatenated
+  int32_t* d_order = nullptr;       // all launches, concatenated
   unsigned int* d_counter = nullptr;
   QEntry* d_queue = nullptr;        // kQueueCap per workgroup, shared by the classes
   ReqTimes* d_times = nullptr;      // max_n per workgroup, shared by the classes
@@ -194,12 +217,20 @@ struct ts_sweep {
   ts_req_result* d_req = nullptr;
   int64_t* d_e2e = nullptr;
   int64_t* d_ttft = nullptr;
-  int class_off[kClasses] = {0, 0, 0}, class_n[kClasses] = {0, 0, 0};
-  int grid[kClasses] = {0, 0, 0};
+  // disaggregated points
+  int32_t n_pd = 0;
+  PdAux* d_pd = nullptr;
+  int64_t* d_s1_admit = nullptr;
+  int64_t* d_s1_first = nullptr;
+  int64_t* d_sub_a2 = nullptr;
+  int32_t* d_sub_gid = nullptr;
+  int32_t* d_gids = nullptr;
+  int class_off[kLaunches] = {}, class_n[kLaunches] = {};
+  int grid[kLaunches] = {};
   int stats_grid = 0;
   hipEvent_t ev_t0 = nullptr, ev_t1 = nullptr, ev_t2 = nullptr;
-  hipEvent_t ev_k0[kClasses] = {nullptr, nullptr, nullptr};
-  hipEvent_t ev_k1[kClasses] = {nullptr, nullptr, nullptr};
+  hipEvent_t ev_k0[kLaunches] = {};
+  hipEvent_t ev_k1[kLaunches] = {};
   hipStream_t last_stream = nullptr;
   bool ran = false;
 };
@@ -218,7 +249,13 @@ void release(ts_sweep* h) {
   (void)hipFree(h->d_req);
   (void)hipFree(h->d_e2e);
   (void)hipFree(h->d_ttft);
-  for (int c = 0; c < kClasses; ++c) {
+  (void)hipFree(h->d_pd);
+  (void)hipFree(h->d_s1_admit);
+  (void)hipFree(h->d_s1_first);
+  (void)hipFree(h->d_sub_a2);
+  (void)hipFree(h->d_sub_gid);
+  (void)hipFree(h->d_gids);
+  for (int c = 0; c < kLaunches; ++c) {
     if (h->ev_k0[c]) (void)hipEventDestroy(h->ev_k0[c]);
     if (h->ev_k1[c]) (void)hipEventDestroy(h->ev_k1[c]);
   }
@@ -315,8 +352,36 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
       sh.e * (sh.L * (sh.d * (sh.d + 2 * sh.dkv) + sh.d * sh.d + (sh.g + 1) * sh.d * sh.f) +
               2 * sh.V * sh.d);
 
-  std::vector<DevPoint> dp((size_t)count);
-  std::vector<double> est((size_t)count);
+  // KV blocks of a device: floor(capacity * util / 1000), minus the weights
+  // when they share the memory, in whole blocks of block_size tokens
+  auto blocks_of = [&](int64_t capacity, int32_t util, int32_t block, int64_t* nb) {
+    const __int128 usable = ((__int128)capacity * util) / 1000;
+    const __int128 budget = usable - (model->weights_in_capacity ? weights : 0);
+    const __int128 per_block = (__int128)block * kv_tok;
+    const __int128 v = budget > 0 ? budget / per_block : 0;
+    if (v > ((__int128)1 << 30)) return false;
+    *nb = (int64_t)v;
+    return true;
+  };
+
+  // ---------------------------------------------------------- simulation units
+  // A one-worker point is one unit.  A disaggregated point is n_prefill
+  // prefill-device units, each over its share of the trace (request i goes
+  // to prefill device i % n_prefill), and n_decode decode-device units, each
+  // over the arrivals of the KV that the merge kernel writes on the device.
+  std::vector<DevPoint> dp;
+  std::vector<double> est;
+  std::vector<int> stage;
+  std::vector<PdAux> aux;
+  dp.reserve((size_t)count);
+  est.reserve((size_t)count);
+  stage.reserve((size_t)count);
+  int64_t n_extra = 0;     // device result records, after the points' own
+  int64_t pd_reqs = 0;     // per-request entries of the disaggregated points
+  int64_t extra_recs = 0;  // trace records after the traces: shares, then arrivals
+  std::map<std::pair<int, int>, int64_t> share_at;  // (trace, n_prefill) -> first share record
+  std::vector<std::pair<int, int>> shares;
+  std::vector<int64_t> dec_region;  // per disaggregated point: its arrival records
   for (int i = 0; i < count; ++i) {
     const ts_point& p = points[first + i];
     if (!std::isfinite(p.peak_flops) || !(p.peak_flops > 0) || !std::isfinite(p.mem_bw) ||
@@ -335,30 +400,40 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
     if (p.admit_mem_permille < 0 || p.admit_mem_permille > 1000) return TS_ERR_ARG;
     if (!std::isfinite(p.swap_bw) || !(p.swap_bw >= 0.0)) return TS_ERR_ARG;
     if (p.swap_overlap != 0 && p.swap_overlap != 1) return TS_ERR_ARG;
-    // KV block budget: floor(capacity * util / 1000), minus the weights when
-    // they share the memory, in whole blocks of block_size tokens
-    const __int128 usable = ((__int128)p.capacity_bytes * p.mem_util_permille) / 1000;
-    const __int128 budget = usable - (model->weights_in_capacity ? weights : 0);
-    const __int128 per_block = (__int128)p.block_size * kv_tok;
-    const __int128 nb = budget > 0 ? budget / per_block : 0;
-    if (nb > ((__int128)1 << 30)) return TS_ERR_UNSUPPORTED;
+    const bool disagg = p.n_prefill != 0 || p.n_decode != 0;
+    if (disagg) {
+      if (p.n_prefill < 1 || p.n_prefill > TS_MAX_DEVICES || p.n_decode < 1 ||
+          p.n_decode > TS_MAX_DEVICES)
+        return TS_ERR_ARG;
+      if (p.policy != TS_POLICY_MIXED) return TS_ERR_ARG;
+      if (!std::isfinite(p.p_peak_flops) || !(p.p_peak_flops > 0) ||
+          !std::isfinite(p.p_mem_bw) || !(p.p_mem_bw > 0) || p.p_capacity_bytes <= 0)
+        return TS_ERR_ARG;
+      if (!std::isfinite(p.kv_link_bw) || !(p.kv_link_bw >= 0.0)) return TS_ERR_ARG;
+    }
+    int64_t nb = 0;
+    if (!blocks_of(p.capacity_bytes, p.mem_util_permille, p.block_size, &nb))
+      return TS_ERR_UNSUPPORTED;
     const TraceStats& ts = tstats[(size_t)p.trace_id];
-    DevPoint& d = dp[(size_t)i];
+    const int32_t N = traces[p.trace_id].n;
+    // the worker (or decode devices) of the point: hardware and memory policy
+    DevPoint d{};
     d.inv_flops_ns = 1e9 / p.peak_flops;
     d.inv_bw_ns = 1e9 / p.mem_bw;
     d.num_blocks = (int32_t)nb;
     d.block = p.block_size;
-    d.cap_tokens = (int64_t)nb * p.block_size;
+    d.cap_tokens = nb * p.block_size;
     d.max_batch = p.max_batch;
     d.chunk = p.chunk_size;
     d.trace_off = (int32_t)toff[(size_t)p.trace_id];
-    d.n = traces[p.trace_id].n;
+    d.n = N;
     d.out_index = i;
+    d.out_point = i;
+    d.pd = -1;
     // blocks a first admission may leave in use; the rest is reserved
-    const int64_t adm_cap =
-        p.admit_mem_permille > 0 ? (int64_t)nb * p.admit_mem_permille / 1000 : (int64_t)nb;
+    const int64_t adm_cap = p.admit_mem_permille > 0 ? nb * p.admit_mem_permille / 1000 : nb;
     d.policy = p.policy;
-    d.adm_reserve = (int32_t)((int64_t)nb - adm_cap);
+    d.adm_reserve = (int32_t)(nb - adm_cap);
     d.cap_prompt = adm_cap * p.block_size;
     d.may_reject = (ts.max_po > d.cap_tokens || ts.max_p > d.cap_prompt) ? 1 : 0;
     // swap preemption: an iteration moves at most every block once (out, or
@@ -368,30 +443,145 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
     d.block_bytes = (int64_t)p.block_size * kv_tok;
     d.inv_link_ns = d.swap ? 1e9 / p.swap_bw : 0.0;
     if (d.swap && (__int128)nb * d.block_bytes >= ((__int128)1 << 53)) return TS_ERR_UNSUPPORTED;
-    const double xfer_max = (double)((int64_t)nb * d.block_bytes) * d.inv_link_ns;
+    const double xfer_max = (double)(nb * d.block_bytes) * d.inv_link_ns;
     if (!exact_and_bounded(coef, ts.max_po, p.max_batch, p.chunk_size, d.inv_flops_ns,
                            d.inv_bw_ns, xfer_max, &d.lg_iter))
       return TS_ERR_UNSUPPORTED;
-    est[(size_t)i] = work_estimate(ts, d.n, p.max_batch, p.chunk_size, p.peak_flops, p.mem_bw,
-                                   (double)weights);
+    if (!disagg) {
+      dp.push_back(d);
+      est.push_back(work_estimate(ts, N, p.max_batch, p.chunk_size, p.peak_flops, p.mem_bw,
+                                  (double)weights));
+      stage.push_back(kStageOne);
+      continue;
+    }
+    // ---- a disaggregated point
+    int64_t nbp = 0;
+    if (!blocks_of(p.p_capacity_bytes, p.mem_util_permille, p.block_size, &nbp))
+      return TS_ERR_UNSUPPORTED;
+    const int n_p = p.n_prefill, n_d = p.n_decode;
+    if (pd_reqs + N > INT32_MAX) return TS_ERR_UNSUPPORTED;
+    PdAux X{};
+    X.n_p = n_p;
+    X.n_d = n_d;
+    X.point = i;
+    X.res0 = (int32_t)(count + n_extra);
+    X.trace_off = d.trace_off;
+    X.n = N;
+    X.req_base = (int32_t)pd_reqs;
+    X.no_kv = (nbp == 0 || nb == 0) ? 1 : 0;
+    X.num_blocks_d = (int32_t)nb;
+    X.kv_bpt = kv_tok;
+    X.inv_link_ns = p.kv_link_bw > 0.0 ? 1e9 / p.kv_link_bw : 0.0;
+    // sub-list (w, v): the requests of prefill device w bound for decode device v
+    std::vector<int64_t> cnt((size_t)n_p * n_d, 0), share_n((size_t)n_p, 0), dec_n((size_t)n_d, 0);
+    for (int32_t r = 0; r < N; ++r) {
+      cnt[(size_t)(r % n_p) * n_d + (size_t)(r % n_d)]++;
+      share_n[(size_t)(r % n_p)]++;
+      dec_n[(size_t)(r % n_d)]++;
+    }
+    int64_t acc = pd_reqs;
+    for (int w = 0; w < n_p; ++w)
+      for (int v = 0; v < n_d; ++v) {
+        X.sub_off[w * kMaxDev + v] = (int32_t)acc;
+        acc += cnt[(size_t)w * n_d + v];
+      }
+    pd_reqs += N;
+    // the prefill devices' shares of the trace, once per (trace, n_prefill)
+    const std::pair<int, int> key(p.trace_id, n_p);
+    auto it = share_at.find(key);
+    int64_t share0;
+    if (it == share_at.end()) {
+      share0 = total_recs + extra_recs;
+      share_at[key] = share0;
+      shares.push_back(key);
+      extra_recs += N;
+    } else {
+      share0 = it->second;
+    }
+    // the decode devices' arrival records
+    const int64_t dec0 = total_recs + extra_recs;
+    extra_recs += N;
+    dec_region.push_back(dec0);
+    int64_t pos = 0;
+    for (int v = 0; v < n_d; ++v) {
+      X.dec_off[v] = (int32_t)(dec0 + pos);
+      X.pos_off[v] = (int32_t)pos;
+      pos += dec_n[(size_t)v];
+    }
+    if (total_recs + extra_recs > INT32_MAX) return TS_ERR_UNSUPPORTED;
+    const int pd_index = (int)aux.size();
+    // prefill devices: their own hardware and memory, continuous batching
+    // over prefills only; they reject what a prefill or a decode device can
+    // never hold
+    DevPoint dpp = d;
+    dpp.inv_flops_ns = 1e9 / p.p_peak_flops;
+    dpp.inv_bw_ns = 1e9 / p.p_mem_bw;
+    dpp.num_blocks = (int32_t)nbp;
+    dpp.cap_tokens = nbp * p.block_size;
+    dpp.policy = TS_POLICY_MIXED;
+    dpp.adm_reserve = 0;
+    dpp.cap_prompt = adm_cap * p.block_size - 1;  // prompt + the next token within the ratio
+    dpp.cap_po2 = nb * p.block_size;
+    dpp.may_reject = (ts.max_p > dpp.cap_tokens || ts.max_po > dpp.cap_po2 ||
+                      ts.max_p > dpp.cap_prompt) ? 1 : 0;
+    dpp.swap = 0;
+    dpp.swap_overlap = 0;
+    dpp.inv_link_ns = 0.0;
+    dpp.pd = pd_index;
+    if (!exact_and_bounded(coef, ts.max_po, p.max_batch, p.chunk_size, dpp.inv_flops_ns,
+                           dpp.inv_bw_ns, 0.0, &dpp.lg_iter))
+      return TS_ERR_UNSUPPORTED;
+    int64_t start = 0;
+    for (int w = 0; w < n_p; ++w) {
+      DevPoint u = dpp;
+      u.trace_off = (int32_t)(share0 + start);
+      u.n = (int32_t)share_n[(size_t)w];
+      u.out_index = (int32_t)(count + n_extra++);
+      u.unit = w;
+      start += share_n[(size_t)w];
+      dp.push_back(u);
+      est.push_back(work_estimate(ts, u.n, p.max_batch, p.chunk_size, p.p_peak_flops,
+                                  p.p_mem_bw, (double)weights));
+      stage.push_back(kStagePrefill);
+    }
+    // decode devices: the point's hardware and memory policy; every request
+    // that reaches them fits
+    X.dec_unit0 = (int32_t)dp.size();
+    for (int v = 0; v < n_d; ++v) {
+      DevPoint u = d;
+      u.trace_off = X.dec_off[v];
+      u.n = 0;  // set on the device by the merge kernel
+      u.out_index = (int32_t)(count + n_extra++);
+      u.pd = pd_index;
+      u.unit = v;
+      u.may_reject = 0;
+      dp.push_back(u);
+      est.push_back(work_estimate(ts, dec_n[(size_t)v], p.max_batch, p.chunk_size, p.peak_flops,
+                                  p.mem_bw, (double)weights));
+      stage.push_back(kStageDecode);
+    }
+    aux.push_back(X);
   }
+  if (count + n_extra > INT32_MAX) return TS_ERR_UNSUPPORTED;
 
-  // ---------------------------------------------------------- classes + order
+  // ---------------------------------------------------------- launches + order
   std::vector<int32_t> order;
-  order.reserve((size_t)count);
+  order.reserve(dp.size());
   ts_sweep* h = new (std::nothrow) ts_sweep();
   if (!h) return TS_ERR_OOM;
-  for (int c = 0; c < kClasses; ++c) {
+  for (int l = 0; l < kLaunches; ++l) {
     std::vector<int32_t> cls;
-    for (int i = 0; i < count; ++i)
-      if (class_of(dp[(size_t)i].max_batch) == c) cls.push_back(i);
+    for (size_t u = 0; u < dp.size(); ++u)
+      if (stage[u] == l / kClasses && class_of(dp[u].max_batch) == l % kClasses)
+        cls.push_back((int32_t)u);
     std::stable_sort(cls.begin(), cls.end(),
                      [&](int32_t a, int32_t b) { return est[(size_t)a] > est[(size_t)b]; });
-    h->class_off[c] = (int)order.size();
-    h->class_n[c] = (int)cls.size();
+    h->class_off[l] = (int)order.size();
+    h->class_n[l] = (int)cls.size();
     order.insert(order.end(), cls.begin(), cls.end());
   }
   h->n_points = count;
+  h->n_pd = (int32_t)aux.size();
   h->max_n = (int32_t)std::max<int64_t>(max_n, 1);
   h->flags = flags;
   h->iter_cap = iter_cap;
@@ -408,24 +598,22 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
   e = hipGetDeviceProperties(&prop, h->device);
   if (e != hipSuccess) { release(h); return device_error(e, "hipGetDeviceProperties"); }
   const int n_cu = prop.multiProcessorCount;
-  for (int c = 0; c < kClasses; ++c) {
-    if (h->class_n[c] == 0) continue;
+  for (int l = 0; l < kLaunches; ++l) {
+    if (h->class_n[l] == 0) continue;
     int per_cu = 0;
-    const void* fn = c == 0 ? (const void*)sim_kernel<1>
-                     : c == 1 ? (const void*)sim_kernel<2> : (const void*)sim_kernel<4>;
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, 64, 0);
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, sim_kernel_fn(l), 64, 0);
     if (e != hipSuccess) { release(h); return device_error(e, "occupancy query"); }
     per_cu = std::max(per_cu, 1);
-    h->grid[c] = std::min(h->class_n[c], n_cu * per_cu);
+    h->grid[l] = std::min(h->class_n[l], n_cu * per_cu);
     // per-workgroup request-time table: max_n entries; keep it under 1 GiB
     const int64_t cap = std::max<int64_t>(1, ((int64_t)1 << 30) /
                                                  ((int64_t)std::max<int64_t>(max_n, 1) *
                                                   (int64_t)sizeof(ReqTimes)));
-    h->grid[c] = (int)std::min<int64_t>(h->grid[c], cap);
+    h->grid[l] = (int)std::min<int64_t>(h->grid[l], cap);
   }
   h->stats_grid = std::max(1, std::min(count, n_cu * 8));
 
-  std::vector<TraceRec> recs((size_t)std::max<int64_t>(total_recs, 1));
+  std::vector<TraceRec> recs((size_t)std::max<int64_t>(total_recs + extra_recs, 1));
   for (int k = 0; k < n_traces; ++k) {
     const ts_trace& tr = traces[k];
     for (int i = 0; i < tr.n; ++i) {
@@ -435,20 +623,38 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
       r.output = tr.output_len[i];
     }
   }
+  for (const auto& key : shares) {  // share w: requests w, w + n_p, ... in order
+    const ts_trace& tr = traces[key.first];
+    int64_t at = share_at[key];
+    for (int w = 0; w < key.second; ++w)
+      for (int i = w; i < tr.n; i += key.second) {
+        TraceRec& r = recs[(size_t)at++];
+        r.arrival_ns = tr.arrival_ns[i];
+        r.prompt = tr.prompt_len[i];
+        r.output = tr.output_len[i];
+      }
+  }
   const size_t per_point = (size_t)h->max_n;
+  const size_t n_res = (size_t)(count + n_extra);
   hipError_t ae = hipSuccess;
   if (ae == hipSuccess) ae = dev_alloc(&h->d_recs, recs.size());
   if (ae == hipSuccess) ae = dev_alloc(&h->d_points, dp.size());
   if (ae == hipSuccess) ae = dev_alloc(&h->d_order, order.size());
-  if (ae == hipSuccess) ae = dev_alloc(&h->d_counter, (size_t)kClasses);
-  const int max_grid = std::max(1, *std::max_element(h->grid, h->grid + kClasses));
+  if (ae == hipSuccess) ae = dev_alloc(&h->d_counter, (size_t)kLaunches);
+  const int max_grid = std::max(1, *std::max_element(h->grid, h->grid + kLaunches));
   if (ae == hipSuccess) ae = dev_alloc(&h->d_queue, (size_t)max_grid * kQueueCap);
   if (ae == hipSuccess) ae = dev_alloc(&h->d_times, (size_t)max_grid * per_point);
-  if (ae == hipSuccess) ae = dev_alloc(&h->d_res, (size_t)count);
+  if (ae == hipSuccess) ae = dev_alloc(&h->d_res, n_res);
   if (ae == hipSuccess) ae = dev_alloc(&h->d_e2e, (size_t)count * per_point);
   if (ae == hipSuccess) ae = dev_alloc(&h->d_ttft, (size_t)count * per_point);
   if (ae == hipSuccess && (flags & TS_F_PER_REQUEST))
     ae = dev_alloc(&h->d_req, (size_t)count * per_point);
+  if (ae == hipSuccess) ae = dev_alloc(&h->d_pd, aux.size());
+  if (ae == hipSuccess) ae = dev_alloc(&h->d_s1_admit, (size_t)pd_reqs);
+  if (ae == hipSuccess) ae = dev_alloc(&h->d_s1_first, (size_t)pd_reqs);
+  if (ae == hipSuccess) ae = dev_alloc(&h->d_sub_a2, (size_t)pd_reqs);
+  if (ae == hipSuccess) ae = dev_alloc(&h->d_sub_gid, (size_t)pd_reqs);
+  if (ae == hipSuccess) ae = dev_alloc(&h->d_gids, recs.size());
   if (ae != hipSuccess) {
     const int rc = ae == hipErrorOutOfMemory ? TS_ERR_OOM : device_error(ae, "hipMalloc");
     if (rc == TS_ERR_OOM) snprintf(g_err, sizeof g_err, "device allocation failed");
@@ -461,8 +667,10 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
   if (e == hipSuccess && !order.empty())
     e = hipMemcpy(h->d_order, order.data(), order.size() * sizeof(int32_t),
                   hipMemcpyHostToDevice);
+  if (e == hipSuccess && !aux.empty())
+    e = hipMemcpy(h->d_pd, aux.data(), aux.size() * sizeof(PdAux), hipMemcpyHostToDevice);
   if (e != hipSuccess) { release(h); return device_error(e, "upload"); }
-  for (int c = 0; c < kClasses && e == hipSuccess; ++c) {
+  for (int c = 0; c < kLaunches && e == hipSuccess; ++c) {
     e = hipEventCreate(&h->ev_k0[c]);
     if (e == hipSuccess) e = hipEventCreate(&h->ev_k1[c]);
   }
@@ -479,43 +687,71 @@ int ts_sweep_run(ts_sweep* h, void* hip_stream) {
   hipStream_t s = (hipStream_t)hip_stream;
   hipError_t e = hipEventRecord(h->ev_t0, s);
   if (e != hipSuccess) return device_error(e, "event record");
-  reset_counters_kernel<<<1, 64, 0, s>>>(h->d_counter, kClasses);
+  reset_counters_kernel<<<1, 64, 0, s>>>(h->d_counter, kLaunches);
   if (h->d_req) {
     const size_t n = (size_t)h->n_points * (size_t)h->max_n;
     const int blocks = (int)std::min<size_t>((n + 255) / 256, 65536);
     fill_pending_kernel<<<std::max(blocks, 1), 256, 0, s>>>(h->d_req, n);
   }
-  for (int c = 0; c < kClasses; ++c) {
-    if (h->class_n[c] == 0) continue;
-    SimArgs a;
-    a.recs = h->d_recs;
-    a.points = h->d_points;
-    a.order = h->d_order + h->class_off[c];
-    a.n_order = h->class_n[c];
-    a.max_n = h->max_n;
-    a.counter = h->d_counter + c;
-    a.queue = h->d_queue;
-    a.times = h->d_times;
-    a.res = h->d_res;
-    a.req = h->d_req;
-    a.e2e = h->d_e2e;
-    a.ttft = h->d_ttft;
-    a.iter_cap = h->iter_cap;
-    a.slo_ttft_ns = h->slo_ttft;
-    a.slo_tpot_ns = h->slo_tpot;
-    a.time_limit_ticks = (uint64_t)h->time_limit_ms * 100000ull;  // 100 MHz clock
-    a.n_layers = h->coef.n_layers;
-    a.lc = h->lc;
-    hipStream_t ks = s;
-    e = hipEventRecord(h->ev_k0[c], ks);
+  SimArgs a;
+  a.recs = h->d_recs;
+  a.points = h->d_points;
+  a.max_n = h->max_n;
+  a.queue = h->d_queue;
+  a.times = h->d_times;
+  a.res = h->d_res;
+  a.req = h->d_req;
+  a.e2e = h->d_e2e;
+  a.ttft = h->d_ttft;
+  a.iter_cap = h->iter_cap;
+  a.slo_ttft_ns = h->slo_ttft;
+  a.slo_tpot_ns = h->slo_tpot;
+  a.time_limit_ticks = (uint64_t)h->time_limit_ms * 100000ull;  // 100 MHz clock
+  a.n_layers = h->coef.n_layers;
+  a.lc = h->lc;
+  a.pd = h->d_pd;
+  a.s1_admit = h->d_s1_admit;
+  a.s1_first = h->d_s1_first;
+  a.sub_a2 = h->d_sub_a2;
+  a.sub_gid = h->d_sub_gid;
+  a.gids = h->d_gids;
+  // one launch per (stage, class), back to back: one-worker points and
+  // prefill devices, the merge of the prefill devices' hand-overs, the
+  // decode devices, then the disaggregated points' records
+  for (int l = 0; l < kLaunches; ++l) {
+    if (l == kStageDecode * kClasses && h->n_pd > 0) {
+      pd_merge_kernel<<<std::min(h->n_pd * kMaxDev, 65536), 256, 0, s>>>(
+          h->d_pd, h->n_pd, h->d_sub_a2, h->d_sub_gid, h->d_recs, h->d_gids, h->d_points);
+      e = hipGetLastError();
+      if (e != hipSuccess) return device_error(e, "merge kernel launch");
+    }
+    if (h->class_n[l] == 0) continue;
+    a.order = h->d_order + h->class_off[l];
+    a.n_order = h->class_n[l];
+    a.counter = h->d_counter + l;
+    e = hipEventRecord(h->ev_k0[l], s);
     if (e != hipSuccess) return device_error(e, "event record");
-    if (kClassChunks[c] == 1) sim_kernel<1><<<h->grid[c], 64, 0, ks>>>(a);
-    else if (kClassChunks[c] == 2) sim_kernel<2><<<h->grid[c], 64, 0, ks>>>(a);
-    else sim_kernel<4><<<h->grid[c], 64, 0, ks>>>(a);
+    switch (l) {
+      case 0: sim_kernel<1, kStageOne><<<h->grid[l], 64, 0, s>>>(a); break;
+      case 1: sim_kernel<2, kStageOne><<<h->grid[l], 64, 0, s>>>(a); break;
+      case 2: sim_kernel<4, kStageOne><<<h->grid[l], 64, 0, s>>>(a); break;
+      case 3: sim_kernel<1, kStagePrefill><<<h->grid[l], 64, 0, s>>>(a); break;
+      case 4: sim_kernel<2, kStagePrefill><<<h->grid[l], 64, 0, s>>>(a); break;
+      case 5: sim_kernel<4, kStagePrefill><<<h->grid[l], 64, 0, s>>>(a); break;
+      case 6: sim_kernel<1, kStageDecode><<<h->grid[l], 64, 0, s>>>(a); break;
+      case 7: sim_kernel<2, kStageDecode><<<h->grid[l], 64, 0, s>>>(a); break;
+      default: sim_kernel<4, kStageDecode><<<h->grid[l], 64, 0, s>>>(a); break;
+    }
     e = hipGetLastError();
     if (e != hipSuccess) return device_error(e, "sim kernel launch");
-    e = hipEventRecord(h->ev_k1[c], ks);
+    e = hipEventRecord(h->ev_k1[l], s);
     if (e != hipSuccess) return device_error(e, "event record");
+  }
+  if (h->n_pd > 0) {
+    pd_combine_kernel<<<std::min(h->n_pd, 65536), 256, 0, s>>>(
+        h->d_pd, h->n_pd, h->d_res, h->d_recs, h->d_e2e, h->d_ttft, h->max_n);
+    e = hipGetLastError();
+    if (e != hipSuccess) return device_error(e, "combine kernel launch");
   }
   e = hipEventRecord(h->ev_t1, s);
   if (e != hipSuccess) return device_error(e, "event record");
@@ -573,7 +809,7 @@ int ts_sweep_kernel_timing(ts_sweep* h, float* ms, int32_t* n_points) {
   if (!h || !ms || !n_points) return TS_ERR_ARG;
   if (!h->ran) return TS_ERR_STATE;
   hipError_t e = hipEventSynchronize(h->ev_t2);
-  for (int c = 0; c < kClasses && e == hipSuccess; ++c) {
+  for (int c = 0; c < kLaunches && e == hipSuccess; ++c) {
     ms[c] = 0.0f;
     n_points[c] = h->class_n[c];
     if (h->class_n[c] > 0) e = hipEventElapsedTime(&ms[c], h->ev_k0[c], h->ev_k1[c]);

@@ -260,6 +260,7 @@ struct SlotLds {
   unsigned long long sum_ttft, sum_e2e, sum_tpot, digest;
   long long max_e2e, last_fin;
   unsigned int slo_ok, slo_tpot_ok;
+  unsigned int sub_cnt[kMaxDev];  // prefill device: requests handed to each decode device
   union {
     StageSlot stage[64];
     int64_t scratch[NCH * 64];
@@ -285,7 +286,11 @@ __device__ __forceinline__ void store_chunk(SlotLds<NCH>& L, Hot& h0, int j, int
 }
 
 // ------------------------------------------------------------ one point
-template <int NCH>
+// MODE: kStageOne (a one-worker design point), kStagePrefill (a prefill
+// device of a disaggregated point: requests leave when their prefill
+// completes and their KV crosses the device's link) or kStageDecode (a
+// decode device: requests arrive with their prompt's KV and first token).
+template <int NCH, int MODE>
 __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
                                                SlotLds<NCH>& L, QEntry* Q, ReqTimes* RT,
                                                const int lane, const LaneRoof& roofc) {
@@ -297,20 +302,48 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
   const int policy = P.policy, adm_reserve = P.adm_reserve;
   const bool pff = policy == TS_POLICY_PREFILL_FIRST;
   const bool swap = P.swap != 0;  // preemption by swap instead of recompute
-  // a request that could never fit, alone or within the admission ratio
+  // a request that could never fit, alone or within the admission ratio (on
+  // a prefill device: its prompt here, or the whole request on a decode device)
   auto rejected = [&](int32_t pr, int32_t ou) {
-    return (int64_t)pr + (int64_t)ou > cap_tok || (int64_t)pr > cap_prompt;
+    if constexpr (MODE == kStagePrefill)
+      return (int64_t)pr > cap_tok || (int64_t)pr + (int64_t)ou > P.cap_po2 ||
+             (int64_t)pr > cap_prompt;
+    else
+      return (int64_t)pr + (int64_t)ou > cap_tok || (int64_t)pr > cap_prompt;
+  };
+  // the disaggregated point a device belongs to
+  PdAux* X = nullptr;
+  int n_pd = 1, nd_pd = 1, req_base = 0, orig_off = 0, pos_off = 0;
+  int64_t kv_bpt = 0, link_free = 0;
+  double inv_kv_link = 0.0;
+  if constexpr (MODE != kStageOne) {
+    X = A.pd + P.pd;
+    n_pd = X->n_p;
+    nd_pd = X->n_d;
+    req_base = X->req_base;
+    orig_off = X->trace_off;
+    kv_bpt = X->kv_bpt;
+    inv_kv_link = X->inv_link_ns;
+    if constexpr (MODE == kStageDecode) pos_off = X->pos_off[P.unit];
+  }
+  // a request's index in the point's trace from its index in this unit's trace
+  auto gid_of = [&](int local) -> int {
+    if constexpr (MODE == kStagePrefill) return P.unit + local * n_pd;
+    else if constexpr (MODE == kStageDecode) return A.gids[P.trace_off + local];
+    else return local;
   };
   const double iF = P.inv_flops_ns, iB = P.inv_bw_ns;
   const int oi = P.out_index;
-  ts_req_result* RR = A.req ? A.req + (size_t)oi * (size_t)A.max_n : nullptr;
-  int64_t* E2E = A.e2e + (size_t)oi * (size_t)A.max_n;
-  int64_t* TTFT = A.ttft + (size_t)oi * (size_t)A.max_n;
+  const int orow = P.out_point;  // the design point's row
+  ts_req_result* RR = A.req ? A.req + (size_t)orow * (size_t)A.max_n : nullptr;
+  int64_t* E2E = A.e2e + (size_t)orow * (size_t)A.max_n + pos_off;
+  int64_t* TTFT = A.ttft + (size_t)orow * (size_t)A.max_n + pos_off;
 
   // statistics of finished / rejected requests: LDS accumulators, cleared
   // by every lane storing the same zeros (no lane-dependent branch)
   L.sum_ttft = 0; L.sum_e2e = 0; L.sum_tpot = 0; L.digest = 0;
   L.max_e2e = -1; L.last_fin = -1; L.slo_ok = 0; L.slo_tpot_ok = 0;
+  L.sub_cnt[lane & (kMaxDev - 1)] = 0;
   __syncthreads();
   int n_rej = 0;
 
@@ -324,12 +357,13 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
         rj = rejected(r.prompt, r.output);
       }
       if (rj) {
-        atomicAdd(&L.digest, (unsigned long long)record_hash(i, -1, -1, -1, 0, 0, TS_REQ_REJECTED));
+        const int g = gid_of(i);
+        atomicAdd(&L.digest, (unsigned long long)record_hash(g, -1, -1, -1, 0, 0, TS_REQ_REJECTED));
         if (RR) {
           ts_req_result o;
           o.admit_ns = -1; o.first_token_ns = -1; o.finish_ns = -1; o.max_gap_ns = 0;
           o.n_preempt = 0; o.status = TS_REQ_REJECTED;
-          RR[i] = o;
+          RR[g] = o;
         }
       }
       n_rej += popc(ballot(rj));
@@ -397,9 +431,12 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
   auto record_done = [&](bool fin, int s, int64_t t_end, int64_t gap, int pos) {
     if (fin) {
       const int id = L.id[s];
+      const int g = gid_of(id);
       const int npr = L.npre[s];
       const ReqTimes rt = RT[id];
-      const int64_t arr = rec[id].arrival_ns;
+      // latencies count from the arrival at the point (a decode device's
+      // trace holds the arrivals of the KV instead)
+      const int64_t arr = MODE == kStageDecode ? A.recs[orig_off + g].arrival_ns : rec[id].arrival_ns;
       const int64_t tt = rt.first - arr;
       const int64_t ee = t_end - arr;
       atomicAdd(&L.sum_ttft, (unsigned long long)tt);
@@ -409,13 +446,13 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       atomicMax(&L.last_fin, (long long)t_end);
       if (tt <= A.slo_ttft_ns && gap <= A.slo_tpot_ns) atomicAdd(&L.slo_ok, 1u);
       if (gap <= A.slo_tpot_ns) atomicAdd(&L.slo_tpot_ok, 1u);
-      atomicAdd(&L.digest, (unsigned long long)record_hash(id, rt.admit, rt.first, t_end, gap,
+      atomicAdd(&L.digest, (unsigned long long)record_hash(g, rt.admit, rt.first, t_end, gap,
                                                            npr, TS_REQ_DONE));
       if (RR) {
         ts_req_result o;
         o.admit_ns = rt.admit; o.first_token_ns = rt.first; o.finish_ns = t_end;
         o.max_gap_ns = gap; o.n_preempt = npr; o.status = TS_REQ_DONE;
-        RR[id] = o;
+        RR[g] = o;
       }
       E2E[pos] = ee;
       TTFT[pos] = tt;
@@ -498,6 +535,34 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
     nrun = nsurv;
   };
 
+  // A prefill device hands the requests of chunk j whose prefill completed
+  // at t_end (lanes in pm) to their decode devices, in slot order: each KV
+  // transfer starts when the device's link is free and takes
+  // ceil(prompt * KV bytes per token * ns per byte).
+  auto hand_over = [&](uint64_t pm, int j, int tgt_lane, int64_t t_end) {
+    while (pm != 0) {
+      const int l = (int)__builtin_ctzll(pm);
+      pm &= pm - 1;
+      const int id_l = __builtin_amdgcn_readfirstlane(L.id[j * 64 + l]);
+      const int p_l = rdl(tgt_lane, l);
+      const int g = P.unit + id_l * n_pd;
+      const int64_t x =
+          inv_kv_link == 0.0 ? 0 : (int64_t)ceil((double)((int64_t)p_l * kv_bpt) * inv_kv_link);
+      link_free = (t_end > link_free ? t_end : link_free) + x;
+      const int v = g % nd_pd;
+      const int c = __builtin_amdgcn_readfirstlane((int)L.sub_cnt[v]);
+      L.sub_cnt[v] = (unsigned int)(c + 1);  // every lane stores the same value
+      const int pos = X->sub_off[P.unit * kMaxDev + v] + c;
+      const int64_t adm = RT[id_l].admit;
+      if (lane == 0) {
+        A.sub_a2[pos] = link_free;
+        A.sub_gid[pos] = g;
+        A.s1_first[req_base + g] = t_end;
+        A.s1_admit[req_base + g] = adm;
+      }
+    }
+  };
+
   const uint64_t clock0 = A.time_limit_ticks ? __builtin_amdgcn_s_memrealtime() : 0;
   while (status == TS_POINT_OK) {
     // ---- 0. steady stretch.  As long as no request is admitted or
@@ -540,9 +605,10 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
           const uint64_t dm = ballot(dec);
           nD += popc(dm);
           if (ballot(dec && ((h.fl & FL_STALE) != 0 || h.rem == 1)) != 0) go = false;
-          if (swap) {
+          if (swap || MODE == kStageDecode) {
             // a request swapped in behind a prefill can finish its prefill
-            // later than a newer one: the decodes may not form a slot prefix
+            // later than a newer one, and a decode device admits decodes
+            // behind re-prefills: the decodes may not form a slot prefix
             if ((dm & (dm + 1)) != 0 || (short_chunk && dm != 0)) go = false;
             short_chunk = short_chunk || dm != ~0ull;
           }
@@ -761,7 +827,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
             // finishing here, is handled in place; everything else runs on
             // the general path.
             if (stop >= stop_hard || npf != 1 || dG == fin_at ||
-                (fl_p & (FL_FIRST | FL_STALE)) != 0)
+                (fl_p & (FL_FIRST | FL_STALE)) != 0 || MODE == kStagePrefill)
               break;
             const int CD = cd_seg + nDa * (dG - seg0);  // decode keys at this iteration
             close_segment();
@@ -1117,6 +1183,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
     // preemption; static batching only into an empty running set;
     // prefill-first only in a prefill iteration).  A first admission leaves
     // the admission-ratio reserve free.
+    int n_darr = 0;  // decode device: arrivals admitted, decoding in this iteration
     if (!preempted && (!pff || pf_iter) && (policy != TS_POLICY_STATIC || nrun == 0)) {
       int guard = M + N / 64 + 4;  // each pass admits or advances a window
       while (nrun < M && (unlimited || R > 0 || (swap && npre > 0)) && (npre > 0 || nwait > 0) &&
@@ -1144,8 +1211,12 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
           if (valid) {
             const TraceRec r = rec[idx];
             c_tgt = r.prompt;
-            c_rem = r.output;
+            c_rem = MODE == kStagePrefill ? 1 : r.output;  // a prefill device runs no decode
             if (P.may_reject && rejected(r.prompt, r.output)) valid = false;
+          }
+          if constexpr (MODE == kStageDecode) {  // arrives with its prompt's KV, first token out
+            c_ctx = c_tgt;
+            c_fl = FL_FIRST | FL_STALE;
           }
         }
         const uint64_t vm = ballot(valid);
@@ -1160,10 +1231,13 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
           continue;
         }
         const int rank = rank_below(vm);
+        // a decode device's arrival decodes at once: blocks for its KV and
+        // the next token, one token of budget
+        const bool darr = MODE == kStageDecode && !fromq;
         const int c_top = c_ctx > c_tgt ? c_ctx : c_tgt;  // tokens held in blocks
-        const int need = valid ? divB(c_top + B - 1) : 0;
+        const int need = valid ? divB(c_top + (darr ? 1 : 0) + B - 1) : 0;
         const int SN = scan_i32(need);
-        const int tq = valid ? c_tgt : 0;
+        const int tq = valid ? (darr ? 1 : c_tgt) : 0;
         const int ET = scan_i32(tq) - tq;
         const int slots_left = M - nrun;
         const bool adm = valid && rank < slots_left && SN <= freeb - (fromq ? 0 : adm_reserve) &&
@@ -1175,13 +1249,25 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
           break;
         }
         const int last_lane = 63 - (int)__builtin_clzll(am);
-        const int qv = swin ? 0 : (unlimited ? c_tgt : (c_tgt < R - ET ? c_tgt : R - ET));
+        const int qv =
+            (swin || darr) ? 0 : (unlimited ? c_tgt : (c_tgt < R - ET ? c_tgt : R - ET));
         const int taken = rdl(SN, last_lane);
         freeb -= taken;
         if (swin) xblk += taken;
-        if (!unlimited) R -= wsum(adm ? qv : 0);
+        if (!unlimited) R -= wsum(adm ? (darr ? 1 : qv) : 0);
         if (adm) {
-          if (!fromq) RT[c_id].admit = t;  // first admission
+          if constexpr (MODE == kStageDecode) {
+            if (!fromq) {  // its times so far come from the prefill device
+              const int g = gid_of(c_id);
+              ReqTimes rt;
+              rt.admit = A.s1_admit[req_base + g];
+              rt.first = A.s1_first[req_base + g];
+              rt.last = rt.first;
+              RT[c_id] = rt;
+            }
+          } else {
+            if (!fromq) RT[c_id].admit = t;  // first admission
+          }
           StageSlot st;
           st.id = c_id; st.tgt = c_tgt; st.rem = c_rem; st.npre = c_npre;
           st.fl = swin ? (c_fl | FL_IDLE) : c_fl;
@@ -1204,6 +1290,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
         }
         __syncthreads();
         nrun += a;
+        if (darr) n_darr += a;
         if (fromq) {
           qhead = (qhead + a) & (kQueueCap - 1);
           npre -= a;
@@ -1224,6 +1311,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
 
     // ---- 6. batch sums and the roofline iteration time (paused decodes of a
     // prefill-first iteration and requests swapped in now take no part)
+    if constexpr (MODE == kStageDecode) nD += n_darr;
     if (pf_iter) nD = 0;
     int l_cd = 0, l_tp = 0, l_cp = 0, TP = 0, CP = 0, Rc = 0;
     int64_t l_ap = 0, AP = 0;
@@ -1284,7 +1372,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       const int s = j * 64 + lane;
       const bool act = s < nrun;
       const bool dec = act && h.ctx >= h.tgt && !pf_iter && !(h.fl & FL_IDLE);
-      bool fin = false;
+      bool fin = false, pfin = false;
       if (pf_iter && act && h.ctx >= h.tgt && !(h.fl & FL_STALE)) {
         // a paused decode: its last token ended the previous iteration
         RT[L.id[s]].last = t;
@@ -1308,11 +1396,23 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
         if (h.ctx == h.tgt && !(h.fl & FL_FIRST)) {  // the full prefill emits a token
           h.fl |= FL_FIRST;
           RT[L.id[s]].first = t_end;
+          if constexpr (MODE == kStagePrefill) {  // and leaves the prefill device
+            h.rem = 0;
+            pfin = true;
+          }
         }
         h.q = 0;
       }
       h.fl &= ~FL_IDLE;
       store_chunk<NCH>(L, h0, j, lane, h);
+      if constexpr (MODE == kStagePrefill) {
+        const uint64_t pm = ballot(pfin);
+        if (pm != 0) {
+          hand_over(pm, j, h.tgt, t_end);
+          l_freed += pfin ? divB(h.ctx + h.room) : 0;  // held blocks
+          nfin += popc(pm);
+        }
+      }
       const uint64_t fm = ballot(fin);
       if (fm != 0) {
         record_done(fin, s, t_end, h.gap, base + rank_below(fm));
@@ -1330,6 +1430,10 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
   }
 
   // ---- per-point results (percentiles are filled by the statistics kernel)
+  if constexpr (MODE == kStagePrefill) {
+    const int v = lane < nd_pd ? lane : nd_pd - 1;  // lanes past n_d repeat the last store
+    X->sub_cnt[P.unit * kMaxDev + v] = (int)L.sub_cnt[v];
+  }
   __syncthreads();
   const int64_t sum_ttft = (int64_t)L.sum_ttft;
   const int64_t sum_e2e = (int64_t)L.sum_e2e;
@@ -1372,7 +1476,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
 
 // Persistent grid: each wave64 workgroup takes the next point from a ticket
 // counter until none is left.
-template <int NCH>
+template <int NCH, int MODE>
 __global__ __launch_bounds__(64, NCH == 4 ? 4 : 5) void sim_kernel(SimArgs A) {
   __shared__ SlotLds<NCH> L;
   const int lane = lane_id();
@@ -1399,13 +1503,19 @@ __global__ __launch_bounds__(64, NCH == 4 ? 4 : 5) void sim_kernel(SimArgs A) {
     const unsigned old = atomicAdd(A.counter, lane == 0 ? 1u : 0u);
     const int tk = __builtin_amdgcn_readfirstlane((int)old);
     if (tk >= A.n_order) break;
-    simulate_point<NCH>(A, A.order[tk], L, Q, RT, lane, roofc);
+    simulate_point<NCH, MODE>(A, A.order[tk], L, Q, RT, lane, roofc);
   }
 }
 
-template __global__ void sim_kernel<1>(SimArgs);
-template __global__ void sim_kernel<2>(SimArgs);
-template __global__ void sim_kernel<4>(SimArgs);
+template __global__ void sim_kernel<1, kStageOne>(SimArgs);
+template __global__ void sim_kernel<2, kStageOne>(SimArgs);
+template __global__ void sim_kernel<4, kStageOne>(SimArgs);
+template __global__ void sim_kernel<1, kStagePrefill>(SimArgs);
+template __global__ void sim_kernel<2, kStagePrefill>(SimArgs);
+template __global__ void sim_kernel<4, kStagePrefill>(SimArgs);
+template __global__ void sim_kernel<1, kStageDecode>(SimArgs);
+template __global__ void sim_kernel<2, kStageDecode>(SimArgs);
+template __global__ void sim_kernel<4, kStageDecode>(SimArgs);
 
 // ------------------------------------------------------------ statistics
 // Nearest-rank percentiles of the finished requests' latencies: k-th
@@ -1479,6 +1589,143 @@ __global__ void fill_pending_kernel(ts_req_result* r, size_t n) {
     o.admit_ns = -1; o.first_token_ns = -1; o.finish_ns = -1; o.max_gap_ns = 0;
     o.n_preempt = 0; o.status = TS_REQ_PENDING;
     r[i] = o;
+  }
+}
+
+// ------------------------------------------------------------ disaggregated points
+// Decode device v of a point receives its requests in (arrival of the KV,
+// request index) order.  Each prefill device's sub-list (w, v) is already in
+// that order (a prefill device completes prefills in admission order and its
+// link delivers them in that order), so a request's place is its index in its
+// own sub-list plus, for every other sub-list, how many entries come before
+// it there (a binary search).  One 256-thread workgroup per (point, decode
+// device); it also sets the decode device's request count.
+__global__ __launch_bounds__(256) void pd_merge_kernel(const PdAux* aux, int n_aux,
+                                                       const int64_t* sub_a2,
+                                                       const int32_t* sub_gid, TraceRec* recs,
+                                                       int32_t* gids, DevPoint* units) {
+  for (int b = blockIdx.x; b < n_aux * kMaxDev; b += gridDim.x) {
+    const PdAux& X = aux[b / kMaxDev];
+    const int v = b % kMaxDev;
+    if (v >= X.n_d) continue;
+    int total = 0;
+    for (int w = 0; w < X.n_p; ++w) {
+      const int cnt = X.sub_cnt[w * kMaxDev + v], off = X.sub_off[w * kMaxDev + v];
+      total += cnt;
+      for (int k = threadIdx.x; k < cnt; k += blockDim.x) {
+        const int64_t a = sub_a2[off + k];
+        const int g = sub_gid[off + k];
+        int rank = k;
+        for (int u = 0; u < X.n_p; ++u) {
+          if (u == w) continue;
+          const int uo = X.sub_off[u * kMaxDev + v];
+          int lo = 0, hi = X.sub_cnt[u * kMaxDev + v];
+          while (lo < hi) {  // entries of sub-list u before (a, g)
+            const int mid = (lo + hi) >> 1;
+            const int64_t am = sub_a2[uo + mid];
+            if (am < a || (am == a && sub_gid[uo + mid] < g)) lo = mid + 1;
+            else hi = mid;
+          }
+          rank += lo;
+        }
+        const TraceRec o = recs[X.trace_off + g];
+        TraceRec r;
+        r.arrival_ns = a;
+        r.prompt = o.prompt;
+        r.output = o.output;
+        recs[X.dec_off[v] + rank] = r;
+        gids[X.dec_off[v] + rank] = g;
+      }
+    }
+    if (threadIdx.x == 0) units[X.dec_unit0 + v].n = total;
+  }
+}
+
+// A disaggregated point's record from its devices' records: requests and
+// latency sums from the decode devices, rejections from the prefill devices,
+// iterations, tokens, the used-block integral (prefill devices first, then
+// decode devices, in index order) and the digest over all devices, the block
+// peak of the busiest decode device.  The decode devices' latencies are then
+// moved to the front of the point's row for the percentile pass.  One
+// 256-thread workgroup per point.
+__global__ __launch_bounds__(256) void pd_combine_kernel(const PdAux* aux, int n_aux,
+                                                         ts_point_result* res,
+                                                         const TraceRec* recs, int64_t* e2e,
+                                                         int64_t* ttft, int max_n) {
+  __shared__ int seg_n[kMaxDev];
+  for (int b = blockIdx.x; b < n_aux; b += gridDim.x) {
+    const PdAux& X = aux[b];
+    if (threadIdx.x == 0) {
+      ts_point_result o;
+      const int nu = X.n_p + X.n_d;
+      o.status = TS_POINT_OK;
+      o.n_done = 0; o.n_rejected = 0; o.num_blocks = X.num_blocks_d;
+      o.n_iters = 0; o.n_preempt = 0; o.prefill_tokens = 0; o.decode_tokens = 0;
+      o.peak_used_blocks = 0;
+      o.first_arrival_ns = X.n > 0 ? recs[X.trace_off].arrival_ns : -1;
+      o.last_finish_ns = -1;
+      o.sum_ttft_ns = 0; o.sum_e2e_ns = 0; o.max_e2e_ns = -1; o.sum_tpot_num_ns = 0;
+      o.p50_e2e_ns = o.p90_e2e_ns = o.p99_e2e_ns = -1;
+      o.p50_ttft_ns = o.p99_ttft_ns = -1;
+      o.slo_ok = 0; o.slo_tpot_ok = 0;
+      o.used_block_ns = 0.0;
+      o.digest = 0;
+      for (int u = 0; u < nu; ++u) {
+        const ts_point_result& r = res[X.res0 + u];
+        const bool dec = u >= X.n_p;
+        o.status = r.status > o.status ? r.status : o.status;
+        o.n_iters += r.n_iters;
+        o.n_preempt += r.n_preempt;
+        o.prefill_tokens += r.prefill_tokens;
+        o.decode_tokens += r.decode_tokens;
+        o.used_block_ns = o.used_block_ns + r.used_block_ns;
+        o.digest += r.digest;
+        if (dec) {
+          o.n_done += r.n_done;
+          o.peak_used_blocks = r.peak_used_blocks > o.peak_used_blocks ? r.peak_used_blocks
+                                                                        : o.peak_used_blocks;
+          o.last_finish_ns = r.last_finish_ns > o.last_finish_ns ? r.last_finish_ns
+                                                                  : o.last_finish_ns;
+          o.sum_ttft_ns += r.sum_ttft_ns;
+          o.sum_e2e_ns += r.sum_e2e_ns;
+          o.max_e2e_ns = r.max_e2e_ns > o.max_e2e_ns ? r.max_e2e_ns : o.max_e2e_ns;
+          o.sum_tpot_num_ns += r.sum_tpot_num_ns;
+          o.slo_ok += r.slo_ok;
+          o.slo_tpot_ok += r.slo_tpot_ok;
+          seg_n[u - X.n_p] = r.n_done;
+        } else {
+          o.n_rejected += r.n_rejected;
+        }
+      }
+      if (X.no_kv) o.status = TS_POINT_NO_KV;
+      res[X.point] = o;
+    }
+    __syncthreads();
+    // decode device v's latencies: from pos_off[v] to the running total;
+    // destinations never pass their sources, and a chunk is read whole
+    // before it is written
+    int64_t* ve = e2e + (size_t)X.point * (size_t)max_n;
+    int64_t* vt = ttft + (size_t)X.point * (size_t)max_n;
+    int dst = 0;
+    for (int v = 0; v < X.n_d; ++v) {
+      const int n = seg_n[v], src = X.pos_off[v];
+      for (int k0 = 0; k0 < n; k0 += 256) {
+        const int k = k0 + (int)threadIdx.x;
+        int64_t a = 0, c = 0;
+        if (k < n) {
+          a = ve[src + k];
+          c = vt[src + k];
+        }
+        __syncthreads();
+        if (k < n) {
+          ve[dst + k] = a;
+          vt[dst + k] = c;
+        }
+        __syncthreads();
+      }
+      dst += n;
+    }
+    __syncthreads();
   }
 }
 

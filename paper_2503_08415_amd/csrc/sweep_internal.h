@@ -16,7 +16,11 @@ struct __attribute__((aligned(16))) TraceRec {
   int32_t output;
 };
 
-// Per design point constants, derived on the host at create time.
+// What a simulation unit is: a one-worker design point, or one device of a
+// disaggregated point (a prefill device, or a decode device).
+enum : int { kStageOne = 0, kStagePrefill = 1, kStageDecode = 2, kStages = 3 };
+
+// Per simulation unit constants, derived on the host at create time.
 struct __attribute__((aligned(16))) DevPoint {
   double inv_flops_ns;  // 1e9 / peak FLOP/s
   double inv_bw_ns;     // 1e9 / bytes per second
@@ -37,6 +41,36 @@ struct __attribute__((aligned(16))) DevPoint {
   int64_t block_bytes;  // KV bytes of one block
   int32_t swap;         // 1: preemption by swap, 0: by recompute
   int32_t swap_overlap; // 1: transfers overlap the iteration's compute
+  int64_t cap_po2;      // prefill device: a prompt + output above this never fits a decode device
+  int32_t out_point;    // the design point's row (latencies, per-request records)
+  int32_t pd;           // disaggregated point's PdAux index, -1 for a one-worker point
+  int32_t unit;         // prefill or decode device index within its point
+  int32_t pad;
+};
+
+constexpr int kMaxDev = TS_MAX_DEVICES;
+
+// One disaggregated design point: where its devices' data lives.  Prefill
+// device w writes the requests it hands to decode device v, in completion
+// order, to the sub-list (w, v) and its length to sub_cnt; the merge kernel
+// orders each decode device's arrivals from those sub-lists.
+struct __attribute__((aligned(16))) PdAux {
+  int32_t n_p, n_d;       // prefill and decode devices
+  int32_t point;          // the design point's row
+  int32_t res0;           // result record of prefill device 0; decode device v at res0 + n_p + v
+  int32_t dec_unit0;      // DevPoint of decode device 0 (its request count is set on the device)
+  int32_t trace_off;      // the point's trace (original arrivals, prompt and output lengths)
+  int32_t n;              // requests in the trace
+  int32_t req_base;       // base of the point's per-request entries in the stage buffers
+  int32_t no_kv;          // a prefill or decode device has no KV block
+  int32_t num_blocks_d;   // a decode device's blocks
+  int64_t kv_bpt;         // KV bytes per token
+  double inv_link_ns;     // ns per byte of a prefill device's KV link; 0 = instant
+  int32_t pad2;
+  int32_t sub_off[kMaxDev * kMaxDev];  // (w, v) -> first entry of the sub-list
+  int32_t sub_cnt[kMaxDev * kMaxDev];  // (w, v) -> entries written
+  int32_t dec_off[kMaxDev];            // decode device v's trace records
+  int32_t pos_off[kMaxDev];            // decode device v's latency entries within the row
 };
 
 // Integer coefficients of the per-operator roofline (exact below 2^53):
@@ -78,7 +112,7 @@ struct LaneCoef {
 constexpr int kQueueCap = 256;  // >= max_batch: queue + running never exceed max_batch
 
 struct SimArgs {
-  const TraceRec* recs;
+  TraceRec* recs;              // traces, prefill devices' shares, decode devices' arrivals
   const DevPoint* points;
   const int32_t* order;        // points of this launch, longest expected first
   int32_t n_order;
@@ -96,6 +130,13 @@ struct SimArgs {
   uint64_t time_limit_ticks;   // 0 = none; 100 MHz device clock ticks per point
   double n_layers;
   LaneCoef lc;
+  // disaggregated points
+  PdAux* pd;
+  int64_t* s1_admit;           // per request: admission on its prefill device
+  int64_t* s1_first;           // per request: first token
+  int64_t* sub_a2;             // sub-lists: when the KV reaches the decode device
+  int32_t* sub_gid;            // sub-lists: request index
+  const int32_t* gids;         // per trace record: request index (decode devices' arrivals)
 };
 
 }  // namespace tsw

@@ -42,7 +42,15 @@ class Point(C.Structure):
                 ("block_size", C.c_int32), ("max_batch", C.c_int32),
                 ("chunk_size", C.c_int32), ("trace_id", C.c_int32), ("policy", C.c_int32),
                 ("admit_mem_permille", C.c_int32), ("swap_overlap", C.c_int32),
-                ("swap_bw", C.c_double)]
+                ("swap_bw", C.c_double), ("n_prefill", C.c_int32), ("n_decode", C.c_int32),
+                ("p_peak_flops", C.c_double), ("p_mem_bw", C.c_double),
+                ("p_capacity_bytes", C.c_int64), ("kv_link_bw", C.c_double)]
+
+
+# point fields a points dict may leave out, and their values then
+POINT_DEFAULTS = {"policy": 0, "admit_mem_permille": 0, "swap_overlap": 0, "swap_bw": 0.0,
+                  "n_prefill": 0, "n_decode": 0, "p_peak_flops": 0.0, "p_mem_bw": 0.0,
+                  "p_capacity_bytes": 0, "kv_link_bw": 0.0}
 
 
 class Options(C.Structure):
@@ -67,7 +75,9 @@ POINT_DTYPE = np.dtype([
 # every entry point declared in include/ts_sweep.h
 EXPORTS = ("ts_sweep_create", "ts_sweep_run", "ts_sweep_results", "ts_sweep_shape",
            "ts_sweep_timing", "ts_sweep_kernel_timing", "ts_sweep_destroy", "ts_status_str")
-N_SIM_KERNELS = 3  # register-chunk classes: max_batch <= 64, <= 128, <= 256
+# simulation launches, 3 * stage + class: stages one-worker points, prefill
+# devices, decode devices; classes max_batch <= 64, <= 128, <= 256
+N_SIM_KERNELS = 9
 
 _lib = None
 
@@ -122,19 +132,14 @@ def model_struct(m: dict) -> Model:
 def points_array(points: dict):
     n = len(points["peak_flops"])
     arr = (Point * max(n, 1))()
-    pol = points.get("policy")
-    adm = points.get("admit_mem_permille")
-    sov = points.get("swap_overlap")
-    sbw = points.get("swap_bw")
+    cols = []
+    for name, ty in Point._fields_:
+        conv = float if ty is C.c_double else int
+        col = points.get(name)
+        cols.append((conv, col, POINT_DEFAULTS.get(name)))
     for i in range(n):
-        arr[i] = Point(float(points["peak_flops"][i]), float(points["mem_bw"][i]),
-                       int(points["capacity_bytes"][i]), int(points["mem_util_permille"][i]),
-                       int(points["block_size"][i]), int(points["max_batch"][i]),
-                       int(points["chunk_size"][i]), int(points["trace_id"][i]),
-                       int(pol[i]) if pol is not None else 0,
-                       int(adm[i]) if adm is not None else 0,
-                       int(sov[i]) if sov is not None else 0,
-                       float(sbw[i]) if sbw is not None else 0.0)
+        arr[i] = Point(*[conv(col[i]) if col is not None else conv(dflt)
+                         for conv, col, dflt in cols])
     return arr, n
 
 

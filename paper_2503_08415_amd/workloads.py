@@ -71,7 +71,8 @@ C4_CAPS = tuple(int(round(24e9 + i * 136e9 / 31)) for i in range(32))
 
 POINT_FIELDS = ("peak_flops", "mem_bw", "capacity_bytes", "mem_util_permille",
                 "block_size", "max_batch", "chunk_size", "trace_id", "policy",
-                "admit_mem_permille", "swap_overlap", "swap_bw")
+                "admit_mem_permille", "swap_overlap", "swap_bw", "n_prefill", "n_decode",
+                "p_peak_flops", "p_mem_bw", "p_capacity_bytes", "kv_link_bw")
 
 _NS = 1e9
 
@@ -171,6 +172,12 @@ def _points(rows):
         "admit_mem_permille": np.asarray(pts["admit_mem_permille"], dtype=np.int32),
         "swap_overlap": np.asarray(pts["swap_overlap"], dtype=np.int32),
         "swap_bw": np.asarray(pts["swap_bw"], dtype=np.float64),
+        "n_prefill": np.asarray(pts["n_prefill"], dtype=np.int32),
+        "n_decode": np.asarray(pts["n_decode"], dtype=np.int32),
+        "p_peak_flops": np.asarray(pts["p_peak_flops"], dtype=np.float64),
+        "p_mem_bw": np.asarray(pts["p_mem_bw"], dtype=np.float64),
+        "p_capacity_bytes": np.asarray(pts["p_capacity_bytes"], dtype=np.int64),
+        "kv_link_bw": np.asarray(pts["kv_link_bw"], dtype=np.float64),
     }
 
 
@@ -310,6 +317,36 @@ def _c7(n_req):
     return "llama2-7b", traces, rows
 
 
+def _c8(n_req):
+    """Disaggregated prefill and decode on an 8-device node (Sec. V: the best
+    prefill-to-decode device ratio over input and output lengths, and the
+    prefill device's compute, capacity and bandwidth): 4 length mixes
+    (lognormal prompts around 128 or 1024 tokens x outputs around 128 or
+    512) x 4 arrival rates x P/D splits {1/7, 2/6, 3/5, 4/4} x prefill
+    hardware {A100-like, 2x FLOP/s, 1/4 capacity, 1/4 bandwidth}, 7B model,
+    decode devices A100-like, KV links of 25 GB/s."""
+    mixes = [(4.85, 4.85), (4.85, 6.2), (6.9, 4.85), (6.9, 6.2)]  # log-means: ~128, ~512, ~1024
+    rates = (5.0, 10.0, 20.0, 40.0)
+    traces = []
+    for m, (lp, lo) in enumerate(mixes):
+        for r, rate in enumerate(rates):
+            spec = {"arrival": ("poisson", rate), "prompt": ("lognormal", lp, 0.6, 4, 8192),
+                    "output": ("lognormal", lo, 0.6, 1, 4096)}
+            traces.append(make_trace(spec, n_req, _seed(8, m, r)))
+    prefill_hw = [(312e12, 2e12, 80_000_000_000), (624e12, 2e12, 80_000_000_000),
+                  (312e12, 2e12, 20_000_000_000), (312e12, 0.5e12, 80_000_000_000)]
+    rows = []
+    for k in range(len(traces)):
+        for n_p in (1, 2, 3, 4):
+            for pf, pb, pc in prefill_hw:
+                rows.append(dict(peak_flops=312e12, mem_bw=2e12, capacity_bytes=80_000_000_000,
+                                 mem_util_permille=900, block_size=16, max_batch=64,
+                                 chunk_size=0, trace_id=k, n_prefill=n_p, n_decode=8 - n_p,
+                                 p_peak_flops=pf, p_mem_bw=pb, p_capacity_bytes=pc,
+                                 kv_link_bw=25e9))
+    return "llama2-7b", traces, rows
+
+
 # name -> (builder, default requests per trace, description)
 CONFIGS = {
     "c1": (_c1, 64, "1 point x 64 requests, 7B MHA, 312 TF / 2 TB/s / 80 GB, "
@@ -326,6 +363,8 @@ CONFIGS = {
                       "static} x admission ratio {off, 60%, 80%, 95%} x {24, 40} GB"),
     "c7": (_c7, 2000, "320 points x 2000 requests, 7B MHA, 16 rates x {recompute, swap "
                       "16/32/64 GB/s, swap 64 GB/s overlapped} x {20, 24} GB x {no chunk, 512}"),
+    "c8": (_c8, 2000, "256 disaggregated points x 2000 requests, 7B MHA, 4 length mixes x "
+                      "4 rates x P/D {1/7, 2/6, 3/5, 4/4} x 4 prefill devices, 25 GB/s KV links"),
 }
 
 

@@ -39,13 +39,13 @@ def test_exports_every_declared_symbol(L):
 def test_struct_layouts():
     assert C.sizeof(S.Model) == 40
     assert C.sizeof(S.Trace) == 32
-    assert C.sizeof(S.Point) == 64
+    assert C.sizeof(S.Point) == 104
     assert C.sizeof(S.Options) == 48
     assert S.REQ_DTYPE.itemsize == 40
     assert S.POINT_DTYPE.itemsize == 176
     src = open(HEADER).read()
     assert "Per-point result: 176 bytes" in src and "40 bytes" in src
-    assert "#define TS_ABI_VERSION 3" in src
+    assert "#define TS_ABI_VERSION 4" in src
 
 
 def test_header_layout_matches_binding(tmp_path):
@@ -111,7 +111,10 @@ def _base():
 def _mod_points(pts, **kw):
     q = {k: v.copy() for k, v in pts.items()}
     for k, v in kw.items():
-        q[k][:] = v
+        if k in q:
+            q[k][:] = v
+        else:
+            q[k] = np.full(len(q["peak_flops"]), v)
     return q
 
 
@@ -134,6 +137,15 @@ def test_invalid_arguments_fail_before_device(L):
     for kw in (dict(max_batch=257), dict(policy=3), dict(policy=-1)):
         rc, h = _create(L, m, traces, _mod_points(pts, **kw))
         assert rc == S.TS_ERR_UNSUPPORTED, kw
+    # disaggregated points
+    pd = dict(n_prefill=1, n_decode=1, p_peak_flops=1e12, p_mem_bw=1e12,
+              p_capacity_bytes=80_000_000_000, kv_link_bw=1e9)
+    for kw in (dict(n_decode=0), dict(n_prefill=0), dict(n_prefill=17), dict(n_decode=17),
+               dict(n_prefill=-1), dict(policy=S.POLICY_STATIC), dict(p_peak_flops=0.0),
+               dict(p_mem_bw=float("nan")), dict(p_capacity_bytes=0), dict(kv_link_bw=-1.0),
+               dict(kv_link_bw=float("inf"))):
+        rc, h = _create(L, m, traces, _mod_points(pts, **dict(pd, **kw)))
+        assert rc == S.TS_ERR_ARG, kw
     unsorted = dict(traces[0])
     unsorted["arrival_ns"] = traces[0]["arrival_ns"][::-1].copy()
     rc, _ = _create(L, m, [unsorted], pts)

@@ -76,12 +76,13 @@ def cap_from(oracle_out):
     return int(oracle_out["n_iters"].max()) * 2 + 1000
 
 
+FLOAT_FIELDS = ("peak_flops", "mem_bw", "swap_bw", "p_peak_flops", "p_mem_bw", "kv_link_bw")
+
+
 def hand_sweep():
     with open(os.path.join(GOLD, "hand_traces.json")) as f:
         g = json.load(f)
     traces, rows = [], []
-    # disaggregated cases join once the kernels run them
-    g["cases"] = [c for c in g["cases"] if c.get("n_prefill", 0) == 0]
     for k, c in enumerate(g["cases"]):
         r = c["requests"]
         traces.append({"arrival_ns": np.array([x[0] for x in r], np.int64),
@@ -93,10 +94,15 @@ def hand_sweep():
                          block_size=b, max_batch=c["max_batch"], chunk_size=c["chunk_size"],
                          trace_id=k, policy=c.get("policy", 0),
                          admit_mem_permille=c.get("admit_mem_permille", 0),
-                         swap_bw=c.get("swap_bw", 0.0), swap_overlap=c.get("swap_overlap", 0)))
+                         swap_bw=c.get("swap_bw", 0.0), swap_overlap=c.get("swap_overlap", 0),
+                         n_prefill=c.get("n_prefill", 0), n_decode=c.get("n_decode", 0),
+                         p_peak_flops=1e300, p_mem_bw=1e300,
+                         p_capacity_bytes=max(1, c.get("prefill_blocks", 0) * b * 16),
+                         kv_link_bw=c.get("kv_link_bw", 0.0)))
     pts = {k: np.array([r[k] for r in rows]) for k in rows[0]}
-    pts = {k: (v.astype(np.float64) if k in ("peak_flops", "mem_bw", "swap_bw") else
-               v.astype(np.int64) if k == "capacity_bytes" else v.astype(np.int32))
+    pts = {k: (v.astype(np.float64) if k in FLOAT_FIELDS else
+               v.astype(np.int64) if k in ("capacity_bytes", "p_capacity_bytes") else
+               v.astype(np.int32))
            for k, v in pts.items()}
     return g["model"], traces, pts, g["cases"]
 
@@ -149,20 +155,35 @@ def _fuzz_case(rng, n_pts):
         permille = int(rng.choice([0, 0, 0, 250, 500, 1000]))
         # swap preemption over a link moving a 16-byte token in 16, 0.5 or 0.016 ns
         swap_bw = float(rng.choice([0.0, 0.0, 0.0, 1e9, 3.2e10, 1e12]))
+        # a quarter of the points disaggregated: 1-3 prefill and 1-3 decode
+        # devices, KV links moving a token in 0, 1 or 10 ns
+        pd = dict(n_prefill=0, n_decode=0, p_peak_flops=0.0, p_mem_bw=0.0, p_capacity_bytes=0,
+                  kv_link_bw=0.0)
+        if rng.random() < 0.25:
+            policy = 0
+            nbp = int(rng.integers(0, 21)) if M < 64 else int(rng.integers(0, 400))
+            pfast = rng.random() < 0.5
+            pd = dict(n_prefill=int(rng.integers(1, 4)), n_decode=int(rng.integers(1, 4)),
+                      p_peak_flops=1e300 if pfast else float(rng.choice([2e9, 5e9])),
+                      p_mem_bw=1e300 if pfast else float(rng.choice([2e8, 1e9])),
+                      p_capacity_bytes=max(1, nbp * b * 16),
+                      kv_link_bw=float(rng.choice([0.0, 16e9, 1.6e9])))
         rows.append(dict(peak_flops=1e300 if fast else float(rng.choice([1e9, 3e9])),
                          mem_bw=1e300 if fast else float(rng.choice([1e8, 7e8])),
                          capacity_bytes=max(1, nb * b * 16), mem_util_permille=1000,
                          block_size=b, max_batch=M, chunk_size=K, trace_id=k,
                          policy=policy, admit_mem_permille=permille, swap_bw=swap_bw,
-                         swap_overlap=int(rng.integers(0, 2))))
+                         swap_overlap=int(rng.integers(0, 2)), **pd))
     pts = {
         "peak_flops": np.array([r["peak_flops"] for r in rows], np.float64),
         "mem_bw": np.array([r["mem_bw"] for r in rows], np.float64),
         "capacity_bytes": np.array([r["capacity_bytes"] for r in rows], np.int64),
-        "swap_bw": np.array([r["swap_bw"] for r in rows], np.float64),
+        "p_capacity_bytes": np.array([r["p_capacity_bytes"] for r in rows], np.int64),
+        **{f: np.array([r[f] for r in rows], np.float64)
+           for f in ("swap_bw", "p_peak_flops", "p_mem_bw", "kv_link_bw")},
         **{f: np.array([r[f] for r in rows], np.int32)
            for f in ("mem_util_permille", "block_size", "max_batch", "chunk_size", "trace_id",
-                     "policy", "admit_mem_permille", "swap_overlap")}}
+                     "policy", "admit_mem_permille", "swap_overlap", "n_prefill", "n_decode")}}
     return traces, pts
 
 
@@ -220,6 +241,82 @@ def test_full_c7_swap(S, oracle):
     fast = pts["swap_bw"] == 64e9
     ov, sq = fast & (pts["swap_overlap"] == 1), fast & (pts["swap_overlap"] == 0)
     assert out["sum_e2e_ns"][ov].sum() < out["sum_e2e_ns"][sq].sum()
+
+
+def test_full_c8_disaggregated(S, oracle):
+    """Disaggregated prefill and decode devices (P/D splits of an 8-device
+    node, four prefill-device variants): every point and every request."""
+    m, traces, pts = W.make_config("c8")
+    t0 = time.time()
+    o_out, o_req = oracle.run_points(m, traces, pts, per_request=True)
+    say("c8: oracle %.1fs, iterations %d" % (time.time() - t0, int(o_out["n_iters"].sum())))
+    out, req = gpu_run(S, m, traces, pts, per_request=True, iter_cap=cap_from(o_out))
+    compare_points(out, o_out, "c8")
+    compare_requests(req, o_req, "c8")
+    assert (out["status"] == 0).all()
+    # first tokens come from the prefill side only: twice the prefill FLOP/s
+    # never raises the TTFT sum
+    hw = np.arange(len(pts["peak_flops"])) % 4
+    assert (out["sum_ttft_ns"][hw == 1] <= out["sum_ttft_ns"][hw == 0]).all()
+
+
+def _pd_rows(base, **kw):
+    r = dict(base)
+    r.update(kw)
+    return r
+
+
+def test_disaggregated_edges(S, oracle):
+    """Disaggregated points at the edges: empty trace, no KV block on either
+    side, the most devices, max batch 256 on both sides, chunked prefill,
+    swap on the decode side, a sub-range of points and the iteration cap."""
+    m = W.MODELS["llama2-7b"]
+    rng = np.random.default_rng(7)
+    n = 300
+    tr = {"arrival_ns": np.sort(rng.integers(0, 5_000_000_000, n)).astype(np.int64),
+          "prompt_len": rng.integers(1, 3000, n).astype(np.int32),
+          "output_len": rng.integers(1, 400, n).astype(np.int32)}
+    empty = {"arrival_ns": np.zeros(0, np.int64), "prompt_len": np.zeros(0, np.int32),
+             "output_len": np.zeros(0, np.int32)}
+    traces = [tr, empty]
+    base = dict(peak_flops=312e12, mem_bw=2e12, capacity_bytes=80_000_000_000,
+                mem_util_permille=900, block_size=16, max_batch=64, chunk_size=0, trace_id=0,
+                policy=0, admit_mem_permille=0, swap_overlap=0, swap_bw=0.0, n_prefill=2,
+                n_decode=3, p_peak_flops=500e12, p_mem_bw=1e12,
+                p_capacity_bytes=40_000_000_000, kv_link_bw=20e9)
+    rows = [
+        _pd_rows(base, trace_id=1),                                    # empty trace
+        _pd_rows(base, p_capacity_bytes=10_000_000_000),               # prefill side: no KV
+        _pd_rows(base, capacity_bytes=10_000_000_000),                 # decode side: no KV
+        _pd_rows(base, n_prefill=16, n_decode=16),                     # the most devices
+        _pd_rows(base, max_batch=256, n_prefill=1, n_decode=1),        # class 2 on both sides
+        _pd_rows(base, max_batch=100, chunk_size=512),                 # class 1, chunked
+        _pd_rows(base, capacity_bytes=18_000_000_000, swap_bw=32e9,    # decode-side pressure,
+                 admit_mem_permille=900, n_decode=1),                  # swap and the ratio
+        _pd_rows(base, capacity_bytes=18_000_000_000, n_decode=1),     # ... with recompute
+        _pd_rows(base, kv_link_bw=0.0, n_prefill=1),                   # instant link
+        _pd_rows(base, n_prefill=0, n_decode=0),                       # one worker, same sweep
+    ]
+    pts = {k: np.array([r[k] for r in rows]) for k in rows[0]}
+    pts = {k: (v.astype(np.float64) if k in FLOAT_FIELDS else
+               v.astype(np.int64) if k in ("capacity_bytes", "p_capacity_bytes") else
+               v.astype(np.int32)) for k, v in pts.items()}
+    o_out, o_req = oracle.run_points(m, traces, pts, per_request=True)
+    assert (o_out["status"][[1, 2]] == 1).all() and o_out["n_preempt"][[6, 7]].min() > 0
+    out, req = gpu_run(S, m, traces, pts, per_request=True, iter_cap=cap_from(o_out))
+    compare_points(out, o_out, "pd edge")
+    compare_requests(req, o_req, "pd edge")
+    # a sub-range of the points
+    sub = dict(first_point=3, n_points=4)
+    out2, req2 = gpu_run(S, m, traces, pts, per_request=True, iter_cap=cap_from(o_out), **sub)
+    compare_points(out2, o_out[3:7], "pd sub-range")
+    compare_requests(req2, o_req[3:7], "pd sub-range")
+    # the iteration cap stops each device alike
+    o_cap, o_rq = oracle.run_points(m, traces, pts, per_request=True, iter_cap=50)
+    g_cap, g_rq = gpu_run(S, m, traces, pts, per_request=True, iter_cap=50)
+    compare_points(g_cap, o_cap, "pd iter cap")
+    compare_requests(g_rq, o_rq, "pd iter cap")
+    assert (g_cap["status"] == 2).sum() >= 5
 
 
 def test_full_c3_points(S, oracle):
