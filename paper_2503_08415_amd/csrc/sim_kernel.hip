@@ -334,7 +334,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
   };
   const double iF = P.inv_flops_ns, iB = P.inv_bw_ns;
   const int oi = P.out_index;
-  const int orow = P.out_point;  // the design point's row
+  const int orow = MODE == kStageOne ? oi : P.out_point;  // the design point's row
   ts_req_result* RR = A.req ? A.req + (size_t)orow * (size_t)A.max_n : nullptr;
   int64_t* E2E = A.e2e + (size_t)orow * (size_t)A.max_n + pos_off;
   int64_t* TTFT = A.ttft + (size_t)orow * (size_t)A.max_n + pos_off;
