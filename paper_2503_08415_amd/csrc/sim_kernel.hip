@@ -261,6 +261,9 @@ struct SlotLds {
   long long max_e2e, last_fin;
   unsigned int slo_ok, slo_tpot_ok;
   unsigned int sub_cnt[kMaxDev];  // prefill device: requests handed to each decode device
+  // steady segment: the two attention operators' FLOPs, bytes and their
+  // per-iteration steps at the segment start, then the other operators' times
+  double segk[13];
   union {
     StageSlot stage[64];
     int64_t scratch[NCH * 64];
@@ -708,6 +711,14 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
           k_t4 = dpp_f64<0x103>(tl0);
           k_t5 = dpp_f64<0x104>(tl0);
           k_lm = dpp_f64<0x105>(tl0);
+          if (lane == 1) {
+            L.segk[0] = Fw; L.segk[1] = Bw; L.segk[2] = dF; L.segk[3] = dB;
+            L.segk[8] = k_t0; L.segk[9] = k_t3; L.segk[10] = k_t4; L.segk[11] = k_t5;
+            L.segk[12] = k_lm;
+          }
+          if (lane == 2) {
+            L.segk[4] = Fw; L.segk[5] = Bw; L.segk[6] = dF; L.segk[7] = dB;
+          }
           // every iteration is below 2^lg_iter ns: this many keep the fp64
           // clock below 2^52
           const int64_t ks = (kT52 - (int64_t)rdl_f64(t_d, 1)) >> P.lg_iter;
@@ -751,6 +762,93 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
         while (more) {
           // steady iterations up to the segment's last
           while (dG != stop) {
+            // iterations that may run as one block: up to 64, through the
+            // segment's last and its first finishing iteration
+            int W = stop - dG;
+            W = W < 64 ? W : 64;
+            W = fin_at - dG + 1 < W ? fin_at - dG + 1 : W;
+            if (W >= 2) {
+              // A block of consecutive iterations, lane i pricing iteration
+              // dG + i exactly as one iteration at a time would (the
+              // operators' FLOPs and bytes are exact integers, stepped by
+              // exact integer increments).  It ends before the first
+              // iteration short of blocks and after the first one whose end
+              // reaches an arrival that matters.
+              const int g0 = dG;
+              int* hist = reinterpret_cast<int*>(L.u.scratch);  // blocks taken per iteration
+              hist[lane] = 0;
+              __syncthreads();
+#pragma unroll
+              for (int j = 0; j < NCH; ++j) {
+                if (j < nchd) {
+                  const int o = rr[j] - g0;  // this slot's next block boundary (alive: >= 0)
+                  if (o >= 0 && o < W)
+                    for (int pz = o; pz < W; pz += B) atomicAdd(&hist[pz], 1);
+                }
+              }
+              __syncthreads();
+              const bool in = lane < W;
+              const int T = scan_i32(in ? hist[lane] : 0);  // blocks taken through iteration i
+              const double mi = (double)(g0 - seg0 + lane);
+              const double F1 = L.segk[0] + mi * L.segk[2];
+              const double B1 = L.segk[1] + mi * L.segk[3];
+              const double F2 = L.segk[4] + mi * L.segk[6];
+              const double B2 = L.segk[5] + mi * L.segk[7];
+              const double t1 = __builtin_fmax(F1 * iF, B1 * iB);
+              const double t2 = __builtin_fmax(F2 * iF, B2 * iB);
+              double lay = L.segk[8] + t1;
+              lay = lay + t2;
+              lay = lay + L.segk[9];
+              lay = lay + L.segk[10];
+              lay = lay + L.segk[11];
+              double tot = A.n_layers * lay;
+              tot = tot + L.segk[12];
+              const double itv = __builtin_fmax(ceil(tot), 1.0);
+              const int64_t S = scan_i64(in ? (int64_t)itv : 0);  // time through iteration i
+              const int64_t t0 = (int64_t)rdl_f64(t_d, 1);
+              const uint64_t short_m = ballot(in && T > freeb);
+              const uint64_t arr_m = watch ? ballot(in && (double)(t0 + S) >= thr) : 0ull;
+              int Kb = W;
+              if (short_m != 0) {
+                const int k = (int)__builtin_ctzll(short_m);
+                Kb = k < Kb ? k : Kb;
+              }
+              if (arr_m != 0) {
+                const int k = (int)__builtin_ctzll(arr_m) + 1;
+                Kb = k < Kb ? k : Kb;
+              }
+              const int last = Kb - 1;
+              // the used-block integral: one fp64 sum in iteration order; when
+              // every term and the total stay below 2^53 it is an exact
+              // integer sum, and any order gives it
+              const double pv = (double)(NB - freeb + T) * itv;
+              const double ub0 = rdl_f64(ub, 1);
+              constexpr double kT53d = 9007199254740992.0;
+              double ubn = ub0;
+              bool exact = ub0 < kT53d && ballot(lane < Kb && !(pv < kT53d)) == 0;
+              if (exact) {
+                const int64_t sum = (int64_t)ub0 + wsum64(lane < Kb ? (int64_t)pv : 0);
+                exact = sum < (int64_t)1 << 53;
+                if (exact) ubn = (double)sum;
+              }
+              if (!exact)
+                for (int k = 0; k < Kb; ++k) ubn = ubn + rdl_f64(pv, k);
+              freeb -= rdl(T, last);
+              t_d = (double)(t0 + rdl64(S, last));
+              ub = ubn;
+              it = rdl_f64(itv, last);
+              const double kd = (double)Kb;
+              Fw = Fw + kd * dF;
+              Bw = Bw + kd * dB;
+#pragma unroll
+              for (int j = 0; j < NCH; ++j) {
+                if (j < nchd) {
+                  const int o = rr[j] - g0;
+                  if (o >= 0 && o < Kb) rr[j] += B * (divB(last - o) + 1);
+                }
+              }
+              dG = g0 + last;  // the block's last iteration; advanced past below
+            } else {
             freeb -= nneed;
 #pragma unroll
             for (int j = 0; j < NCH; ++j)
@@ -772,6 +870,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
             t_d = t_d + it;
             Fw = Fw + dF;
             Bw = Bw + dB;
+            }
             if (dG == fin_at) {
               // Alive decodes emitting their last token finish at the end of
               // this iteration.  Iteration times never fall within a
