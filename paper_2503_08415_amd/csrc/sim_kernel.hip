@@ -681,7 +681,8 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
         // iteration and key sum, the head prefill's chunk, every operator's
         // work and its per-iteration step, and the segment's last iteration.
         auto setup = [&]() {
-          int mx = 0, cs = 0;
+          // per lane over the chunks first, then one reduction each
+          int mxl = 0, csl = 0;
 #pragma unroll
           for (int j = 0; j < NCH; ++j) {
             if (j < nchd) {
@@ -689,11 +690,13 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
               const int rem0 = j == 0 ? h0.rem : L.x_rem[e];
               const int ctx0 = j == 0 ? h0.ctx : L.x_ctx[e];
               const bool al = rr[j] >= 0;
-              const int m = rdl(scan_max_i32(al ? 0x7fffffff - rem0 : 0), 63);
-              mx = m > mx ? m : mx;
-              cs += wsum(al ? ctx0 + 1 : 0);
+              const int m = al ? 0x7fffffff - rem0 : 0;
+              mxl = m > mxl ? m : mxl;
+              csl += al ? ctx0 + 1 : 0;
             }
           }
+          const int mx = rdl(scan_max_i32(mxl), 63);
+          const int cs = wsum(csl);
           fin_at = nDa > 0 ? 0x7fffffff - mx - 1 : 0x3fffffff;
           cd_seg = cs + nDa * dG;
           q = npf > 0 ? K - nDa : 0;
