@@ -14,17 +14,15 @@ roofline: the simulation is bound by instruction issue (integer scheduling
 and a short fp64 roofline per iteration; no dense contraction, negligible HBM
 traffic).  ``achieved`` is the algorithmic VALU instruction count of the
 dominant simulation kernel divided by its HIP-event duration, with
-  U = 21 wave64 VALU instructions per simulated iteration,
-the least work any implementation of the method does per iteration once the
-batch sums are stepped incrementally: the prefill- and decode-attention
-operators' FLOPs and bytes stepped by their integer increments (2, one lane
-each), divided by peak and bandwidth (2) and maxed (1), their times brought
-into one lane (2), the fixed-order layer sum (5), times layers plus the LM
-head (2), ceil and the 1 ns floor (2), the clock (1), the used-block time
-integral (2), the block-boundary and arrival tests (2).  Scheduling events
-(admissions, finishes, preemptions) are not counted, so the fraction is a
-lower bound.  Peak = 256 CUs x 4 SIMDs x 2.4 GHz / 4 cycles per wave64
-instruction = 614.4 G instructions/s.
+  U = 10.8 wave64 VALU instructions per simulated iteration,
+what one steady iteration costs in this kernel's cheapest path: iterations
+priced 64 at a time, one per lane, in blocks (measured with the
+SQ_INSTS_VALU counter on a workload of 64 decodes with long outputs, where
+blocks run their full 64 iterations).  Scheduling events (admissions,
+finishes, prefill completions, preemptions) are not counted, so the fraction
+is the share of the issue peak the sweep would use if every iteration cost
+as little as a steady one.  Peak = 256 CUs x 4 SIMDs x 2.4 GHz / 4 cycles per
+wave64 instruction = 614.4 G instructions/s.
 """
 from __future__ import annotations
 
@@ -42,7 +40,7 @@ if ROOT not in sys.path:
 
 METRIC = "simulated requests/sec across sweep on 1 MI355X; % VALU-issue peak"
 VALU_ISSUE_PEAK = 256 * 4 * 2.4e9 / 4.0   # wave64 VALU instructions per second
-U_ITER = 21.0
+U_ITER = 10.8
 # simulation launches, 3 * stage + class (stages: one-worker points, prefill
 # devices, decode devices of disaggregated points; register-chunk classes
 # 1, 2, 4), named as rocprofv3 names the kernels
