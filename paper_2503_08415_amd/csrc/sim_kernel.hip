@@ -80,6 +80,21 @@ __device__ __forceinline__ int64_t scan_i64(int64_t v) {
   v += dpp0_64<0x143, 0xc>(v);
   return v;
 }
+// Inclusive prefix sum of doubles (zero fill adds +0.0).  Exact while every
+// value is an integer and every partial sum stays below 2^53, whatever the
+// order of the additions.
+__device__ __forceinline__ double scan_f64(double v) {
+  auto sh = [](double x, auto ctrl) {
+    return __builtin_bit_cast(double, ctrl(__builtin_bit_cast(int64_t, x)));
+  };
+  v = v + sh(v, [](int64_t x) { return dpp0_64<0x111, 0xf>(x); });
+  v = v + sh(v, [](int64_t x) { return dpp0_64<0x112, 0xf>(x); });
+  v = v + sh(v, [](int64_t x) { return dpp0_64<0x114, 0xf>(x); });
+  v = v + sh(v, [](int64_t x) { return dpp0_64<0x118, 0xf>(x); });
+  v = v + sh(v, [](int64_t x) { return dpp0_64<0x142, 0xa>(x); });
+  v = v + sh(v, [](int64_t x) { return dpp0_64<0x143, 0xc>(x); });
+  return v;
+}
 // Inclusive prefix max of non-negative values (0 is the identity).
 __device__ __forceinline__ int64_t scan_max_i64(int64_t v) {
   int64_t u;
@@ -807,10 +822,11 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
               double tot = A.n_layers * lay;
               tot = tot + L.segk[12];
               const double itv = __builtin_fmax(ceil(tot), 1.0);
-              const int64_t S = scan_i64(in ? (int64_t)itv : 0);  // time through iteration i
-              const int64_t t0 = (int64_t)rdl_f64(t_d, 1);
+              // the clock at each iteration's end: integers below 2^52, so
+              // the fp64 prefix sum is exact
+              const double tend = rdl_f64(t_d, 1) + scan_f64(in ? itv : 0.0);
               const uint64_t short_m = ballot(in && T > freeb);
-              const uint64_t arr_m = watch ? ballot(in && (double)(t0 + S) >= thr) : 0ull;
+              const uint64_t arr_m = watch ? ballot(in && tend >= thr) : 0ull;
               int Kb = W;
               if (short_m != 0) {
                 const int k = (int)__builtin_ctzll(short_m);
@@ -830,14 +846,16 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
               double ubn = ub0;
               bool exact = ub0 < kT53d && ballot(lane < Kb && !(pv < kT53d)) == 0;
               if (exact) {
-                const int64_t sum = (int64_t)ub0 + wsum64(lane < Kb ? (int64_t)pv : 0);
-                exact = sum < (int64_t)1 << 53;
-                if (exact) ubn = (double)sum;
+                // integer terms: the tree sum is exact exactly when the true
+                // total stays below 2^53 (rounding is monotone, 2^53 exact)
+                const double sum = ub0 + rdl_f64(scan_f64(lane < Kb ? pv : 0.0), 63);
+                exact = sum < kT53d;
+                if (exact) ubn = sum;
               }
               if (!exact)
                 for (int k = 0; k < Kb; ++k) ubn = ubn + rdl_f64(pv, k);
               freeb -= rdl(T, last);
-              t_d = (double)(t0 + rdl64(S, last));
+              t_d = rdl_f64(tend, last);
               ub = ubn;
               it = rdl_f64(itv, last);
               const double kd = (double)Kb;
