@@ -1638,35 +1638,56 @@ template __global__ void sim_kernel<2, kStageDecode>(SimArgs);
 template __global__ void sim_kernel<4, kStageDecode>(SimArgs);
 
 // ------------------------------------------------------------ statistics
-// Nearest-rank percentiles of the finished requests' latencies: k-th
-// smallest by most-significant-digit radix select (8-bit digits) with an
-// LDS histogram.  One 256-thread workgroup per point.
-__device__ int64_t select_kth(const int64_t* v, int n, int k, int* hist, int* sh) {
-  uint64_t prefix = 0;
-  for (int shift = 56; shift >= 0; shift -= 8) {
-    const uint64_t hi_mask = shift == 56 ? 0ull : (~0ull << (shift + 8));
-    hist[threadIdx.x] = 0;
+// Nearest-rank percentiles of the finished requests' latencies: the k-th
+// smallest values by most-significant-digit radix select (8-bit digits),
+// several ranks at once (one LDS histogram each, one pass over the values per
+// digit), starting at the highest digit any value uses.  One 256-thread
+// workgroup per point.
+template <int NK>
+__device__ void select_ranks(const int64_t* v, int n, const int* ks, int top_shift,
+                             int64_t* out, int* hist, int* sh) {
+  uint64_t prefix[NK];
+  int k[NK];
+#pragma unroll
+  for (int r = 0; r < NK; ++r) {
+    prefix[r] = 0;
+    k[r] = ks[r];
+  }
+  for (int shift = top_shift; shift >= 0; shift -= 8) {
+    const uint64_t hi_mask = shift >= 56 ? 0ull : (~0ull << (shift + 8));
+#pragma unroll
+    for (int r = 0; r < NK; ++r) hist[r * 256 + threadIdx.x] = 0;
     __syncthreads();
     for (int i = threadIdx.x; i < n; i += 256) {
       const uint64_t x = (uint64_t)v[i];
-      if (((x ^ prefix) & hi_mask) == 0) atomicAdd(&hist[(x >> shift) & 255u], 1);
+      const int d = (int)((x >> shift) & 255u);
+#pragma unroll
+      for (int r = 0; r < NK; ++r)
+        if (((x ^ prefix[r]) & hi_mask) == 0) atomicAdd(&hist[r * 256 + d], 1);
     }
     __syncthreads();
-    if (threadIdx.x == 0) {
+    if (threadIdx.x < NK) {
+      const int r = threadIdx.x;
       int acc = 0, d = 0;
       for (; d < 255; ++d) {
-        if (acc + hist[d] > k) break;
-        acc += hist[d];
+        if (acc + hist[r * 256 + d] > sh[2 * NK + r]) break;
+        acc += hist[r * 256 + d];
       }
-      sh[0] = d;
-      sh[1] = k - acc;
+      sh[2 * r] = d;
+      sh[2 * r + 1] = sh[2 * NK + r] - acc;
     }
     __syncthreads();
-    prefix |= (uint64_t)sh[0] << shift;
-    k = sh[1];
+#pragma unroll
+    for (int r = 0; r < NK; ++r) {
+      prefix[r] |= (uint64_t)sh[2 * r] << shift;
+      k[r] = sh[2 * r + 1];
+    }
+    __syncthreads();
+    if (threadIdx.x < NK) sh[2 * NK + threadIdx.x] = k[threadIdx.x];
     __syncthreads();
   }
-  return (int64_t)prefix;
+#pragma unroll
+  for (int r = 0; r < NK; ++r) out[r] = (int64_t)prefix[r];
 }
 
 __device__ __forceinline__ int nearest_rank_index(int pct, int n) {
@@ -1676,19 +1697,28 @@ __device__ __forceinline__ int nearest_rank_index(int pct, int n) {
 __global__ __launch_bounds__(256) void stats_kernel(const int64_t* e2e, const int64_t* ttft,
                                                     ts_point_result* res, int max_n,
                                                     int n_points) {
-  __shared__ int hist[256];
-  __shared__ int sh[2];
+  __shared__ int hist[3 * 256];
+  __shared__ int sh[9];
   for (int p = blockIdx.x; p < n_points; p += gridDim.x) {
     const int n = res[p].n_done;
     int64_t r[5] = {-1, -1, -1, -1, -1};
     if (n > 0) {
       const int64_t* ve = e2e + (size_t)p * (size_t)max_n;
       const int64_t* vt = ttft + (size_t)p * (size_t)max_n;
-      r[0] = select_kth(ve, n, nearest_rank_index(50, n), hist, sh);
-      r[1] = select_kth(ve, n, nearest_rank_index(90, n), hist, sh);
-      r[2] = select_kth(ve, n, nearest_rank_index(99, n), hist, sh);
-      r[3] = select_kth(vt, n, nearest_rank_index(50, n), hist, sh);
-      r[4] = select_kth(vt, n, nearest_rank_index(99, n), hist, sh);
+      // every latency lies in [0, max_e2e] (a first token never comes after
+      // the finish): digits above the top one are zero for all of them
+      const uint64_t mx = (uint64_t)res[p].max_e2e_ns;
+      const int bits = mx == 0 ? 1 : 64 - __builtin_clzll(mx);
+      const int top_shift = ((bits - 1) / 8) * 8;
+      const int ke[3] = {nearest_rank_index(50, n), nearest_rank_index(90, n),
+                         nearest_rank_index(99, n)};
+      const int kt[2] = {nearest_rank_index(50, n), nearest_rank_index(99, n)};
+      if (threadIdx.x < 3) sh[6 + threadIdx.x] = ke[threadIdx.x];
+      __syncthreads();
+      select_ranks<3>(ve, n, ke, top_shift, r, hist, sh);
+      if (threadIdx.x < 2) sh[4 + threadIdx.x] = kt[threadIdx.x];
+      __syncthreads();
+      select_ranks<2>(vt, n, kt, top_shift, r + 3, hist, sh);
     }
     if (threadIdx.x == 0) {
       res[p].p50_e2e_ns = r[0];
