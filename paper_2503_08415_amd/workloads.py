@@ -347,6 +347,20 @@ def _c8(n_req):
     return "llama2-7b", traces, rows
 
 
+def _u1(n_req):
+    """Calibration of the steady path: 8192 identical points, each 64
+    requests arriving together (prompt 16, output 4000) that decode side by
+    side for 4000 iterations, so almost every iteration is a steady one in a
+    full 64-iteration block."""
+    n = 64
+    traces = [{"arrival_ns": np.zeros(n, np.int64), "prompt_len": np.full(n, 16, np.int32),
+               "output_len": np.full(n, 4000, np.int32)}]
+    rows = [dict(peak_flops=312e12, mem_bw=2e12, capacity_bytes=80_000_000_000,
+                 mem_util_permille=900, block_size=16, max_batch=64, chunk_size=0,
+                 trace_id=0) for _ in range(8192)]
+    return "llama2-7b", traces, rows
+
+
 # name -> (builder, default requests per trace, description)
 CONFIGS = {
     "c1": (_c1, 64, "1 point x 64 requests, 7B MHA, 312 TF / 2 TB/s / 80 GB, "
@@ -363,6 +377,8 @@ CONFIGS = {
                       "static} x admission ratio {off, 60%, 80%, 95%} x {24, 40} GB"),
     "c7": (_c7, 2000, "320 points x 2000 requests, 7B MHA, 16 rates x {recompute, swap "
                       "16/32/64 GB/s, swap 64 GB/s overlapped} x {20, 24} GB x {no chunk, 512}"),
+    "u1": (_u1, 64, "8192 points x 64 requests decoding together for 4000 iterations "
+                    "(calibration of the steady path)"),
     "c8": (_c8, 2000, "256 disaggregated points x 2000 requests, 7B MHA, 4 length mixes x "
                       "4 rates x P/D {1/7, 2/6, 3/5, 4/4} x 4 prefill devices, 25 GB/s KV links"),
 }
