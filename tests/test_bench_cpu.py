@@ -1,0 +1,53 @@
+"""Host-side checks of the benchmark contract and the synthetic workloads
+(no GPU): the multi-GPU refusal, the seeded generators' determinism, and the
+shapes each named sweep promises."""
+import os
+import subprocess
+import sys
+
+import numpy as np
+import pytest
+
+from paper_2503_08415_amd import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_bench_refuses_more_than_one_gpu():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+
+
+@pytest.mark.parametrize("name", ["c1", "c2", "c6", "c7", "c8", "u1"])
+def test_workloads_are_seeded_and_shaped(name):
+    m1, t1, p1 = W.make_config(name)
+    m2, t2, p2 = W.make_config(name)
+    assert m1 == m2 and len(t1) == len(t2)
+    for a, b in zip(t1, t2):
+        for k in ("arrival_ns", "prompt_len", "output_len"):
+            assert np.array_equal(a[k], b[k])
+        assert (np.diff(a["arrival_ns"]) >= 0).all()
+        assert (a["prompt_len"] >= 1).all() and (a["output_len"] >= 1).all()
+    for k in p1:
+        assert np.array_equal(p1[k], p2[k])
+    n = len(p1["peak_flops"])
+    assert set(p1) == set(W.POINT_FIELDS)
+    assert ((p1["trace_id"] >= 0) & (p1["trace_id"] < len(t1))).all()
+    assert W.CONFIGS[name][2].startswith("%d " % n)  # the description names the point count
+
+
+def test_c8_splits_an_eight_device_node():
+    _, _, p = W.make_config("c8")
+    assert ((p["n_prefill"] + p["n_decode"]) == 8).all()
+    assert set(p["n_prefill"].tolist()) == {1, 2, 3, 4}
+    assert (p["policy"] == 0).all() and (p["kv_link_bw"] > 0).all()
+
+
+def test_u1_calibration_workload_is_one_steady_batch():
+    _, t, p = W.make_config("u1")
+    assert len(t) == 1 and len(p["peak_flops"]) == 8192
+    tr = t[0]
+    assert (tr["arrival_ns"] == 0).all() and len(tr["arrival_ns"]) == 64
+    assert (tr["output_len"] == 4000).all() and (p["max_batch"] == 64).all()
