@@ -186,3 +186,37 @@ def test_null_handle_calls(L):
     a, b = C.c_float(), C.c_float()
     assert L.ts_sweep_timing(None, C.byref(a), C.byref(b)) == S.TS_ERR_ARG
     L.ts_sweep_destroy(None)
+
+
+def test_missing_library_fails_loudly():
+    # the binding has no fallback: without the built library every call raises
+    code = ("import sys; sys.path.insert(0, %r)\n"
+            "from paper_2503_08415_amd import sweep as S\n"
+            "S.LIB_PATH = '/nonexistent/libts_sweep.so'\n"
+            "try:\n    S.lib()\nexcept RuntimeError as e:\n    print('raised', e)\n" % ROOT)
+    import subprocess
+    import sys
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0 and r.stdout.startswith("raised") and "not built" in r.stdout
+
+
+def test_product_package_never_reaches_the_oracle():
+    # the oracle is test infrastructure: no module of the package imports,
+    # loads or names it as code
+    pkg = os.path.join(ROOT, "paper_2503_08415_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if not f.endswith((".py", ".hip", ".h", ".c", ".cpp")):
+                continue
+            src = open(os.path.join(dirpath, f)).read()
+            assert not re.search(r"^\s*(from|import)\s+oracle\b", src, flags=re.M), f
+            assert "tso_" not in src and "libtso" not in src and "tso.h" not in src, f
+
+
+def test_oracle_shares_no_code_with_the_hip_path():
+    odir = os.path.join(ROOT, "oracle")
+    for f in os.listdir(odir):
+        if f.endswith((".py", ".c", ".h")):
+            src = open(os.path.join(odir, f)).read()
+            for name in ("paper_2503_08415_amd", "ts_sweep", "csrc", "sweep_internal"):
+                assert name not in src, (f, name)
