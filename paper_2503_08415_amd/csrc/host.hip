@@ -605,8 +605,9 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
     if (e != hipSuccess) { release(h); return device_error(e, "occupancy query"); }
     per_cu = std::max(per_cu, 1);
     h->grid[l] = std::min(h->class_n[l], n_cu * per_cu);
-    // per-workgroup request-time table: max_n entries; keep it under 1 GiB
-    const int64_t cap = std::max<int64_t>(1, ((int64_t)1 << 30) /
+    // per-workgroup request-time table: max_n entries; keep it under 16 GiB
+    // (a full grid at 10^4 requests per point needs about 1.2 GB)
+    const int64_t cap = std::max<int64_t>(1, ((int64_t)1 << 34) /
                                                  ((int64_t)std::max<int64_t>(max_n, 1) *
                                                   (int64_t)sizeof(ReqTimes)));
     h->grid[l] = (int)std::min<int64_t>(h->grid[l], cap);

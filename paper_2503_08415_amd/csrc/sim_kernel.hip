@@ -257,9 +257,10 @@ struct Hot {
   int64_t gap;
 };
 
-// Admission staging: one entry per admitted candidate of a window.
+// Admission staging: one entry per admitted candidate of a window (its
+// request index and preemption count go straight to their slot).
 struct StageSlot {
-  int32_t id, tgt, rem, npre, fl, q, room, ctx;
+  int32_t tgt, rem, fl, q, room, ctx;
   int64_t gap;
 };
 
@@ -268,9 +269,10 @@ struct SlotLds {
   static constexpr int NX = NCH > 1 ? NCH - 1 : 1;  // LDS chunks (storage for one when unused)
   int32_t x_ctx[NX * 64], x_tgt[NX * 64], x_rem[NX * 64], x_room[NX * 64], x_q[NX * 64];
   int64_t x_gap[NX * 64];
-  int32_t x_fl[NX * 64];
   int32_t id[NCH * 64];    // request index per slot
   int32_t npre[NCH * 64];  // times preempted per slot
+  uint8_t x_fl[NX * 64];   // flags fit a byte: with the staging below, 256 slots
+                           // take at most 10 KiB, so 16 workgroups share a CU
   // finished-request statistics of the point, accumulated by LDS atomics
   unsigned long long sum_ttft, sum_e2e, sum_tpot, digest;
   long long max_e2e, last_fin;
@@ -1388,8 +1390,10 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
           } else {
             if (!fromq) RT[c_id].admit = t;  // first admission
           }
+          L.id[nrun + rank] = c_id;  // rank < M - nrun: a free slot
+          L.npre[nrun + rank] = c_npre;
           StageSlot st;
-          st.id = c_id; st.tgt = c_tgt; st.rem = c_rem; st.npre = c_npre;
+          st.tgt = c_tgt; st.rem = c_rem;
           st.fl = swin ? (c_fl | FL_IDLE) : c_fl;
           st.q = qv; st.room = need * B - c_top; st.ctx = c_ctx; st.gap = c_gap;
           L.u.stage[rank] = st;
@@ -1404,8 +1408,6 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
             h.ctx = st.ctx; h.tgt = st.tgt; h.rem = st.rem; h.room = st.room; h.fl = st.fl;
             h.q = st.q; h.gap = st.gap;
             store_chunk<NCH>(L, h0, j, lane, h);
-            L.id[s] = st.id;
-            L.npre[s] = st.npre;
           }
         }
         __syncthreads();
