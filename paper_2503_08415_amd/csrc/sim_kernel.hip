@@ -44,9 +44,16 @@ __device__ __forceinline__ int64_t rdl64(int64_t v, int l) {
   return (int64_t)(((uint64_t)hi << 32) | lo);
 }
 
+// Row shift with zero fill (bound_ctrl): every lane is written, no "old".
+template <int CTRL>
+__device__ __forceinline__ int shr0(int v) {
+  return __builtin_amdgcn_mov_dpp(v, CTRL, 0xf, 0xf, true);
+}
 // DPP move with zero for lanes whose source is outside the row / not selected.
+// A row shift over every row needs no zeroed "old": bound_ctrl fills it.
 template <int CTRL, int ROWS>
 __device__ __forceinline__ int dpp0(int v) {
+  if constexpr (ROWS == 0xf && (CTRL & 0xff0) == 0x110) return shr0<CTRL>(v);
   return __builtin_amdgcn_update_dpp(0, v, CTRL, ROWS, 0xf, false);
 }
 template <int CTRL, int ROWS>
@@ -54,11 +61,6 @@ __device__ __forceinline__ int64_t dpp0_64(int64_t v) {
   const uint32_t lo = (uint32_t)dpp0<CTRL, ROWS>((int)(uint32_t)v);
   const uint32_t hi = (uint32_t)dpp0<CTRL, ROWS>((int)(uint32_t)((uint64_t)v >> 32));
   return (int64_t)(((uint64_t)hi << 32) | lo);
-}
-// Row shift with zero fill (bound_ctrl): every lane is written, no "old".
-template <int CTRL>
-__device__ __forceinline__ int shr0(int v) {
-  return __builtin_amdgcn_mov_dpp(v, CTRL, 0xf, 0xf, true);
 }
 // Inclusive prefix sum over the 64 lanes: Hillis-Steele inside each 16-lane
 // row (row_shr 1, 2, 4, 8), then row 15 -> rows 1,3 and row 31 -> rows 2,3.
