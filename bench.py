@@ -14,11 +14,11 @@ roofline: the simulation is bound by instruction issue (integer scheduling
 and a short fp64 roofline per iteration; no dense contraction, negligible HBM
 traffic).  ``achieved`` is the algorithmic VALU instruction count of the
 dominant simulation kernel divided by its HIP-event duration, with
-  U = 9.8 wave64 VALU instructions per simulated iteration,
+  U = 9.5 wave64 VALU instructions per simulated iteration,
 what one steady iteration costs in this kernel's cheapest path: iterations
-priced 64 at a time, one per lane, in blocks (measured with the
+priced up to 64 at a time, one per lane, in blocks (measured with the
 SQ_INSTS_VALU counter on the u1 workload, 64 decodes with long outputs per
-point, where blocks run their full 64 iterations).  Scheduling events (admissions,
+point, where blocks run about 50 iterations on average; rounded down).  Scheduling events (admissions,
 finishes, prefill completions, preemptions) are not counted, so the fraction
 is the share of the issue peak the sweep would use if every iteration cost
 as little as a steady one.  Peak = 256 CUs x 4 SIMDs x 2.4 GHz / 4 cycles per
@@ -40,7 +40,7 @@ if ROOT not in sys.path:
 
 METRIC = "simulated requests/sec across sweep on 1 MI355X; % VALU-issue peak"
 VALU_ISSUE_PEAK = 256 * 4 * 2.4e9 / 4.0   # wave64 VALU instructions per second
-U_ITER = 9.8
+U_ITER = 9.5
 # simulation launches, 3 * stage + class (stages: one-worker points, prefill
 # devices, decode devices of disaggregated points; register-chunk classes
 # 1, 2, 4), named as rocprofv3 names the kernels

@@ -350,8 +350,9 @@ def _c8(n_req):
 def _u1(n_req):
     """Calibration of the steady path: 8192 identical points, each 64
     requests arriving together (prompt 16, output 4000) that decode side by
-    side for 4000 iterations, so almost every iteration is a steady one in a
-    full 64-iteration block."""
+    side, so almost every iteration is a steady one in a long block.  Their
+    KV does not all fit (6976 blocks of 16 tokens), so block shortages
+    preempt some of them: about 6300 iterations per point."""
     n = 64
     traces = [{"arrival_ns": np.zeros(n, np.int64), "prompt_len": np.full(n, 16, np.int32),
                "output_len": np.full(n, 4000, np.int32)}]
@@ -377,7 +378,7 @@ CONFIGS = {
                       "static} x admission ratio {off, 60%, 80%, 95%} x {24, 40} GB"),
     "c7": (_c7, 2000, "320 points x 2000 requests, 7B MHA, 16 rates x {recompute, swap "
                       "16/32/64 GB/s, swap 64 GB/s overlapped} x {20, 24} GB x {no chunk, 512}"),
-    "u1": (_u1, 64, "8192 points x 64 requests decoding together for 4000 iterations "
+    "u1": (_u1, 64, "8192 points x 64 requests decoding together, output 4000 "
                     "(calibration of the steady path)"),
     "c8": (_c8, 2000, "256 disaggregated points x 2000 requests, 7B MHA, 4 length mixes x "
                       "4 rates x P/D {1/7, 2/6, 3/5, 4/4} x 4 prefill devices, 25 GB/s KV links"),
