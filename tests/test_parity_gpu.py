@@ -370,6 +370,25 @@ def test_c5_full_sweep_sampled(S, oracle):
     assert (out["peak_used_blocks"] <= out["num_blocks"]).all()
 
 
+@pytest.mark.parametrize("name,nreq", [("c5", 2000), ("c4", 1000), ("c3", 1000)])
+def test_sweep_subsets_per_request(S, oracle, name, nreq):
+    """2048 seeded points of a large sweep at fewer requests per trace,
+    every point and every request against the oracle (both chunk classes,
+    chunked prefill, heavy preemption)."""
+    m, traces, pts = W.make_config(name, n_requests=nreq)
+    n = len(pts["peak_flops"])
+    idx = np.sort(np.random.default_rng(7).choice(n, size=min(2048, n), replace=False))
+    pts = W.subset_points(pts, idx)
+    t0 = time.time()
+    o_out, o_req = oracle.run_points(m, traces, pts, per_request=True)
+    say("%s subset: oracle %.1fs, preemptions %d" % (name, time.time() - t0,
+                                                     int(o_out["n_preempt"].sum())))
+    out, req = gpu_run(S, m, traces, pts, per_request=True, iter_cap=cap_from(o_out))
+    compare_points(out, o_out, name)
+    compare_requests(req, o_req, name)
+    assert len(set(pts["max_batch"].tolist())) > 1 or name == "c4"
+
+
 def test_determinism_and_point_order(S):
     m, traces, pts = W.make_config("c3", n_requests=300)
     n = len(pts["peak_flops"])
