@@ -187,8 +187,10 @@ __device__ __forceinline__ double rdl_f64(double v, int l) {
 
 // This lane's operator coefficients (zero above lane 6), read from LDS on
 // use rather than held in registers across the whole simulation.
+// An LDS (address space 3) pointer: reads are ds_read, not flat loads.
+typedef const volatile __attribute__((address_space(3))) double* LdsDoubles;
 struct LaneRoof {
-  const volatile double* tab;  // [4][8]: f, b0, b1, b2 per operator lane
+  LdsDoubles tab;  // [4][8]: f, b0, b1, b2 per operator lane
   int cl;                      // operator lane: min(lane, 7)
   bool is_attp, is_attd, is_lm;
   __device__ double f() const { return tab[cl]; }
@@ -1615,7 +1617,7 @@ __global__ __launch_bounds__(64, NCH == 4 ? 4 : 5) void sim_kernel(SimArgs A) {
   }
   __syncthreads();
   LaneRoof roofc;
-  roofc.tab = coef;
+  roofc.tab = (LdsDoubles)coef;
   roofc.cl = lane < 8 ? lane : 7;
   roofc.is_attp = lane == 1;
   roofc.is_attd = lane == 2;
