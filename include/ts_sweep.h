@@ -220,6 +220,12 @@ typedef struct {
  * call: TS_ERR_ARG for invalid input, TS_ERR_UNSUPPORTED when a cost-model
  * integer (a point's KV bytes, with swap) could exceed 2^53 (exact fp64) or a
  * block count exceeds 2^30.
+ * Device memory it allocates: the traces (16 B per request), the latency
+ * arrays of the percentile pass (16 B per point per request of its trace's
+ * length, padded to the longest trace), a request-time table per workgroup
+ * (24 B per request of the longest trace; the grid shrinks to keep these
+ * tables within 16 GiB), and with TS_F_PER_REQUEST the request records
+ * (40 B per point per request); TS_ERR_OOM when they do not fit.
  * On success *out receives the handle; on failure *out is NULL. */
 int ts_sweep_create(const ts_model *model, const ts_trace *traces, int32_t n_traces,
                     const ts_point *points, int32_t n_points, const ts_options *opt,
