@@ -51,7 +51,8 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "sim_kernel_traffic_c5.md")
 # the sources whose change invalidates the recorded traffic counters
 KERNEL_SOURCES = ("paper_2503_08415_amd/csrc/sim_kernel.hip",
                   "paper_2503_08415_amd/csrc/sweep_internal.h",
-                  "paper_2503_08415_amd/csrc/host.hip")
+                  "paper_2503_08415_amd/csrc/host.hip",
+                  "paper_2503_08415_amd/build.py")  # the compiler flags
 
 
 def workloads_configs():

@@ -20,6 +20,9 @@ FLAGS = [
     "-ffp-contract=off",
     # no packed fp32 instructions in device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # the ILP-first machine scheduler: fewer spills in the 256-slot kernels
+    # (about 3 % faster there, no change elsewhere)
+    "-mllvm", "-amdgpu-sched-strategy=max-ilp",
     "-Wall", "-Wno-unused-function",
 ]
 
