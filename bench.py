@@ -152,8 +152,8 @@ def main():
         print(json.dumps({"copy_calibration_bytes": args.copy_calibration, "copies": 8}))
         return
     if args.gpus != 1:
-        print("bench.py runs on one GPU: the sweep's design points are independent and this "
-              "build measures one GPU's share; --gpus %d is not supported" % args.gpus,
+        print("bench.py runs on one GPU: the sweep's design points are independent and the "
+              "benchmark measures one GPU's share; --gpus %d is not supported" % args.gpus,
               file=sys.stderr)
         sys.exit(2)
 

@@ -63,7 +63,7 @@ extern "C" {
 /* call status */
 #define TS_OK 0
 #define TS_ERR_ARG (-1)         /* invalid argument (NULL, range, unsorted trace, ...) */
-#define TS_ERR_UNSUPPORTED (-2) /* valid but outside what this build supports */
+#define TS_ERR_UNSUPPORTED (-2) /* valid but outside what the library supports */
 #define TS_ERR_OOM (-3)         /* device or host allocation failed */
 #define TS_ERR_DEVICE (-4)      /* HIP runtime error (no device, launch failure, ...) */
 #define TS_ERR_STATE (-5)       /* call out of order (results before run) */
