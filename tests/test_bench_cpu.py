@@ -51,3 +51,27 @@ def test_u1_calibration_workload_is_one_steady_batch():
     tr = t[0]
     assert (tr["arrival_ns"] == 0).all() and len(tr["arrival_ns"]) == 64
     assert (tr["output_len"] == 4000).all() and (p["max_batch"] == 64).all()
+
+
+def test_traffic_is_reported_only_for_the_profiled_sources(tmp_path, monkeypatch):
+    sys.path.insert(0, ROOT)
+    import bench
+    f = tmp_path / "traffic.md"
+    f.write_text("```\nsources-sha256: %s\ntraffic-bytes: c5 sim_kernel<4,0> 2.5e+10\n```\n"
+                 % bench.kernel_sources_sha256())
+    monkeypatch.setattr(bench, "TRAFFIC_FILE", str(f))
+    assert bench.recorded_traffic("c5", "sim_kernel<4,0>") == 2.5e10
+    assert bench.recorded_traffic("c5", "sim_kernel<1,0>") is None
+    assert bench.recorded_traffic("c6", "sim_kernel<4,0>") is None
+    # a change to a kernel source or the build flags voids the figure
+    monkeypatch.setattr(bench, "kernel_sources_sha256", lambda: "0" * 64)
+    assert bench.recorded_traffic("c5", "sim_kernel<4,0>") is None
+    monkeypatch.setattr(bench, "TRAFFIC_FILE", str(tmp_path / "missing.md"))
+    assert bench.recorded_traffic("c5", "sim_kernel<4,0>") is None
+
+
+def test_build_flags_are_part_of_the_profiled_sources():
+    sys.path.insert(0, ROOT)
+    import bench
+    assert "paper_2503_08415_amd/build.py" in bench.KERNEL_SOURCES
+    assert all(os.path.exists(os.path.join(ROOT, p)) for p in bench.KERNEL_SOURCES)
