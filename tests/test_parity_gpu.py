@@ -195,7 +195,7 @@ def test_fuzz_tiny_points(S, oracle):
              "weights_in_capacity": 0}
     rng = np.random.default_rng(2024)
     total_pre = 0
-    for rnd in range(3):
+    for rnd in range(12):
         traces, pts = _fuzz_case(rng, 1500)
         o_out, o_req = oracle.run_points(model, traces, pts, per_request=True)
         say("fuzz round %d: oracle preemptions %d" % (rnd, int(o_out["n_preempt"].sum())))
