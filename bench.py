@@ -103,12 +103,26 @@ def kernel_class(max_batch):
     return np.where(mb <= 64, 0, np.where(mb <= 128, 1, 2))
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(model, traces, points, target_s, seed=0):
-    """The oracle on a bounded, seeded sample of the same design points."""
+    """The oracle on a bounded, seeded sample of the same design points.
+
+    Returns the baseline record and (sample indices, oracle point results),
+    which the caller compares with the GPU's results for those points."""
     from oracle import tso
     from paper_2503_08415_amd import workloads
     n_points = len(points["peak_flops"])
-    cores = min(len(os.sched_getaffinity(0)), 16)
+    cores = tso.default_threads()
     rng = np.random.default_rng(seed)
     order = rng.permutation(n_points)
     # calibrate on a first slice, then size the sample to about target_s
@@ -124,10 +138,36 @@ def cpu_baseline(model, traces, points, target_s, seed=0):
     out, _ = tso.run_points(model, traces, sub, n_threads=cores)
     dt = time.perf_counter() - t0
     n_req = int(sum(len(traces[int(t)]["arrival_ns"]) for t in sub["trace_id"]))
-    return {"value": n_req / dt, "unit": "simulated requests/s", "cores": cores,
-            "kind": "oracle",
-            "sample": "%d of %d design points (seeded random), %d simulated requests, %.1f s wall"
-                      % (len(sample), n_points, n_req, dt)}
+    try:
+        affinity = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        affinity = os.cpu_count() or 1
+    rec = {"value": n_req / dt, "unit": "simulated requests/s", "cores": cores,
+           "kind": "oracle",
+           "sample": "%d of %d design points (seeded random), %d simulated requests, %.1f s wall"
+                     % (len(sample), n_points, n_req, dt),
+           "cpu_model": cpu_model(), "host_cores": os.cpu_count(), "affinity_cores": affinity,
+           "threads_note": "one thread per design point at a time, on min(affinity cores, 16)"
+                           " threads: one GPU's share of the host"}
+    return rec, (sample, out)
+
+
+def parity_of(gpu_out, sample, oracle_out):
+    """Field-by-field comparison of the GPU's point results with the
+    oracle's on the sampled points (used_block_ns within 1e-9 relative)."""
+    g = gpu_out[sample]
+    bad = np.zeros(len(sample), dtype=bool)
+    fields = []
+    for f in oracle_out.dtype.names:
+        if f == "used_block_ns":
+            ne = ~np.isclose(g[f], oracle_out[f], rtol=1e-9, atol=0.0)
+        else:
+            ne = g[f] != oracle_out[f]
+        if ne.any():
+            fields.append(f)
+        bad |= ne
+    return {"points": int(len(sample)), "mismatches": int(bad.sum()), "fields": fields,
+            "run": "the last timed step's results"}
 
 
 def main():
@@ -165,6 +205,13 @@ def main():
     model, traces, points = workloads.make_config(args.config)
     n_points = len(points["peak_flops"])
     n_req = int(sum(len(traces[int(t)]["arrival_ns"]) for t in points["trace_id"]))
+    digest = workloads.digests(model, traces, points)
+    pinned = None
+    try:
+        with open(os.path.join(ROOT, "tests", "golden", "workload_sha256.json")) as f:
+            pinned = json.load(f)["configs"].get(args.config) == digest
+    except OSError:
+        pass
     log("workload %s: %d points, %d simulated requests (generated in %.1fs)"
         % (args.config, n_points, n_req, time.perf_counter() - t0))
     sw = sweep.Sweep(model, traces, points)
@@ -228,21 +275,33 @@ def main():
                    "design_points": n_points, "simulated_requests": n_req,
                    "model": "none (simulated transformer shape)",
                    "parallelism": "one wave64 workgroup per design point"},
+        "workload_sha256": {"traces": digest["traces"], "points": digest["points"],
+                            "matches_committed": pinned},
         "roofline": roofline,
         "kernels_ms": {KERNEL_NAMES[i]: float(kmean[i]) for i in range(len(kmean))
                        if kmean[i] > 0},
         "simulation_phase_ms": float(np.mean(sim_ms)), "statistics_ms": float(np.mean(stats_ms)),
         "results_copy_ms": 1e3 * results_s,
+        "frac_step": float(w.sum()) / (ms_per_step * 1e-3) / VALU_ISSUE_PEAK,
         "simulated_iterations": int(out["n_iters"].sum()),
         "simulated_iterations_by_kernel": (
             {} if disagg else {KERNEL_NAMES[i]: int(out["n_iters"][cls == i].sum())
                                for i in range(3) if (cls == i).any()}),
         "point_status_counts": status,
     }
+    parity_ok = True
     if args.cpu_seconds > 0:
         log("cpu baseline: oracle on a sample (~%.0fs)..." % args.cpu_seconds)
-        line["cpu_baseline"] = cpu_baseline(model, traces, points, args.cpu_seconds)
+        line["cpu_baseline"], (sample, o_out) = cpu_baseline(model, traces, points,
+                                                             args.cpu_seconds)
+        line["parity"] = parity_of(out, sample, o_out)
+        parity_ok = line["parity"]["mismatches"] == 0
     print(json.dumps(line), flush=True)
+    if not parity_ok:
+        log("PARITY FAILURE: %d of %d sampled points differ from the oracle (%s)"
+            % (line["parity"]["mismatches"], line["parity"]["points"],
+               ", ".join(line["parity"]["fields"])))
+        sys.exit(1)
 
 
 if __name__ == "__main__":

@@ -225,7 +225,10 @@ typedef struct {
  * length, padded to the longest trace), a request-time table per workgroup
  * (24 B per request of the longest trace; the grid shrinks to keep these
  * tables within 16 GiB), and with TS_F_PER_REQUEST the request records
- * (40 B per point per request); TS_ERR_OOM when they do not fit.
+ * (40 B per point per request); TS_ERR_OOM, before any allocation, when
+ * their sum exceeds the device's free memory (or an allocation fails).
+ * The handle belongs to the device current at create time; every later call
+ * selects that device itself.
  * On success *out receives the handle; on failure *out is NULL. */
 int ts_sweep_create(const ts_model *model, const ts_trace *traces, int32_t n_traces,
                     const ts_point *points, int32_t n_points, const ts_options *opt,
@@ -234,7 +237,9 @@ int ts_sweep_create(const ts_model *model, const ts_trace *traces, int32_t n_tra
 /* Enqueue the whole sweep (simulation kernels, then the statistics kernel)
  * on hip_stream (a hipStream_t; NULL = the default stream).  Returns once
  * the work is enqueued.  May be called again to re-run; each run restarts
- * every point from its initial state. */
+ * every point from its initial state and replaces the previous results.  A
+ * re-run on another stream first waits (on the device) for the previous
+ * run, whose buffers it reuses. */
 int ts_sweep_run(ts_sweep *h, void *hip_stream);
 
 /* Wait for the last run and copy results to the host.  out_points receives

@@ -169,7 +169,19 @@ class _TraceKeep:
                                     o.ctypes.data_as(C.POINTER(C.c_int32)), len(a))
 
 
+def default_threads() -> int:
+    """Threads across design points: the cores this process may run on, at
+    most 16 (one GPU's share of a shared host)."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        n = os.cpu_count() or 1
+    return max(1, min(n, 16))
+
+
 def _options(iter_cap=0, slo_ttft_ns=0, slo_tpot_ns=0, n_threads=0, check_invariants=0):
+    if int(n_threads) <= 0:
+        n_threads = default_threads()
     return Options(int(iter_cap), int(slo_ttft_ns), int(slo_tpot_ns), int(n_threads),
                    int(check_invariants))
 

@@ -281,7 +281,7 @@ const char* ts_status_str(int status) {
     case TS_OK: return "ok";
     case TS_ERR_ARG: return "invalid argument";
     case TS_ERR_UNSUPPORTED: return "unsupported input (batch cap, policy, or exact-fp64 range)";
-    case TS_ERR_OOM: return "out of memory";
+    case TS_ERR_OOM: return g_err[0] ? g_err : "out of memory";
     case TS_ERR_DEVICE: return g_err[0] ? g_err : "HIP device error";
     case TS_ERR_STATE: return "call out of order";
     default: return "unknown status";
@@ -637,12 +637,34 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
   }
   const size_t per_point = (size_t)h->max_n;
   const size_t n_res = (size_t)(count + n_extra);
+  const int max_grid = std::max(1, *std::max_element(h->grid, h->grid + kLaunches));
+  {
+    // Everything the handle will hold on the device; more than the free
+    // device memory is TS_ERR_OOM before any allocation is attempted.
+    const double need =
+        (double)recs.size() * (sizeof(TraceRec) + sizeof(int32_t)) +
+        (double)dp.size() * sizeof(DevPoint) + (double)order.size() * sizeof(int32_t) +
+        (double)max_grid * (kQueueCap * sizeof(QEntry) + per_point * sizeof(ReqTimes)) +
+        (double)n_res * sizeof(ts_point_result) +
+        (double)count * (double)per_point *
+            (2.0 * sizeof(int64_t) + ((flags & TS_F_PER_REQUEST) ? sizeof(ts_req_result) : 0)) +
+        (double)aux.size() * sizeof(PdAux) +
+        (double)pd_reqs * (3 * sizeof(int64_t) + sizeof(int32_t));
+    size_t mem_free = 0, mem_total = 0;
+    e = hipMemGetInfo(&mem_free, &mem_total);
+    if (e != hipSuccess) { release(h); return device_error(e, "hipMemGetInfo"); }
+    if (need > (double)mem_free) {
+      snprintf(g_err, sizeof g_err, "the sweep needs %.3g bytes of device memory, %.3g free",
+               need, (double)mem_free);
+      release(h);
+      return TS_ERR_OOM;
+    }
+  }
   hipError_t ae = hipSuccess;
   if (ae == hipSuccess) ae = dev_alloc(&h->d_recs, recs.size());
   if (ae == hipSuccess) ae = dev_alloc(&h->d_points, dp.size());
   if (ae == hipSuccess) ae = dev_alloc(&h->d_order, order.size());
   if (ae == hipSuccess) ae = dev_alloc(&h->d_counter, (size_t)kLaunches);
-  const int max_grid = std::max(1, *std::max_element(h->grid, h->grid + kLaunches));
   if (ae == hipSuccess) ae = dev_alloc(&h->d_queue, (size_t)max_grid * kQueueCap);
   if (ae == hipSuccess) ae = dev_alloc(&h->d_times, (size_t)max_grid * per_point);
   if (ae == hipSuccess) ae = dev_alloc(&h->d_res, n_res);
@@ -686,7 +708,16 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
 int ts_sweep_run(ts_sweep* h, void* hip_stream) {
   if (!h) return TS_ERR_ARG;
   hipStream_t s = (hipStream_t)hip_stream;
-  hipError_t e = hipEventRecord(h->ev_t0, s);
+  hipError_t e = hipSetDevice(h->device);
+  if (e != hipSuccess) return device_error(e, "hipSetDevice");
+  // A re-run reuses the work-queue counters, queues, time tables and result
+  // buffers of the previous run: on another stream it must wait for that
+  // run's last kernel.
+  if (h->ran && s != h->last_stream) {
+    e = hipStreamWaitEvent(s, h->ev_t2, 0);
+    if (e != hipSuccess) return device_error(e, "stream wait");
+  }
+  e = hipEventRecord(h->ev_t0, s);
   if (e != hipSuccess) return device_error(e, "event record");
   reset_counters_kernel<<<1, 64, 0, s>>>(h->d_counter, kLaunches);
   if (h->d_req) {
@@ -773,7 +804,8 @@ int ts_sweep_results(ts_sweep* h, ts_point_result* out_points, ts_req_result* ou
   if (!h->ran) return TS_ERR_STATE;
   if (out_requests && !h->d_req) return TS_ERR_STATE;
   if (!out_points && h->n_points > 0) return TS_ERR_ARG;
-  hipError_t e = hipStreamSynchronize(h->last_stream);
+  hipError_t e = hipSetDevice(h->device);
+  if (e == hipSuccess) e = hipStreamSynchronize(h->last_stream);
   if (e != hipSuccess) return device_error(e, "stream synchronize");
   if (h->n_points > 0) {
     e = hipMemcpy(out_points, h->d_res, (size_t)h->n_points * sizeof(ts_point_result),
@@ -799,7 +831,8 @@ int ts_sweep_shape(const ts_sweep* h, int32_t* n_points, int32_t* max_n) {
 int ts_sweep_timing(ts_sweep* h, float* sim_ms, float* stats_ms) {
   if (!h || !sim_ms || !stats_ms) return TS_ERR_ARG;
   if (!h->ran) return TS_ERR_STATE;
-  hipError_t e = hipEventSynchronize(h->ev_t2);
+  hipError_t e = hipSetDevice(h->device);
+  if (e == hipSuccess) e = hipEventSynchronize(h->ev_t2);
   if (e == hipSuccess) e = hipEventElapsedTime(sim_ms, h->ev_t0, h->ev_t1);
   if (e == hipSuccess) e = hipEventElapsedTime(stats_ms, h->ev_t1, h->ev_t2);
   if (e != hipSuccess) return device_error(e, "event timing");
@@ -809,7 +842,8 @@ int ts_sweep_timing(ts_sweep* h, float* sim_ms, float* stats_ms) {
 int ts_sweep_kernel_timing(ts_sweep* h, float* ms, int32_t* n_points) {
   if (!h || !ms || !n_points) return TS_ERR_ARG;
   if (!h->ran) return TS_ERR_STATE;
-  hipError_t e = hipEventSynchronize(h->ev_t2);
+  hipError_t e = hipSetDevice(h->device);
+  if (e == hipSuccess) e = hipEventSynchronize(h->ev_t2);
   for (int c = 0; c < kLaunches && e == hipSuccess; ++c) {
     ms[c] = 0.0f;
     n_points[c] = h->class_n[c];

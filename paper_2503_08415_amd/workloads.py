@@ -32,7 +32,7 @@ import numpy as np
 
 __all__ = [
     "MODELS", "CONFIGS", "make_trace", "make_config", "POINT_FIELDS",
-    "FLOPS_GRID8", "BW_GRID8", "C4_CAPS",
+    "FLOPS_GRID8", "BW_GRID8", "C4_CAPS", "digests",
 ]
 
 # Transformer shapes (LLaMA-family layouts; the paper validates on
@@ -403,3 +403,23 @@ def subset_points(points: dict, idx) -> dict:
     """Select design points by index (same field layout)."""
     idx = np.asarray(idx, dtype=np.int64)
     return {k: np.ascontiguousarray(v[idx]) for k, v in points.items()}
+
+
+def digests(model: dict, traces, points: dict) -> dict:
+    """SHA-256 of a workload's bytes: traces (arrival int64, prompt int32,
+    output int32 per trace, little-endian, in trace order), the point grid
+    (fields in sorted order) and the model shape (sorted JSON)."""
+    import hashlib
+    import json
+    ht = hashlib.sha256()
+    for tr in traces:
+        ht.update(np.ascontiguousarray(tr["arrival_ns"], dtype="<i8").tobytes())
+        ht.update(np.ascontiguousarray(tr["prompt_len"], dtype="<i4").tobytes())
+        ht.update(np.ascontiguousarray(tr["output_len"], dtype="<i4").tobytes())
+    hp = hashlib.sha256()
+    for f in sorted(points):
+        hp.update(f.encode())
+        hp.update(np.ascontiguousarray(points[f]).tobytes())
+    hm = hashlib.sha256(json.dumps(model, sort_keys=True).encode())
+    return {"traces": ht.hexdigest(), "points": hp.hexdigest(), "model": hm.hexdigest(),
+            "n_traces": len(traces), "n_points": int(len(points["peak_flops"]))}

@@ -75,3 +75,32 @@ def test_build_flags_are_part_of_the_profiled_sources():
     import bench
     assert "paper_2503_08415_amd/build.py" in bench.KERNEL_SOURCES
     assert all(os.path.exists(os.path.join(ROOT, p)) for p in bench.KERNEL_SOURCES)
+
+
+def _manifest():
+    import json
+    with open(os.path.join(ROOT, "tests", "golden", "workload_sha256.json")) as f:
+        return json.load(f)["configs"]
+
+
+@pytest.mark.parametrize("name", sorted(W.CONFIGS))
+def test_workload_bytes_match_committed_digests(name):
+    """Every named workload generates exactly the committed bytes
+    (tests/golden/make_workload_sha256.py wrote the digests)."""
+    assert W.digests(*W.make_config(name)) == _manifest()[name]
+
+
+def test_iteration_work_unit_is_frozen_to_the_u1_calibration():
+    """U, the algorithmic VALU instructions per simulated iteration behind
+    roofline.achieved, is 9.5 and never above what the committed u1 counter
+    run measured per iteration of the cheapest path (it may only move down,
+    with a new u1 profile)."""
+    import re
+    sys.path.insert(0, ROOT)
+    import bench
+    assert bench.U_ITER == 9.5
+    with open(os.path.join(ROOT, "profiles", "sim_kernel_sq_counters_u1.md")) as f:
+        text = f.read()
+    m = re.search(r"\|\s*SQ_INSTS_VALU\s*\|\s*[0-9.e+]+\s*\|\s*([0-9.]+)\s*\|", text)
+    assert m, "the u1 profile states SQ_INSTS_VALU per simulated iteration"
+    assert bench.U_ITER <= float(m.group(1))

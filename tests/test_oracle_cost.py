@@ -183,3 +183,23 @@ def test_gqa_changes_only_attention_and_qkv(oracle):
 def test_infinitely_fast_hardware_floor(oracle):
     m = W.MODELS["gqa-7b"]
     assert oracle.iter_ns(m, 1e9 / 1e300, 1e9 / 1e300, [(2048, 30000, 1, 1)] * 4) == 1
+
+
+def test_realistic_scale_iteration_times(oracle):
+    """LLaMA2-7B on 312 TFLOP/s and 2 TB/s: a batch-1 decode, a batch-64
+    decode and a 1024-token prefill, against values computed outside this
+    repository's code (tests/golden/cost_7b_scale.json, Sec. II-A)."""
+    g = _load("cost_7b_scale.json")
+    m = W.MODELS["llama2-7b"]
+    iF = 1e9 / g["hardware"]["peak_flops"]
+    iB = 1e9 / g["hardware"]["mem_bw"]
+    for c in g["cases"]:
+        if "batch_repeat" in c:
+            row, k = c["batch_repeat"]
+            batch = [tuple(row)] * k
+        else:
+            batch = [tuple(r) for r in c["batch"]]
+        assert oracle.iter_ns(m, iF, iB, batch) == c["iter_ns"], c["name"]
+    # the batch-1 decode sits within 3 % of weights / bandwidth (Sec. II-A)
+    w = oracle.derive(m, _pt())["weight_bytes"]
+    assert abs(g["cases"][0]["iter_ns"] - w * iB) < 0.03 * w * iB

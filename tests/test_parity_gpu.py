@@ -38,7 +38,12 @@ def S():
 
 
 def gpu_run(S, model, traces, points, per_request=False, **kw):
-    kw.setdefault("point_time_limit_ms", 60_000)  # watchdog: a stuck point ends, never hangs
+    # No wall-clock watchdog by default: the same code path as the benchmark,
+    # whose steady stretches run to their first event.  Every call passes an
+    # iteration cap (from the oracle where it has run), so a scheduling bug
+    # ends as a mismatch, never as a hang.
+    assert kw.get("iter_cap", 0) > 0, "every GPU run carries an iteration cap"
+    kw.setdefault("point_time_limit_ms", 0)
     sw = S.Sweep(model, traces, points, per_request=per_request, **kw)
     try:
         sw.run()
@@ -344,21 +349,18 @@ def test_full_c4_points(S, oracle):
     compare_points(out, o_out, "c4")
 
 
-def c5_sample_index(n_points, n_sample=96, seed=5):
-    rng = np.random.default_rng(seed)
-    return np.sort(rng.choice(n_points, size=n_sample, replace=False))
-
-
-def test_c5_full_sweep_sampled(S, oracle):
-    """The full 65536-point sweep as the benchmark launches it; the oracle
-    recomputes a seeded sample of points one by one."""
+def test_c5_all_points(S, oracle):
+    """The full 65536-point x 10000-request c5 sweep, launched as the
+    benchmark launches it: every point's counters, sums, percentiles and
+    request digest against the oracle."""
     m, traces, pts = W.make_config("c5")
-    idx = c5_sample_index(len(pts["peak_flops"]))
+    n_pts = len(pts["peak_flops"])
     t0 = time.time()
-    o_out, _ = oracle.run_points(m, traces, W.subset_points(pts, idx))
-    say("c5: oracle on %d sampled points %.1fs" % (len(idx), time.time() - t0))
-    out, _ = gpu_run(S, m, traces, pts, iter_cap=cap_from(o_out) * 4)
-    compare_points(out[idx], o_out, "c5 sample")
+    o_out, _ = oracle.run_points(m, traces, pts)
+    say("c5: oracle on all %d points %.1fs (%d threads)" % (n_pts, time.time() - t0,
+                                                          oracle.default_threads()))
+    out, _ = gpu_run(S, m, traces, pts, iter_cap=cap_from(o_out))
+    compare_points(out, o_out, "c5")
     assert (out["status"] == 0).all()
     # properties that hold at any size
     n = len(traces[0]["arrival_ns"])
@@ -368,6 +370,98 @@ def test_c5_full_sweep_sampled(S, oracle):
     tr_p = np.array([int(t["prompt_len"].sum()) for t in traces])
     assert (out["prefill_tokens"] >= tr_p[pts["trace_id"]]).all()
     assert (out["peak_used_blocks"] <= out["num_blocks"]).all()
+
+
+def test_c5_full_size_per_request(S, oracle):
+    """512 seeded c5 points at the full 10000 requests: every request record."""
+    m, traces, pts = W.make_config("c5")
+    idx = np.sort(np.random.default_rng(5).choice(len(pts["peak_flops"]), 512, replace=False))
+    sub = W.subset_points(pts, idx)
+    o_out, o_req = oracle.run_points(m, traces, sub, per_request=True)
+    out, req = gpu_run(S, m, traces, sub, per_request=True, iter_cap=cap_from(o_out))
+    compare_points(out, o_out, "c5 per request")
+    compare_requests(req, o_req, "c5 per request")
+
+
+def test_rerun_same_handle_other_stream(S, oracle):
+    """One handle run twice, the second time on another stream: both runs
+    equal the oracle (the benchmark times re-runs of one handle)."""
+    import torch
+    m, traces, pts = W.make_config("c2")
+    o_out, o_req = oracle.run_points(m, traces, pts, per_request=True)
+    sw = S.Sweep(m, traces, pts, per_request=True, iter_cap=cap_from(o_out))
+    try:
+        sw.run(torch.cuda.current_stream())
+        a, ra = sw.results()
+        compare_points(a, o_out, "first run")
+        compare_requests(ra, o_req, "first run")
+        other = torch.cuda.Stream()
+        sw.run(torch.cuda.current_stream())
+        sw.run(other)  # ordered after the run before it, on the device
+        b, rb = sw.results()
+        compare_points(b, o_out, "re-run")
+        compare_requests(rb, o_req, "re-run")
+        assert a.tobytes() == b.tobytes() and ra.tobytes() == rb.tobytes()
+        sim_ms, stats_ms = sw.timing()
+        assert sim_ms > 0 and stats_ms >= 0
+    finally:
+        sw.close()
+
+
+def test_call_order_errors(S):
+    """results / timing before the first run, and request records asked of a
+    handle created without them, are TS_ERR_STATE."""
+    import ctypes as C
+    m, traces, pts = W.make_config("c1")
+    sw = S.Sweep(m, traces, pts, iter_cap=100_000)
+    try:
+        for call in (sw.results, sw.timing, sw.kernel_timing):
+            with pytest.raises(S.SweepError) as ei:
+                call()
+            assert ei.value.rc == S.TS_ERR_STATE
+        sw.run()
+        out, req = sw.results()
+        assert req is None and out["n_done"][0] == 64
+        pbuf = np.zeros(1, dtype=S.POINT_DTYPE)
+        rbuf = np.zeros((1, sw.max_n), dtype=S.REQ_DTYPE)
+        rc = S.lib().ts_sweep_results(sw._h, C.c_void_p(pbuf.ctypes.data),
+                                      C.c_void_p(rbuf.ctypes.data))
+        assert rc == S.TS_ERR_STATE
+    finally:
+        sw.close()
+
+
+def test_device_memory_shortage_is_oom(S):
+    """A sweep whose buffers exceed the device's memory fails with
+    TS_ERR_OOM at create, before any allocation; the library stays usable."""
+    m = W.MODELS["llama2-7b"]
+    n = 1_000_000
+    tr = {"arrival_ns": np.arange(n, dtype=np.int64), "prompt_len": np.full(n, 8, np.int32),
+          "output_len": np.full(n, 8, np.int32)}
+    k = 20_000  # latency arrays alone: 20000 points x 1e6 requests x 16 B = 320 GB
+    pts = {"peak_flops": np.full(k, 312e12), "mem_bw": np.full(k, 2e12),
+           "capacity_bytes": np.full(k, 80_000_000_000, np.int64),
+           "mem_util_permille": np.full(k, 900, np.int32),
+           "block_size": np.full(k, 16, np.int32), "max_batch": np.full(k, 64, np.int32),
+           "chunk_size": np.zeros(k, np.int32), "trace_id": np.zeros(k, np.int32)}
+    with pytest.raises(S.SweepError) as ei:
+        S.Sweep(m, [tr], pts, iter_cap=1)
+    assert ei.value.rc == S.TS_ERR_OOM
+    assert "device memory" in S.lib().ts_status_str(S.TS_ERR_OOM).decode()
+    m1, t1, p1 = W.make_config("c1")
+    out, _ = gpu_run(S, m1, t1, p1, iter_cap=100_000)
+    assert out["n_done"][0] == 64
+
+
+def test_watchdog_path_per_request(S, oracle):
+    """With the wall-clock watchdog on, steady stretches stop every 256
+    iterations for its clock check: the same results, request by request."""
+    m, traces, pts = W.make_config("c2")
+    o_out, o_req = oracle.run_points(m, traces, pts, per_request=True)
+    out, req = gpu_run(S, m, traces, pts, per_request=True, iter_cap=cap_from(o_out),
+                       point_time_limit_ms=60_000)
+    compare_points(out, o_out, "watchdog")
+    compare_requests(req, o_req, "watchdog")
 
 
 @pytest.mark.parametrize("name,nreq", [("c5", 2000), ("c4", 1000), ("c3", 1000)])
