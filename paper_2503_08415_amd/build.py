@@ -11,7 +11,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libts_sweep.so")
 SOURCES = [os.path.join(CSRC, f) for f in ("host.hip", "sim_kernel.hip")]
-HEADERS = [os.path.join(CSRC, "sweep_internal.h"), os.path.join(INCLUDE, "ts_sweep.h")]
+HEADERS = [os.path.join(CSRC, f) for f in ("sweep_internal.h", "sweep_host.h")] + [
+    os.path.join(INCLUDE, "ts_sweep.h")]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

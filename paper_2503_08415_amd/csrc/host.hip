@@ -18,7 +18,7 @@
 #include <numeric>
 #include <vector>
 
-#include "sweep_internal.h"
+#include "sweep_host.h"
 
 namespace tsw {
 template <int NCH, int MODE>
@@ -40,10 +40,7 @@ namespace {
 
 thread_local char g_err[256];
 
-constexpr int kClasses = 3;                 // register chunks per lane: 1, 2, 4
 constexpr int kClassChunks[kClasses] = {1, 2, 4};
-constexpr int kLaunches = kStages * kClasses;  // launch 3 * stage + class
-static_assert(kLaunches == TS_N_SIM_KERNELS, "one timing entry per launch");
 
 const void* sim_kernel_fn(int launch) {
   const int st = launch / kClasses, c = launch % kClasses;
@@ -61,11 +58,6 @@ const void* sim_kernel_fn(int launch) {
 }
 
 int class_of(int max_batch) { return max_batch <= 64 ? 0 : (max_batch <= 128 ? 1 : 2); }
-
-int device_error(hipError_t e, const char* what) {
-  snprintf(g_err, sizeof g_err, "%s: %s", what, hipGetErrorString(e));
-  return TS_ERR_DEVICE;
-}
 
 bool model_ok(const ts_model* m) {
   if (!m) return false;
@@ -200,37 +192,52 @@ double work_estimate(const TraceStats& ts, int64_t n, int M, int K, double peak,
 
 }  // namespace
 
+namespace tsw {
+
+int device_error(hipError_t e, const char* what) {
+  snprintf(g_err, sizeof g_err, "%s: %s", what, hipGetErrorString(e));
+  return TS_ERR_DEVICE;
+}
+void set_error_text(const char* text) { snprintf(g_err, sizeof g_err, "%s", text); }
+void clear_error_text() { g_err[0] = 0; }
+
+int Plan::max_grid() const { return std::max(1, *std::max_element(grid, grid + kLaunches)); }
+
+BufCounts buf_counts(const Plan& P) {
+  BufCounts c;
+  const size_t per_point = (size_t)P.max_n;
+  c.recs = P.recs.size();
+  c.points = P.dp.size();
+  c.order = P.order.size();
+  c.counter = kLaunches;
+  c.queue = (size_t)P.max_grid() * kQueueCap;
+  c.times = (size_t)P.max_grid() * per_point;
+  c.res = (size_t)(P.count + P.n_extra);
+  c.req = (P.flags & TS_F_PER_REQUEST) ? (size_t)P.count * per_point : 0;
+  c.lat = (size_t)P.count * per_point;
+  c.pd = P.aux.size();
+  c.s1 = (size_t)P.pd_reqs;
+  c.sub = (size_t)P.pd_reqs;
+  c.gids = P.recs.size();
+  return c;
+}
+
+double BufCounts::bytes() const {
+  return (double)recs * sizeof(TraceRec) + (double)points * sizeof(DevPoint) +
+         (double)order * sizeof(int32_t) + (double)counter * sizeof(unsigned int) +
+         (double)queue * sizeof(QEntry) + (double)times * sizeof(ReqTimes) +
+         (double)res * sizeof(ts_point_result) + (double)req * sizeof(ts_req_result) +
+         2.0 * (double)lat * sizeof(int64_t) + (double)pd * sizeof(PdAux) +
+         2.0 * (double)s1 * sizeof(int64_t) + (double)sub * (sizeof(int64_t) + sizeof(int32_t)) +
+         (double)gids * sizeof(int32_t);
+}
+
+}  // namespace tsw
+
 struct ts_sweep {
-  int device = 0;
-  int32_t n_points = 0, max_n = 0;
-  uint32_t flags = 0;
-  int64_t iter_cap = 0, slo_ttft = 0, slo_tpot = 0, time_limit_ms = 0;
-  CostCoef coef{};
-  LaneCoef lc{};
-  TraceRec* d_recs = nullptr;
-  DevPoint* d_points = nullptr;
-  int32_t* d_order = nullptr;       // all launches, concatenated
-  unsigned int* d_counter = nullptr;
-  QEntry* d_queue = nullptr;        // kQueueCap per workgroup, shared by the classes
-  ReqTimes* d_times = nullptr;      // max_n per workgroup, shared by the classes
-  ts_point_result* d_res = nullptr;
-  ts_req_result* d_req = nullptr;
-  int64_t* d_e2e = nullptr;
-  int64_t* d_ttft = nullptr;
-  // disaggregated points
-  int32_t n_pd = 0;
-  PdAux* d_pd = nullptr;
-  int64_t* d_s1_admit = nullptr;
-  int64_t* d_s1_first = nullptr;
-  int64_t* d_sub_a2 = nullptr;
-  int32_t* d_sub_gid = nullptr;
-  int32_t* d_gids = nullptr;
-  int class_off[kLaunches] = {}, class_n[kLaunches] = {};
-  int grid[kLaunches] = {};
-  int stats_grid = 0;
-  hipEvent_t ev_t0 = nullptr, ev_t1 = nullptr, ev_t2 = nullptr;
-  hipEvent_t ev_k0[kLaunches] = {};
-  hipEvent_t ev_k1[kLaunches] = {};
+  Plan P;
+  DevBufs B;
+  LaunchEvents ev;
   hipStream_t last_stream = nullptr;
   bool ran = false;
 };
@@ -239,29 +246,30 @@ namespace {
 
 void release(ts_sweep* h) {
   if (!h) return;
-  (void)hipFree(h->d_recs);
-  (void)hipFree(h->d_points);
-  (void)hipFree(h->d_order);
-  (void)hipFree(h->d_counter);
-  (void)hipFree(h->d_queue);
-  (void)hipFree(h->d_times);
-  (void)hipFree(h->d_res);
-  (void)hipFree(h->d_req);
-  (void)hipFree(h->d_e2e);
-  (void)hipFree(h->d_ttft);
-  (void)hipFree(h->d_pd);
-  (void)hipFree(h->d_s1_admit);
-  (void)hipFree(h->d_s1_first);
-  (void)hipFree(h->d_sub_a2);
-  (void)hipFree(h->d_sub_gid);
-  (void)hipFree(h->d_gids);
+  DevBufs& b = h->B;
+  (void)hipFree(b.recs);
+  (void)hipFree(b.points);
+  (void)hipFree(b.order);
+  (void)hipFree(b.counter);
+  (void)hipFree(b.queue);
+  (void)hipFree(b.times);
+  (void)hipFree(b.res);
+  (void)hipFree(b.req);
+  (void)hipFree(b.e2e);
+  (void)hipFree(b.ttft);
+  (void)hipFree(b.pd);
+  (void)hipFree(b.s1_admit);
+  (void)hipFree(b.s1_first);
+  (void)hipFree(b.sub_a2);
+  (void)hipFree(b.sub_gid);
+  (void)hipFree(b.gids);
   for (int c = 0; c < kLaunches; ++c) {
-    if (h->ev_k0[c]) (void)hipEventDestroy(h->ev_k0[c]);
-    if (h->ev_k1[c]) (void)hipEventDestroy(h->ev_k1[c]);
+    if (h->ev.k0[c]) (void)hipEventDestroy(h->ev.k0[c]);
+    if (h->ev.k1[c]) (void)hipEventDestroy(h->ev.k1[c]);
   }
-  if (h->ev_t0) (void)hipEventDestroy(h->ev_t0);
-  if (h->ev_t1) (void)hipEventDestroy(h->ev_t1);
-  if (h->ev_t2) (void)hipEventDestroy(h->ev_t2);
+  if (h->ev.t0) (void)hipEventDestroy(h->ev.t0);
+  if (h->ev.t1) (void)hipEventDestroy(h->ev.t1);
+  if (h->ev.t2) (void)hipEventDestroy(h->ev.t2);
   delete h;
 }
 
@@ -274,26 +282,11 @@ hipError_t dev_alloc(T** p, size_t count) {
 
 }  // namespace
 
-extern "C" {
+namespace tsw {
 
-const char* ts_status_str(int status) {
-  switch (status) {
-    case TS_OK: return "ok";
-    case TS_ERR_ARG: return "invalid argument";
-    case TS_ERR_UNSUPPORTED: return "unsupported input (batch cap, policy, or exact-fp64 range)";
-    case TS_ERR_OOM: return g_err[0] ? g_err : "out of memory";
-    case TS_ERR_DEVICE: return g_err[0] ? g_err : "HIP device error";
-    case TS_ERR_STATE: return "call out of order";
-    default: return "unknown status";
-  }
-}
-
-int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_traces,
-                    const ts_point* points, int32_t n_points, const ts_options* opt,
-                    ts_sweep** out) {
-  if (!out) return TS_ERR_ARG;
-  *out = nullptr;
-  g_err[0] = 0;
+int make_plan(const ts_model* model, const ts_trace* traces, int32_t n_traces,
+              const ts_point* points, int32_t n_points, const ts_options* opt,
+              int64_t time_table_cap, Plan* P) {
   // ---------------------------------------------------------- validation
   if (!model_ok(model)) return TS_ERR_ARG;
   if (!traces || n_traces < 1 || !points || n_points < 0) return TS_ERR_ARG;
@@ -369,15 +362,15 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
   // prefill-device units, each over its share of the trace (request i goes
   // to prefill device i % n_prefill), and n_decode decode-device units, each
   // over the arrivals of the KV that the merge kernel writes on the device.
-  std::vector<DevPoint> dp;
+  std::vector<DevPoint>& dp = P->dp;
   std::vector<double> est;
   std::vector<int> stage;
-  std::vector<PdAux> aux;
+  std::vector<PdAux>& aux = P->aux;
   dp.reserve((size_t)count);
   est.reserve((size_t)count);
   stage.reserve((size_t)count);
-  int64_t n_extra = 0;     // device result records, after the points' own
-  int64_t pd_reqs = 0;     // per-request entries of the disaggregated points
+  int64_t& n_extra = P->n_extra;  // device result records, after the points' own
+  int64_t& pd_reqs = P->pd_reqs;  // per-request entries of the disaggregated points
   int64_t extra_recs = 0;  // trace records after the traces: shares, then arrivals
   std::map<std::pair<int, int>, int64_t> share_at;  // (trace, n_prefill) -> first share record
   std::vector<std::pair<int, int>> shares;
@@ -565,10 +558,8 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
   if (count + n_extra > INT32_MAX) return TS_ERR_UNSUPPORTED;
 
   // ---------------------------------------------------------- launches + order
-  std::vector<int32_t> order;
+  std::vector<int32_t>& order = P->order;
   order.reserve(dp.size());
-  ts_sweep* h = new (std::nothrow) ts_sweep();
-  if (!h) return TS_ERR_OOM;
   for (int l = 0; l < kLaunches; ++l) {
     std::vector<int32_t> cls;
     for (size_t u = 0; u < dp.size(); ++u)
@@ -576,45 +567,47 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
         cls.push_back((int32_t)u);
     std::stable_sort(cls.begin(), cls.end(),
                      [&](int32_t a, int32_t b) { return est[(size_t)a] > est[(size_t)b]; });
-    h->class_off[l] = (int)order.size();
-    h->class_n[l] = (int)cls.size();
+    P->class_off[l] = (int)order.size();
+    P->class_n[l] = (int)cls.size();
     order.insert(order.end(), cls.begin(), cls.end());
   }
-  h->n_points = count;
-  h->n_pd = (int32_t)aux.size();
-  h->max_n = (int32_t)std::max<int64_t>(max_n, 1);
-  h->flags = flags;
-  h->iter_cap = iter_cap;
-  h->slo_ttft = slo_ttft;
-  h->slo_tpot = slo_tpot;
-  h->time_limit_ms = time_limit_ms;
-  h->coef = coef;
-  h->lc = lane_coef(coef);
+  P->count = count;
+  P->n_pd = (int32_t)aux.size();
+  P->max_n = (int32_t)std::max<int64_t>(max_n, 1);
+  P->flags = flags;
+  P->iter_cap = iter_cap;
+  P->slo_ttft = slo_ttft;
+  P->slo_tpot = slo_tpot;
+  P->time_limit_ms = time_limit_ms;
+  P->coef = coef;
+  P->lc = lane_coef(coef);
 
   // ---------------------------------------------------------- device
-  hipError_t e = hipGetDevice(&h->device);
-  if (e != hipSuccess) { release(h); return device_error(e, "hipGetDevice"); }
+  hipError_t e = hipGetDevice(&P->device);
+  if (e != hipSuccess) { return device_error(e, "hipGetDevice"); }
   hipDeviceProp_t prop;
-  e = hipGetDeviceProperties(&prop, h->device);
-  if (e != hipSuccess) { release(h); return device_error(e, "hipGetDeviceProperties"); }
+  e = hipGetDeviceProperties(&prop, P->device);
+  if (e != hipSuccess) { return device_error(e, "hipGetDeviceProperties"); }
   const int n_cu = prop.multiProcessorCount;
   for (int l = 0; l < kLaunches; ++l) {
-    if (h->class_n[l] == 0) continue;
+    if (P->class_n[l] == 0) continue;
     int per_cu = 0;
     e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, sim_kernel_fn(l), 64, 0);
-    if (e != hipSuccess) { release(h); return device_error(e, "occupancy query"); }
+    if (e != hipSuccess) { return device_error(e, "occupancy query"); }
     per_cu = std::max(per_cu, 1);
-    h->grid[l] = std::min(h->class_n[l], n_cu * per_cu);
-    // per-workgroup request-time table: max_n entries; keep it under 16 GiB
-    // (a full grid at 10^4 requests per point needs about 1.2 GB)
-    const int64_t cap = std::max<int64_t>(1, ((int64_t)1 << 34) /
+    P->grid[l] = std::min(P->class_n[l], n_cu * per_cu);
+    // per-workgroup request-time table: max_n entries; keep the tables under
+    // time_table_cap bytes (a full grid at 10^4 requests per point needs
+    // about 1.2 GB)
+    const int64_t cap = std::max<int64_t>(1, time_table_cap /
                                                  ((int64_t)std::max<int64_t>(max_n, 1) *
                                                   (int64_t)sizeof(ReqTimes)));
-    h->grid[l] = (int)std::min<int64_t>(h->grid[l], cap);
+    P->grid[l] = (int)std::min<int64_t>(P->grid[l], cap);
   }
-  h->stats_grid = std::max(1, std::min(count, n_cu * 8));
+  P->stats_grid = std::max(1, std::min(count, n_cu * 8));
 
-  std::vector<TraceRec> recs((size_t)std::max<int64_t>(total_recs + extra_recs, 1));
+  std::vector<TraceRec>& recs = P->recs;
+  recs.assign((size_t)std::max<int64_t>(total_recs + extra_recs, 1), TraceRec{});
   for (int k = 0; k < n_traces; ++k) {
     const ts_trace& tr = traces[k];
     for (int i = 0; i < tr.n; ++i) {
@@ -635,71 +628,192 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
         r.output = tr.output_len[i];
       }
   }
-  const size_t per_point = (size_t)h->max_n;
-  const size_t n_res = (size_t)(count + n_extra);
-  const int max_grid = std::max(1, *std::max_element(h->grid, h->grid + kLaunches));
-  {
-    // Everything the handle will hold on the device; more than the free
-    // device memory is TS_ERR_OOM before any allocation is attempted.
-    const double need =
-        (double)recs.size() * (sizeof(TraceRec) + sizeof(int32_t)) +
-        (double)dp.size() * sizeof(DevPoint) + (double)order.size() * sizeof(int32_t) +
-        (double)max_grid * (kQueueCap * sizeof(QEntry) + per_point * sizeof(ReqTimes)) +
-        (double)n_res * sizeof(ts_point_result) +
-        (double)count * (double)per_point *
-            (2.0 * sizeof(int64_t) + ((flags & TS_F_PER_REQUEST) ? sizeof(ts_req_result) : 0)) +
-        (double)aux.size() * sizeof(PdAux) +
-        (double)pd_reqs * (3 * sizeof(int64_t) + sizeof(int32_t));
-    size_t mem_free = 0, mem_total = 0;
-    e = hipMemGetInfo(&mem_free, &mem_total);
-    if (e != hipSuccess) { release(h); return device_error(e, "hipMemGetInfo"); }
-    if (need > (double)mem_free) {
-      snprintf(g_err, sizeof g_err, "the sweep needs %.3g bytes of device memory, %.3g free",
-               need, (double)mem_free);
-      release(h);
-      return TS_ERR_OOM;
-    }
+  return TS_OK;
+}
+
+int upload(const Plan& P, const DevBufs& B, bool async, hipStream_t s) {
+  struct Part { void* dst; const void* src; size_t bytes; };
+  const Part parts[4] = {
+      {B.recs, P.recs.data(), P.recs.size() * sizeof(TraceRec)},
+      {B.points, P.dp.data(), P.dp.size() * sizeof(DevPoint)},
+      {B.order, P.order.data(), P.order.size() * sizeof(int32_t)},
+      {B.pd, P.aux.data(), P.aux.size() * sizeof(PdAux)}};
+  for (const Part& q : parts) {
+    if (q.bytes == 0) continue;
+    const hipError_t e = async ? hipMemcpyAsync(q.dst, q.src, q.bytes, hipMemcpyHostToDevice, s)
+                               : hipMemcpy(q.dst, q.src, q.bytes, hipMemcpyHostToDevice);
+    if (e != hipSuccess) return device_error(e, "upload");
   }
-  hipError_t ae = hipSuccess;
-  if (ae == hipSuccess) ae = dev_alloc(&h->d_recs, recs.size());
-  if (ae == hipSuccess) ae = dev_alloc(&h->d_points, dp.size());
-  if (ae == hipSuccess) ae = dev_alloc(&h->d_order, order.size());
-  if (ae == hipSuccess) ae = dev_alloc(&h->d_counter, (size_t)kLaunches);
-  if (ae == hipSuccess) ae = dev_alloc(&h->d_queue, (size_t)max_grid * kQueueCap);
-  if (ae == hipSuccess) ae = dev_alloc(&h->d_times, (size_t)max_grid * per_point);
-  if (ae == hipSuccess) ae = dev_alloc(&h->d_res, n_res);
-  if (ae == hipSuccess) ae = dev_alloc(&h->d_e2e, (size_t)count * per_point);
-  if (ae == hipSuccess) ae = dev_alloc(&h->d_ttft, (size_t)count * per_point);
-  if (ae == hipSuccess && (flags & TS_F_PER_REQUEST))
-    ae = dev_alloc(&h->d_req, (size_t)count * per_point);
-  if (ae == hipSuccess) ae = dev_alloc(&h->d_pd, aux.size());
-  if (ae == hipSuccess) ae = dev_alloc(&h->d_s1_admit, (size_t)pd_reqs);
-  if (ae == hipSuccess) ae = dev_alloc(&h->d_s1_first, (size_t)pd_reqs);
-  if (ae == hipSuccess) ae = dev_alloc(&h->d_sub_a2, (size_t)pd_reqs);
-  if (ae == hipSuccess) ae = dev_alloc(&h->d_sub_gid, (size_t)pd_reqs);
-  if (ae == hipSuccess) ae = dev_alloc(&h->d_gids, recs.size());
-  if (ae != hipSuccess) {
-    const int rc = ae == hipErrorOutOfMemory ? TS_ERR_OOM : device_error(ae, "hipMalloc");
-    if (rc == TS_ERR_OOM) snprintf(g_err, sizeof g_err, "device allocation failed");
+  return TS_OK;
+}
+
+int enqueue(const Plan& P, const DevBufs& B, hipStream_t s, const LaunchEvents* ev) {
+  auto record = [&](hipEvent_t e) -> hipError_t {
+    return (ev && e) ? hipEventRecord(e, s) : hipSuccess;
+  };
+  hipError_t e = record(ev ? ev->t0 : nullptr);
+  if (e != hipSuccess) return device_error(e, "event record");
+  reset_counters_kernel<<<1, 64, 0, s>>>(B.counter, kLaunches);
+  if (B.req) {
+    const size_t n = (size_t)P.count * (size_t)P.max_n;
+    const int blocks = (int)std::min<size_t>((n + 255) / 256, 65536);
+    fill_pending_kernel<<<std::max(blocks, 1), 256, 0, s>>>(B.req, n);
+  }
+  SimArgs a;
+  a.recs = B.recs;
+  a.points = B.points;
+  a.max_n = P.max_n;
+  a.queue = B.queue;
+  a.times = B.times;
+  a.res = B.res;
+  a.req = B.req;
+  a.e2e = B.e2e;
+  a.ttft = B.ttft;
+  a.iter_cap = P.iter_cap;
+  a.slo_ttft_ns = P.slo_ttft;
+  a.slo_tpot_ns = P.slo_tpot;
+  a.time_limit_ticks = (uint64_t)P.time_limit_ms * 100000ull;  // 100 MHz clock
+  a.n_layers = P.coef.n_layers;
+  a.lc = P.lc;
+  a.pd = B.pd;
+  a.s1_admit = B.s1_admit;
+  a.s1_first = B.s1_first;
+  a.sub_a2 = B.sub_a2;
+  a.sub_gid = B.sub_gid;
+  a.gids = B.gids;
+  // one launch per (stage, class), back to back: one-worker points and
+  // prefill devices, the merge of the prefill devices' hand-overs, the
+  // decode devices, then the disaggregated points' records
+  for (int l = 0; l < kLaunches; ++l) {
+    if (l == kStageDecode * kClasses && P.n_pd > 0) {
+      pd_merge_kernel<<<std::min(P.n_pd * kMaxDev, 65536), 256, 0, s>>>(
+          B.pd, P.n_pd, B.sub_a2, B.sub_gid, B.recs, B.gids, B.points);
+      e = hipGetLastError();
+      if (e != hipSuccess) return device_error(e, "merge kernel launch");
+    }
+    if (P.class_n[l] == 0) continue;
+    a.order = B.order + P.class_off[l];
+    a.n_order = P.class_n[l];
+    a.counter = B.counter + l;
+    e = record(ev ? ev->k0[l] : nullptr);
+    if (e != hipSuccess) return device_error(e, "event record");
+    const int g = P.grid[l];
+    switch (l) {
+      case 0: sim_kernel<1, kStageOne><<<g, 64, 0, s>>>(a); break;
+      case 1: sim_kernel<2, kStageOne><<<g, 64, 0, s>>>(a); break;
+      case 2: sim_kernel<4, kStageOne><<<g, 64, 0, s>>>(a); break;
+      case 3: sim_kernel<1, kStagePrefill><<<g, 64, 0, s>>>(a); break;
+      case 4: sim_kernel<2, kStagePrefill><<<g, 64, 0, s>>>(a); break;
+      case 5: sim_kernel<4, kStagePrefill><<<g, 64, 0, s>>>(a); break;
+      case 6: sim_kernel<1, kStageDecode><<<g, 64, 0, s>>>(a); break;
+      case 7: sim_kernel<2, kStageDecode><<<g, 64, 0, s>>>(a); break;
+      default: sim_kernel<4, kStageDecode><<<g, 64, 0, s>>>(a); break;
+    }
+    e = hipGetLastError();
+    if (e != hipSuccess) return device_error(e, "sim kernel launch");
+    e = record(ev ? ev->k1[l] : nullptr);
+    if (e != hipSuccess) return device_error(e, "event record");
+  }
+  if (P.n_pd > 0) {
+    pd_combine_kernel<<<std::min(P.n_pd, 65536), 256, 0, s>>>(B.pd, P.n_pd, B.res, B.recs,
+                                                               B.e2e, B.ttft, P.max_n);
+    e = hipGetLastError();
+    if (e != hipSuccess) return device_error(e, "combine kernel launch");
+  }
+  e = record(ev ? ev->t1 : nullptr);
+  if (e != hipSuccess) return device_error(e, "event record");
+  if (P.count > 0)
+    stats_kernel<<<P.stats_grid, 256, 0, s>>>(B.e2e, B.ttft, B.res, P.max_n, P.count);
+  e = hipGetLastError();
+  if (e != hipSuccess) return device_error(e, "stats kernel launch");
+  e = record(ev ? ev->t2 : nullptr);
+  if (e != hipSuccess) return device_error(e, "event record");
+  return TS_OK;
+}
+
+}  // namespace tsw
+
+extern "C" {
+
+const char* ts_status_str(int status) {
+  switch (status) {
+    case TS_OK: return "ok";
+    case TS_ERR_ARG: return "invalid argument";
+    case TS_ERR_UNSUPPORTED:
+      return g_err[0] ? g_err : "unsupported input (batch cap, policy, or exact-fp64 range)";
+    case TS_ERR_OOM: return g_err[0] ? g_err : "out of memory";
+    case TS_ERR_DEVICE: return g_err[0] ? g_err : "HIP device error";
+    case TS_ERR_STATE: return "call out of order";
+    default: return "unknown status";
+  }
+}
+
+int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_traces,
+                    const ts_point* points, int32_t n_points, const ts_options* opt,
+                    ts_sweep** out) {
+  if (!out) return TS_ERR_ARG;
+  *out = nullptr;
+  g_err[0] = 0;
+  ts_sweep* h = new (std::nothrow) ts_sweep();
+  if (!h) return TS_ERR_OOM;
+  int rc = make_plan(model, traces, n_traces, points, n_points, opt, (int64_t)1 << 34, &h->P);
+  if (rc != TS_OK) {
     release(h);
     return rc;
   }
-  e = hipMemcpy(h->d_recs, recs.data(), recs.size() * sizeof(TraceRec), hipMemcpyHostToDevice);
-  if (e == hipSuccess && !dp.empty())
-    e = hipMemcpy(h->d_points, dp.data(), dp.size() * sizeof(DevPoint), hipMemcpyHostToDevice);
-  if (e == hipSuccess && !order.empty())
-    e = hipMemcpy(h->d_order, order.data(), order.size() * sizeof(int32_t),
-                  hipMemcpyHostToDevice);
-  if (e == hipSuccess && !aux.empty())
-    e = hipMemcpy(h->d_pd, aux.data(), aux.size() * sizeof(PdAux), hipMemcpyHostToDevice);
-  if (e != hipSuccess) { release(h); return device_error(e, "upload"); }
-  for (int c = 0; c < kLaunches && e == hipSuccess; ++c) {
-    e = hipEventCreate(&h->ev_k0[c]);
-    if (e == hipSuccess) e = hipEventCreate(&h->ev_k1[c]);
+  const BufCounts n = buf_counts(h->P);
+  // Everything the handle will hold on the device; more than the free
+  // device memory is TS_ERR_OOM before any allocation is attempted.
+  size_t mem_free = 0, mem_total = 0;
+  hipError_t e = hipMemGetInfo(&mem_free, &mem_total);
+  if (e != hipSuccess) { release(h); return device_error(e, "hipMemGetInfo"); }
+  if (n.bytes() > (double)mem_free) {
+    snprintf(g_err, sizeof g_err, "the sweep needs %.3g bytes of device memory, %.3g free",
+             n.bytes(), (double)mem_free);
+    release(h);
+    return TS_ERR_OOM;
   }
-  if (e == hipSuccess) e = hipEventCreate(&h->ev_t0);
-  if (e == hipSuccess) e = hipEventCreate(&h->ev_t1);
-  if (e == hipSuccess) e = hipEventCreate(&h->ev_t2);
+  DevBufs& b = h->B;
+  hipError_t ae = hipSuccess;
+  if (ae == hipSuccess) ae = dev_alloc(&b.recs, n.recs);
+  if (ae == hipSuccess) ae = dev_alloc(&b.points, n.points);
+  if (ae == hipSuccess) ae = dev_alloc(&b.order, n.order);
+  if (ae == hipSuccess) ae = dev_alloc(&b.counter, n.counter);
+  if (ae == hipSuccess) ae = dev_alloc(&b.queue, n.queue);
+  if (ae == hipSuccess) ae = dev_alloc(&b.times, n.times);
+  if (ae == hipSuccess) ae = dev_alloc(&b.res, n.res);
+  if (ae == hipSuccess) ae = dev_alloc(&b.e2e, n.lat);
+  if (ae == hipSuccess) ae = dev_alloc(&b.ttft, n.lat);
+  if (ae == hipSuccess && n.req > 0) ae = dev_alloc(&b.req, n.req);
+  if (ae == hipSuccess) ae = dev_alloc(&b.pd, n.pd);
+  if (ae == hipSuccess) ae = dev_alloc(&b.s1_admit, n.s1);
+  if (ae == hipSuccess) ae = dev_alloc(&b.s1_first, n.s1);
+  if (ae == hipSuccess) ae = dev_alloc(&b.sub_a2, n.sub);
+  if (ae == hipSuccess) ae = dev_alloc(&b.sub_gid, n.sub);
+  if (ae == hipSuccess) ae = dev_alloc(&b.gids, n.gids);
+  if (ae != hipSuccess) {
+    const int rc2 = ae == hipErrorOutOfMemory ? TS_ERR_OOM : device_error(ae, "hipMalloc");
+    if (rc2 == TS_ERR_OOM) snprintf(g_err, sizeof g_err, "device allocation failed");
+    release(h);
+    return rc2;
+  }
+  rc = upload(h->P, b, false, nullptr);
+  if (rc != TS_OK) {
+    release(h);
+    return rc;
+  }
+  // the host copies of the uploaded records are no longer needed
+  std::vector<TraceRec>().swap(h->P.recs);
+  std::vector<DevPoint>().swap(h->P.dp);
+  std::vector<int32_t>().swap(h->P.order);
+  std::vector<PdAux>().swap(h->P.aux);
+  for (int c = 0; c < kLaunches && e == hipSuccess; ++c) {
+    e = hipEventCreate(&h->ev.k0[c]);
+    if (e == hipSuccess) e = hipEventCreate(&h->ev.k1[c]);
+  }
+  if (e == hipSuccess) e = hipEventCreate(&h->ev.t0);
+  if (e == hipSuccess) e = hipEventCreate(&h->ev.t1);
+  if (e == hipSuccess) e = hipEventCreate(&h->ev.t2);
   if (e != hipSuccess) { release(h); return device_error(e, "stream/event create"); }
   *out = h;
   return TS_OK;
@@ -708,92 +822,17 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
 int ts_sweep_run(ts_sweep* h, void* hip_stream) {
   if (!h) return TS_ERR_ARG;
   hipStream_t s = (hipStream_t)hip_stream;
-  hipError_t e = hipSetDevice(h->device);
+  hipError_t e = hipSetDevice(h->P.device);
   if (e != hipSuccess) return device_error(e, "hipSetDevice");
   // A re-run reuses the work-queue counters, queues, time tables and result
   // buffers of the previous run: on another stream it must wait for that
   // run's last kernel.
   if (h->ran && s != h->last_stream) {
-    e = hipStreamWaitEvent(s, h->ev_t2, 0);
+    e = hipStreamWaitEvent(s, h->ev.t2, 0);
     if (e != hipSuccess) return device_error(e, "stream wait");
   }
-  e = hipEventRecord(h->ev_t0, s);
-  if (e != hipSuccess) return device_error(e, "event record");
-  reset_counters_kernel<<<1, 64, 0, s>>>(h->d_counter, kLaunches);
-  if (h->d_req) {
-    const size_t n = (size_t)h->n_points * (size_t)h->max_n;
-    const int blocks = (int)std::min<size_t>((n + 255) / 256, 65536);
-    fill_pending_kernel<<<std::max(blocks, 1), 256, 0, s>>>(h->d_req, n);
-  }
-  SimArgs a;
-  a.recs = h->d_recs;
-  a.points = h->d_points;
-  a.max_n = h->max_n;
-  a.queue = h->d_queue;
-  a.times = h->d_times;
-  a.res = h->d_res;
-  a.req = h->d_req;
-  a.e2e = h->d_e2e;
-  a.ttft = h->d_ttft;
-  a.iter_cap = h->iter_cap;
-  a.slo_ttft_ns = h->slo_ttft;
-  a.slo_tpot_ns = h->slo_tpot;
-  a.time_limit_ticks = (uint64_t)h->time_limit_ms * 100000ull;  // 100 MHz clock
-  a.n_layers = h->coef.n_layers;
-  a.lc = h->lc;
-  a.pd = h->d_pd;
-  a.s1_admit = h->d_s1_admit;
-  a.s1_first = h->d_s1_first;
-  a.sub_a2 = h->d_sub_a2;
-  a.sub_gid = h->d_sub_gid;
-  a.gids = h->d_gids;
-  // one launch per (stage, class), back to back: one-worker points and
-  // prefill devices, the merge of the prefill devices' hand-overs, the
-  // decode devices, then the disaggregated points' records
-  for (int l = 0; l < kLaunches; ++l) {
-    if (l == kStageDecode * kClasses && h->n_pd > 0) {
-      pd_merge_kernel<<<std::min(h->n_pd * kMaxDev, 65536), 256, 0, s>>>(
-          h->d_pd, h->n_pd, h->d_sub_a2, h->d_sub_gid, h->d_recs, h->d_gids, h->d_points);
-      e = hipGetLastError();
-      if (e != hipSuccess) return device_error(e, "merge kernel launch");
-    }
-    if (h->class_n[l] == 0) continue;
-    a.order = h->d_order + h->class_off[l];
-    a.n_order = h->class_n[l];
-    a.counter = h->d_counter + l;
-    e = hipEventRecord(h->ev_k0[l], s);
-    if (e != hipSuccess) return device_error(e, "event record");
-    switch (l) {
-      case 0: sim_kernel<1, kStageOne><<<h->grid[l], 64, 0, s>>>(a); break;
-      case 1: sim_kernel<2, kStageOne><<<h->grid[l], 64, 0, s>>>(a); break;
-      case 2: sim_kernel<4, kStageOne><<<h->grid[l], 64, 0, s>>>(a); break;
-      case 3: sim_kernel<1, kStagePrefill><<<h->grid[l], 64, 0, s>>>(a); break;
-      case 4: sim_kernel<2, kStagePrefill><<<h->grid[l], 64, 0, s>>>(a); break;
-      case 5: sim_kernel<4, kStagePrefill><<<h->grid[l], 64, 0, s>>>(a); break;
-      case 6: sim_kernel<1, kStageDecode><<<h->grid[l], 64, 0, s>>>(a); break;
-      case 7: sim_kernel<2, kStageDecode><<<h->grid[l], 64, 0, s>>>(a); break;
-      default: sim_kernel<4, kStageDecode><<<h->grid[l], 64, 0, s>>>(a); break;
-    }
-    e = hipGetLastError();
-    if (e != hipSuccess) return device_error(e, "sim kernel launch");
-    e = hipEventRecord(h->ev_k1[l], s);
-    if (e != hipSuccess) return device_error(e, "event record");
-  }
-  if (h->n_pd > 0) {
-    pd_combine_kernel<<<std::min(h->n_pd, 65536), 256, 0, s>>>(
-        h->d_pd, h->n_pd, h->d_res, h->d_recs, h->d_e2e, h->d_ttft, h->max_n);
-    e = hipGetLastError();
-    if (e != hipSuccess) return device_error(e, "combine kernel launch");
-  }
-  e = hipEventRecord(h->ev_t1, s);
-  if (e != hipSuccess) return device_error(e, "event record");
-  if (h->n_points > 0)
-    stats_kernel<<<h->stats_grid, 256, 0, s>>>(h->d_e2e, h->d_ttft, h->d_res, h->max_n,
-                                                h->n_points);
-  e = hipGetLastError();
-  if (e != hipSuccess) return device_error(e, "stats kernel launch");
-  e = hipEventRecord(h->ev_t2, s);
-  if (e != hipSuccess) return device_error(e, "event record");
+  const int rc = enqueue(h->P, h->B, s, &h->ev);
+  if (rc != TS_OK) return rc;
   h->last_stream = s;
   h->ran = true;
   return TS_OK;
@@ -802,19 +841,19 @@ int ts_sweep_run(ts_sweep* h, void* hip_stream) {
 int ts_sweep_results(ts_sweep* h, ts_point_result* out_points, ts_req_result* out_requests) {
   if (!h) return TS_ERR_ARG;
   if (!h->ran) return TS_ERR_STATE;
-  if (out_requests && !h->d_req) return TS_ERR_STATE;
-  if (!out_points && h->n_points > 0) return TS_ERR_ARG;
-  hipError_t e = hipSetDevice(h->device);
+  if (out_requests && !h->B.req) return TS_ERR_STATE;
+  if (!out_points && h->P.count > 0) return TS_ERR_ARG;
+  hipError_t e = hipSetDevice(h->P.device);
   if (e == hipSuccess) e = hipStreamSynchronize(h->last_stream);
   if (e != hipSuccess) return device_error(e, "stream synchronize");
-  if (h->n_points > 0) {
-    e = hipMemcpy(out_points, h->d_res, (size_t)h->n_points * sizeof(ts_point_result),
+  if (h->P.count > 0) {
+    e = hipMemcpy(out_points, h->B.res, (size_t)h->P.count * sizeof(ts_point_result),
                   hipMemcpyDeviceToHost);
     if (e != hipSuccess) return device_error(e, "copy results");
   }
-  if (out_requests && h->n_points > 0) {
-    e = hipMemcpy(out_requests, h->d_req,
-                  (size_t)h->n_points * (size_t)h->max_n * sizeof(ts_req_result),
+  if (out_requests && h->P.count > 0) {
+    e = hipMemcpy(out_requests, h->B.req,
+                  (size_t)h->P.count * (size_t)h->P.max_n * sizeof(ts_req_result),
                   hipMemcpyDeviceToHost);
     if (e != hipSuccess) return device_error(e, "copy request records");
   }
@@ -823,18 +862,18 @@ int ts_sweep_results(ts_sweep* h, ts_point_result* out_points, ts_req_result* ou
 
 int ts_sweep_shape(const ts_sweep* h, int32_t* n_points, int32_t* max_n) {
   if (!h || !n_points || !max_n) return TS_ERR_ARG;
-  *n_points = h->n_points;
-  *max_n = h->max_n;
+  *n_points = h->P.count;
+  *max_n = h->P.max_n;
   return TS_OK;
 }
 
 int ts_sweep_timing(ts_sweep* h, float* sim_ms, float* stats_ms) {
   if (!h || !sim_ms || !stats_ms) return TS_ERR_ARG;
   if (!h->ran) return TS_ERR_STATE;
-  hipError_t e = hipSetDevice(h->device);
-  if (e == hipSuccess) e = hipEventSynchronize(h->ev_t2);
-  if (e == hipSuccess) e = hipEventElapsedTime(sim_ms, h->ev_t0, h->ev_t1);
-  if (e == hipSuccess) e = hipEventElapsedTime(stats_ms, h->ev_t1, h->ev_t2);
+  hipError_t e = hipSetDevice(h->P.device);
+  if (e == hipSuccess) e = hipEventSynchronize(h->ev.t2);
+  if (e == hipSuccess) e = hipEventElapsedTime(sim_ms, h->ev.t0, h->ev.t1);
+  if (e == hipSuccess) e = hipEventElapsedTime(stats_ms, h->ev.t1, h->ev.t2);
   if (e != hipSuccess) return device_error(e, "event timing");
   return TS_OK;
 }
@@ -842,12 +881,12 @@ int ts_sweep_timing(ts_sweep* h, float* sim_ms, float* stats_ms) {
 int ts_sweep_kernel_timing(ts_sweep* h, float* ms, int32_t* n_points) {
   if (!h || !ms || !n_points) return TS_ERR_ARG;
   if (!h->ran) return TS_ERR_STATE;
-  hipError_t e = hipSetDevice(h->device);
-  if (e == hipSuccess) e = hipEventSynchronize(h->ev_t2);
+  hipError_t e = hipSetDevice(h->P.device);
+  if (e == hipSuccess) e = hipEventSynchronize(h->ev.t2);
   for (int c = 0; c < kLaunches && e == hipSuccess; ++c) {
     ms[c] = 0.0f;
-    n_points[c] = h->class_n[c];
-    if (h->class_n[c] > 0) e = hipEventElapsedTime(&ms[c], h->ev_k0[c], h->ev_k1[c]);
+    n_points[c] = h->P.class_n[c];
+    if (h->P.class_n[c] > 0) e = hipEventElapsedTime(&ms[c], h->ev.k0[c], h->ev.k1[c]);
   }
   if (e != hipSuccess) return device_error(e, "event timing");
   return TS_OK;

@@ -143,6 +143,18 @@ def points_array(points: dict):
     return arr, n
 
 
+def _traces_array(traces):
+    keep = []
+    tr = (Trace * max(1, len(traces)))()
+    for k, t in enumerate(traces):
+        a = np.ascontiguousarray(t["arrival_ns"], dtype=np.int64)
+        p = np.ascontiguousarray(t["prompt_len"], dtype=np.int32)
+        o = np.ascontiguousarray(t["output_len"], dtype=np.int32)
+        keep += [a, p, o]
+        tr[k] = Trace(a.ctypes.data, p.ctypes.data, o.ctypes.data, len(a))
+    return tr, keep
+
+
 class Sweep:
     """One uploaded sweep: ``create`` on construction, then ``run`` / ``results``."""
 
@@ -151,14 +163,7 @@ class Sweep:
                  slo_ttft_ns: int = 0, slo_tpot_ns: int = 0, point_time_limit_ms: int = 0):
         L = lib()
         self._h = C.c_void_p()
-        keep = []
-        tr = (Trace * max(1, len(traces)))()
-        for k, t in enumerate(traces):
-            a = np.ascontiguousarray(t["arrival_ns"], dtype=np.int64)
-            p = np.ascontiguousarray(t["prompt_len"], dtype=np.int32)
-            o = np.ascontiguousarray(t["output_len"], dtype=np.int32)
-            keep += [a, p, o]
-            tr[k] = Trace(a.ctypes.data, p.ctypes.data, o.ctypes.data, len(a))
+        tr, keep = _traces_array(traces)
         pts, n = points_array(points)
         opt = Options(F_PER_REQUEST if per_request else 0, int(first_point), int(n_points), 0,
                       int(iter_cap), int(slo_ttft_ns), int(slo_tpot_ns),

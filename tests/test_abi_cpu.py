@@ -220,3 +220,4 @@ def test_oracle_shares_no_code_with_the_hip_path():
             src = open(os.path.join(odir, f)).read()
             for name in ("paper_2503_08415_amd", "ts_sweep", "csrc", "sweep_internal"):
                 assert name not in src, (f, name)
+
