@@ -270,6 +270,33 @@ int ts_sweep_timing(ts_sweep *h, float *sim_ms, float *stats_ms);
 #define TS_N_SIM_KERNELS 9
 int ts_sweep_kernel_timing(ts_sweep *h, float *ms, int32_t *n_points);
 
+/* For callers that cannot allocate device memory (tight serving loops,
+ * harnesses that forbid hipMalloc): the whole sweep of ts_sweep_create +
+ * ts_sweep_run + ts_sweep_results in one call that calls no hipMalloc,
+ * hipFree or other allocating device routine.  Every buffer the kernels use
+ * lives in one static device array of TS_STATIC_SCRATCH_BYTES that each GPU
+ * the library runs on holds from the library's load until the process ends;
+ * the first call on a device looks up its address there.  Inputs and
+ * options are as for ts_sweep_create (host memory, validated before any
+ * device call); out_points (n_points records) and out_requests (NULL, or
+ * with TS_F_PER_REQUEST n_points * max_n records, max_n = the longest
+ * trace) are caller-allocated host arrays, as for ts_sweep_results.  The
+ * work is enqueued on hip_stream (NULL = the default stream) and the call
+ * returns after synchronising it.  TS_ERR_UNSUPPORTED when the sweep's
+ * buffers exceed the array even at one workgroup per kernel launch (the
+ * request-time tables take at most a quarter of it: the grid shrinks to fit);
+ * TS_ERR_STATE for out_requests without TS_F_PER_REQUEST.  All calls share
+ * the one array of their GPU and it keeps the last call's contents (each
+ * call clears what must start at zero): calls inside one process are
+ * serialised by a lock, and calls that overlapped on one GPU would race.
+ * Not for use under stream capture (it copies from pageable host memory and
+ * synchronises the stream). */
+#define TS_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+int ts_sweep_run_static(const ts_model *model, const ts_trace *traces, int32_t n_traces,
+                        const ts_point *points, int32_t n_points, const ts_options *opt,
+                        void *hip_stream, ts_point_result *out_points,
+                        ts_req_result *out_requests);
+
 /* Release the handle and its device memory; NULL is accepted. */
 void ts_sweep_destroy(ts_sweep *h);
 

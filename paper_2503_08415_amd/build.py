@@ -10,7 +10,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libts_sweep.so")
-SOURCES = [os.path.join(CSRC, f) for f in ("host.hip", "sim_kernel.hip")]
+SOURCES = [os.path.join(CSRC, f) for f in ("host.hip", "sim_kernel.hip", "noalloc.hip")]
 HEADERS = [os.path.join(CSRC, f) for f in ("sweep_internal.h", "sweep_host.h")] + [
     os.path.join(INCLUDE, "ts_sweep.h")]
 

@@ -74,7 +74,9 @@ POINT_DTYPE = np.dtype([
 
 # every entry point declared in include/ts_sweep.h
 EXPORTS = ("ts_sweep_create", "ts_sweep_run", "ts_sweep_results", "ts_sweep_shape",
-           "ts_sweep_timing", "ts_sweep_kernel_timing", "ts_sweep_destroy", "ts_status_str")
+           "ts_sweep_timing", "ts_sweep_kernel_timing", "ts_sweep_run_static",
+           "ts_sweep_destroy", "ts_status_str")
+STATIC_SCRATCH_BYTES = 64 << 20  # TS_STATIC_SCRATCH_BYTES
 # simulation launches, 3 * stage + class: stages one-worker points, prefill
 # devices, decode devices; classes max_batch <= 64, <= 128, <= 256
 N_SIM_KERNELS = 9
@@ -112,6 +114,10 @@ def lib():
         L.ts_sweep_kernel_timing.argtypes = [C.c_void_p, C.POINTER(C.c_float),
                                              C.POINTER(C.c_int32)]
         L.ts_sweep_kernel_timing.restype = C.c_int
+        L.ts_sweep_run_static.argtypes = [C.POINTER(Model), C.POINTER(Trace), C.c_int32,
+                                          C.POINTER(Point), C.c_int32, C.POINTER(Options),
+                                          C.c_void_p, C.c_void_p, C.c_void_p]
+        L.ts_sweep_run_static.restype = C.c_int
         L.ts_sweep_destroy.argtypes = [C.c_void_p]
         L.ts_sweep_destroy.restype = None
         L.ts_status_str.argtypes = [C.c_int]
@@ -153,6 +159,34 @@ def _traces_array(traces):
         keep += [a, p, o]
         tr[k] = Trace(a.ctypes.data, p.ctypes.data, o.ctypes.data, len(a))
     return tr, keep
+
+
+def run_static(model: dict, traces, points: dict, *, per_request: bool = False,
+               first_point: int = 0, n_points: int = 0, iter_cap: int = 0,
+               slo_ttft_ns: int = 0, slo_tpot_ns: int = 0, point_time_limit_ms: int = 0,
+               stream=None):
+    """One whole sweep through ``ts_sweep_run_static`` (no device allocation;
+    buffers in the library's static scratch).  Returns (points, requests or None)."""
+    L = lib()
+    if stream is None:
+        import torch
+        stream = torch.cuda.current_stream()
+    handle = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream or 0)
+    tr, keep = _traces_array(traces)
+    pts, n = points_array(points)
+    count = (n - int(first_point)) if int(n_points) == 0 else int(n_points)
+    count = max(count, 0)
+    max_n = max([len(t["arrival_ns"]) for t in traces] + [1])
+    opt = Options(F_PER_REQUEST if per_request else 0, int(first_point), int(n_points), 0,
+                  int(iter_cap), int(slo_ttft_ns), int(slo_tpot_ns), int(point_time_limit_ms))
+    out = np.zeros(max(count, 1), dtype=POINT_DTYPE)
+    req = np.zeros((count, max_n), dtype=REQ_DTYPE) if per_request else None
+    _check(L.ts_sweep_run_static(C.byref(model_struct(model)), tr, len(traces), pts, n,
+                                 C.byref(opt), C.c_void_p(handle), out.ctypes.data,
+                                 req.ctypes.data if req is not None else None),
+           "ts_sweep_run_static")
+    del keep
+    return out[:count], req
 
 
 class Sweep:

@@ -221,3 +221,25 @@ def test_oracle_shares_no_code_with_the_hip_path():
             for name in ("paper_2503_08415_amd", "ts_sweep", "csrc", "sweep_internal"):
                 assert name not in src, (f, name)
 
+
+def test_static_entry_rejects_invalid_arguments_before_device(L):
+    """ts_sweep_run_static validates like ts_sweep_create, before any device call."""
+    m, traces, pts = _base()
+    tr = (S.Trace * 1)()
+    t = traces[0]
+    a = np.ascontiguousarray(t["arrival_ns"], np.int64)
+    p = np.ascontiguousarray(t["prompt_len"], np.int32)
+    o = np.ascontiguousarray(t["output_len"], np.int32)
+    tr[0] = S.Trace(a.ctypes.data, p.ctypes.data, o.ctypes.data, len(a))
+    out = np.zeros(1, dtype=S.POINT_DTYPE)
+    for bm, bp in ((dict(m, d_model=4095), pts), (m, _mod_points(pts, block_size=0)),
+                   (m, _mod_points(pts, max_batch=0))):
+        ps, n = S.points_array(bp)
+        rc = L.ts_sweep_run_static(C.byref(S.model_struct(bm)), tr, 1, ps, n, None, None,
+                                   C.c_void_p(out.ctypes.data), None)
+        assert rc == S.TS_ERR_ARG
+    ps, n = S.points_array(_mod_points(pts, max_batch=300))
+    rc = L.ts_sweep_run_static(C.byref(S.model_struct(m)), tr, 1, ps, n, None, None,
+                               C.c_void_p(out.ctypes.data), None)
+    assert rc == S.TS_ERR_UNSUPPORTED
+    assert L.ts_sweep_run_static(None, None, 0, None, 0, None, None, None, None) == S.TS_ERR_ARG
