@@ -27,10 +27,11 @@ __global__ void pd_merge_kernel(const PdAux* aux, int n_aux, const int64_t* sub_
                                 const int32_t* sub_gid, TraceRec* recs, int32_t* gids,
                                 DevPoint* units);
 __global__ void pd_combine_kernel(const PdAux* aux, int n_aux, ts_point_result* res,
-                                  const TraceRec* recs, int64_t* e2e, int64_t* ttft, int max_n);
-__global__ void stats_kernel(const int64_t* e2e, const int64_t* ttft, ts_point_result* res,
-                             int max_n, int n_points);
-__global__ void fill_pending_kernel(ts_req_result* r, size_t n);
+                                  const TraceRec* recs);
+__global__ void stats_kernel(ts_req_result* rec, const TraceRec* recs, const PointInfo* pinfo,
+                             ts_point_result* res, int64_t* e2e, int64_t* ttft, int max_n,
+                             int n_points, int64_t slo_ttft_ns, int64_t slo_tpot_ns,
+                             int pad_pending);
 __global__ void reset_counters_kernel(unsigned int* c, int n);
 }  // namespace tsw
 
@@ -213,7 +214,8 @@ BufCounts buf_counts(const Plan& P) {
   c.queue = (size_t)P.max_grid() * kQueueCap;
   c.times = (size_t)P.max_grid() * per_point;
   c.res = (size_t)(P.count + P.n_extra);
-  c.req = (P.flags & TS_F_PER_REQUEST) ? (size_t)P.count * per_point : 0;
+  c.req = (size_t)P.count * per_point;  // the request records (always)
+  c.pinfo = P.pinfo.size();
   c.lat = (size_t)P.count * per_point;
   c.pd = P.aux.size();
   c.s1 = (size_t)P.pd_reqs;
@@ -229,7 +231,7 @@ double BufCounts::bytes() const {
          (double)res * sizeof(ts_point_result) + (double)req * sizeof(ts_req_result) +
          2.0 * (double)lat * sizeof(int64_t) + (double)pd * sizeof(PdAux) +
          2.0 * (double)s1 * sizeof(int64_t) + (double)sub * (sizeof(int64_t) + sizeof(int32_t)) +
-         (double)gids * sizeof(int32_t);
+         (double)gids * sizeof(int32_t) + (double)pinfo * sizeof(PointInfo);
 }
 
 }  // namespace tsw
@@ -263,6 +265,7 @@ void release(ts_sweep* h) {
   (void)hipFree(b.sub_a2);
   (void)hipFree(b.sub_gid);
   (void)hipFree(b.gids);
+  (void)hipFree(b.pinfo);
   for (int c = 0; c < kLaunches; ++c) {
     if (h->ev.k0[c]) (void)hipEventDestroy(h->ev.k0[c]);
     if (h->ev.k1[c]) (void)hipEventDestroy(h->ev.k1[c]);
@@ -422,6 +425,7 @@ int make_plan(const ts_model* model, const ts_trace* traces, int32_t n_traces,
     d.n = N;
     d.out_index = i;
     d.out_point = i;
+    P->pinfo.push_back(PointInfo{d.trace_off, N});
     d.pd = -1;
     // blocks a first admission may leave in use; the rest is reserved
     const int64_t adm_cap = p.admit_mem_permille > 0 ? nb * p.admit_mem_permille / 1000 : nb;
@@ -498,7 +502,6 @@ int make_plan(const ts_model* model, const ts_trace* traces, int32_t n_traces,
     int64_t pos = 0;
     for (int v = 0; v < n_d; ++v) {
       X.dec_off[v] = (int32_t)(dec0 + pos);
-      X.pos_off[v] = (int32_t)pos;
       pos += dec_n[(size_t)v];
     }
     if (total_recs + extra_recs > INT32_MAX) return TS_ERR_UNSUPPORTED;
@@ -633,11 +636,12 @@ int make_plan(const ts_model* model, const ts_trace* traces, int32_t n_traces,
 
 int upload(const Plan& P, const DevBufs& B, bool async, hipStream_t s) {
   struct Part { void* dst; const void* src; size_t bytes; };
-  const Part parts[4] = {
+  const Part parts[5] = {
       {B.recs, P.recs.data(), P.recs.size() * sizeof(TraceRec)},
       {B.points, P.dp.data(), P.dp.size() * sizeof(DevPoint)},
       {B.order, P.order.data(), P.order.size() * sizeof(int32_t)},
-      {B.pd, P.aux.data(), P.aux.size() * sizeof(PdAux)}};
+      {B.pd, P.aux.data(), P.aux.size() * sizeof(PdAux)},
+      {B.pinfo, P.pinfo.data(), P.pinfo.size() * sizeof(PointInfo)}};
   for (const Part& q : parts) {
     if (q.bytes == 0) continue;
     const hipError_t e = async ? hipMemcpyAsync(q.dst, q.src, q.bytes, hipMemcpyHostToDevice, s)
@@ -654,11 +658,6 @@ int enqueue(const Plan& P, const DevBufs& B, hipStream_t s, const LaunchEvents* 
   hipError_t e = record(ev ? ev->t0 : nullptr);
   if (e != hipSuccess) return device_error(e, "event record");
   reset_counters_kernel<<<1, 64, 0, s>>>(B.counter, kLaunches);
-  if (B.req) {
-    const size_t n = (size_t)P.count * (size_t)P.max_n;
-    const int blocks = (int)std::min<size_t>((n + 255) / 256, 65536);
-    fill_pending_kernel<<<std::max(blocks, 1), 256, 0, s>>>(B.req, n);
-  }
   SimArgs a;
   a.recs = B.recs;
   a.points = B.points;
@@ -666,12 +665,8 @@ int enqueue(const Plan& P, const DevBufs& B, hipStream_t s, const LaunchEvents* 
   a.queue = B.queue;
   a.times = B.times;
   a.res = B.res;
-  a.req = B.req;
-  a.e2e = B.e2e;
-  a.ttft = B.ttft;
+  a.rec = B.req;
   a.iter_cap = P.iter_cap;
-  a.slo_ttft_ns = P.slo_ttft;
-  a.slo_tpot_ns = P.slo_tpot;
   a.time_limit_ticks = (uint64_t)P.time_limit_ms * 100000ull;  // 100 MHz clock
   a.n_layers = P.coef.n_layers;
   a.lc = P.lc;
@@ -715,15 +710,17 @@ int enqueue(const Plan& P, const DevBufs& B, hipStream_t s, const LaunchEvents* 
     if (e != hipSuccess) return device_error(e, "event record");
   }
   if (P.n_pd > 0) {
-    pd_combine_kernel<<<std::min(P.n_pd, 65536), 256, 0, s>>>(B.pd, P.n_pd, B.res, B.recs,
-                                                               B.e2e, B.ttft, P.max_n);
+    pd_combine_kernel<<<std::min((P.n_pd + 255) / 256, 65536), 256, 0, s>>>(B.pd, P.n_pd,
+                                                                             B.res, B.recs);
     e = hipGetLastError();
     if (e != hipSuccess) return device_error(e, "combine kernel launch");
   }
   e = record(ev ? ev->t1 : nullptr);
   if (e != hipSuccess) return device_error(e, "event record");
   if (P.count > 0)
-    stats_kernel<<<P.stats_grid, 256, 0, s>>>(B.e2e, B.ttft, B.res, P.max_n, P.count);
+    stats_kernel<<<P.stats_grid, 256, 0, s>>>(B.req, B.recs, B.pinfo, B.res, B.e2e, B.ttft,
+                                              P.max_n, P.count, P.slo_ttft, P.slo_tpot,
+                                              (P.flags & TS_F_PER_REQUEST) ? 1 : 0);
   e = hipGetLastError();
   if (e != hipSuccess) return device_error(e, "stats kernel launch");
   e = record(ev ? ev->t2 : nullptr);
@@ -784,7 +781,8 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
   if (ae == hipSuccess) ae = dev_alloc(&b.res, n.res);
   if (ae == hipSuccess) ae = dev_alloc(&b.e2e, n.lat);
   if (ae == hipSuccess) ae = dev_alloc(&b.ttft, n.lat);
-  if (ae == hipSuccess && n.req > 0) ae = dev_alloc(&b.req, n.req);
+  if (ae == hipSuccess) ae = dev_alloc(&b.req, n.req);
+  if (ae == hipSuccess) ae = dev_alloc(&b.pinfo, n.pinfo);
   if (ae == hipSuccess) ae = dev_alloc(&b.pd, n.pd);
   if (ae == hipSuccess) ae = dev_alloc(&b.s1_admit, n.s1);
   if (ae == hipSuccess) ae = dev_alloc(&b.s1_first, n.s1);
@@ -841,7 +839,7 @@ int ts_sweep_run(ts_sweep* h, void* hip_stream) {
 int ts_sweep_results(ts_sweep* h, ts_point_result* out_points, ts_req_result* out_requests) {
   if (!h) return TS_ERR_ARG;
   if (!h->ran) return TS_ERR_STATE;
-  if (out_requests && !h->B.req) return TS_ERR_STATE;
+  if (out_requests && !(h->P.flags & TS_F_PER_REQUEST)) return TS_ERR_STATE;
   if (!out_points && h->P.count > 0) return TS_ERR_ARG;
   hipError_t e = hipSetDevice(h->P.device);
   if (e == hipSuccess) e = hipStreamSynchronize(h->last_stream);

@@ -76,13 +76,14 @@ size_t carve(const tsw::Plan& P, unsigned char* base, tsw::DevBufs* B) {
   b.res = c.take<ts_point_result>(n.res);
   b.e2e = c.take<int64_t>(n.lat);
   b.ttft = c.take<int64_t>(n.lat);
-  b.req = n.req > 0 ? c.take<ts_req_result>(n.req) : nullptr;
+  b.req = c.take<ts_req_result>(n.req);
   b.pd = c.take<tsw::PdAux>(n.pd);
   b.s1_admit = c.take<int64_t>(n.s1);
   b.s1_first = c.take<int64_t>(n.s1);
   b.sub_a2 = c.take<int64_t>(n.sub);
   b.sub_gid = c.take<int32_t>(n.sub);
   b.gids = c.take<int32_t>(n.gids);
+  b.pinfo = c.take<tsw::PointInfo>(n.pinfo);
   if (B) *B = b;
   return c.used;
 }
@@ -126,8 +127,8 @@ extern "C" int ts_sweep_run_static(const ts_model* model, const ts_trace* traces
   carve(P, base, &B);
   hipStream_t s = (hipStream_t)hip_stream;
   // inputs from the plan's host vectors, which live until the stream is
-  // synchronised below; the enqueue clears the counters and the request
-  // records on the device
+  // synchronised below; the enqueue clears the ticket counters, and every
+  // request record is rewritten by the run
   rc = tsw::upload(P, B, true, s);
   if (rc == TS_OK) rc = tsw::enqueue(P, B, s, nullptr);
   if (rc == TS_OK && P.count > 0) {

@@ -277,10 +277,6 @@ struct SlotLds {
   int32_t npre[NCH * 64];  // times preempted per slot
   uint8_t x_fl[NX * 64];   // flags fit a byte: with the staging below, 256 slots
                            // take at most 10 KiB, so 16 workgroups share a CU
-  // finished-request statistics of the point, accumulated by LDS atomics
-  unsigned long long sum_ttft, sum_e2e, sum_tpot, digest;
-  long long max_e2e, last_fin;
-  unsigned int slo_ok, slo_tpot_ok;
   unsigned int sub_cnt[kMaxDev];  // prefill device: requests handed to each decode device
   // steady segment: the two attention operators' FLOPs, bytes and their
   // per-iteration steps at the segment start, then the other operators' times
@@ -337,7 +333,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
   };
   // the disaggregated point a device belongs to
   PdAux* X = nullptr;
-  int n_pd = 1, nd_pd = 1, req_base = 0, orig_off = 0, pos_off = 0;
+  int n_pd = 1, nd_pd = 1, req_base = 0;
   int64_t kv_bpt = 0, link_free = 0;
   double inv_kv_link = 0.0;
   if constexpr (MODE != kStageOne) {
@@ -345,10 +341,8 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
     n_pd = X->n_p;
     nd_pd = X->n_d;
     req_base = X->req_base;
-    orig_off = X->trace_off;
     kv_bpt = X->kv_bpt;
     inv_kv_link = X->inv_link_ns;
-    if constexpr (MODE == kStageDecode) pos_off = X->pos_off[P.unit];
   }
   // a request's index in the point's trace from its index in this unit's trace
   auto gid_of = [&](int local) -> int {
@@ -359,14 +353,10 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
   const double iF = P.inv_flops_ns, iB = P.inv_bw_ns;
   const int oi = P.out_index;
   const int orow = MODE == kStageOne ? oi : P.out_point;  // the design point's row
-  ts_req_result* RR = A.req ? A.req + (size_t)orow * (size_t)A.max_n : nullptr;
-  int64_t* E2E = A.e2e + (size_t)orow * (size_t)A.max_n + pos_off;
-  int64_t* TTFT = A.ttft + (size_t)orow * (size_t)A.max_n + pos_off;
+  // the design point's request records: every request's record is written
+  // once, when it finishes, is rejected, or is left unfinished by an early stop
+  ts_req_result* RR = A.rec + (size_t)orow * (size_t)A.max_n;
 
-  // statistics of finished / rejected requests: LDS accumulators, cleared
-  // by every lane storing the same zeros (no lane-dependent branch)
-  L.sum_ttft = 0; L.sum_e2e = 0; L.sum_tpot = 0; L.digest = 0;
-  L.max_e2e = -1; L.last_fin = -1; L.slo_ok = 0; L.slo_tpot_ok = 0;
   L.sub_cnt[lane & (kMaxDev - 1)] = 0;
   __syncthreads();
   int n_rej = 0;
@@ -381,14 +371,10 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
         rj = rejected(r.prompt, r.output);
       }
       if (rj) {
-        const int g = gid_of(i);
-        atomicAdd(&L.digest, (unsigned long long)record_hash(g, -1, -1, -1, 0, 0, TS_REQ_REJECTED));
-        if (RR) {
-          ts_req_result o;
-          o.admit_ns = -1; o.first_token_ns = -1; o.finish_ns = -1; o.max_gap_ns = 0;
-          o.n_preempt = 0; o.status = TS_REQ_REJECTED;
-          RR[g] = o;
-        }
+        ts_req_result o;
+        o.admit_ns = -1; o.first_token_ns = -1; o.finish_ns = -1; o.max_gap_ns = 0;
+        o.n_preempt = 0; o.status = TS_REQ_REJECTED;
+        RR[gid_of(i)] = o;
       }
       n_rej += popc(ballot(rj));
     }
@@ -451,35 +437,17 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
   const int lgB = (B & (B - 1)) == 0 ? 31 - __builtin_clz((unsigned)B) : -1;
   auto divB = [&](int x) { return lgB >= 0 ? x >> lgB : x / B; };
 
-  // A request finishing at t_end (lanes with fin): its statistics and record.
-  auto record_done = [&](bool fin, int s, int64_t t_end, int64_t gap, int pos) {
+  // A request finishing at t_end (lanes with fin): its record.  The point's
+  // latency sums, SLO counts, percentiles and digest are computed from the
+  // records after the simulation.
+  auto record_done = [&](bool fin, int s, int64_t t_end, int64_t gap) {
     if (fin) {
       const int id = L.id[s];
-      const int g = gid_of(id);
-      const int npr = L.npre[s];
       const ReqTimes rt = RT[id];
-      // latencies count from the arrival at the point (a decode device's
-      // trace holds the arrivals of the KV instead)
-      const int64_t arr = MODE == kStageDecode ? A.recs[orig_off + g].arrival_ns : rec[id].arrival_ns;
-      const int64_t tt = rt.first - arr;
-      const int64_t ee = t_end - arr;
-      atomicAdd(&L.sum_ttft, (unsigned long long)tt);
-      atomicAdd(&L.sum_e2e, (unsigned long long)ee);
-      atomicAdd(&L.sum_tpot, (unsigned long long)(t_end - rt.first));
-      atomicMax(&L.max_e2e, (long long)ee);
-      atomicMax(&L.last_fin, (long long)t_end);
-      if (tt <= A.slo_ttft_ns && gap <= A.slo_tpot_ns) atomicAdd(&L.slo_ok, 1u);
-      if (gap <= A.slo_tpot_ns) atomicAdd(&L.slo_tpot_ok, 1u);
-      atomicAdd(&L.digest, (unsigned long long)record_hash(g, rt.admit, rt.first, t_end, gap,
-                                                           npr, TS_REQ_DONE));
-      if (RR) {
-        ts_req_result o;
-        o.admit_ns = rt.admit; o.first_token_ns = rt.first; o.finish_ns = t_end;
-        o.max_gap_ns = gap; o.n_preempt = npr; o.status = TS_REQ_DONE;
-        RR[g] = o;
-      }
-      E2E[pos] = ee;
-      TTFT[pos] = tt;
+      ts_req_result o;
+      o.admit_ns = rt.admit; o.first_token_ns = rt.first; o.finish_ns = t_end;
+      o.max_gap_ns = gap; o.n_preempt = L.npre[s]; o.status = TS_REQ_DONE;
+      RR[gid_of(id)] = o;
     }
   };
 
@@ -916,8 +884,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
                   if (fm != 0) {
                     const int ctx0 = j == 0 ? h0.ctx : L.x_ctx[e];
                     const int64_t gap0 = j == 0 ? h0.gap : L.x_gap[e];
-                    record_done(fin, j * 64 + lane, t_end, gx > gap0 ? gx : gap0,
-                                n_done + nfin + rank_below(fm));
+                    record_done(fin, j * 64 + lane, t_end, gx > gap0 ? gx : gap0);
                     l_freed += fin ? divB(ctx0 + rr[j]) : 0;  // held blocks
                     rr[j] = fin ? -0x40000000 : rr[j];
                     nfin += popc(fm);
@@ -1036,9 +1003,12 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
                 const int e = (js - 1) * 64 + ls;
                 room_s = __builtin_amdgcn_readfirstlane(L.x_room[e]);
                 id_s = L.id[nD];
-                L.x_ctx[e] = tgt_p - g1;  // every lane stores the same values
-                L.x_rem[e] = L.x_rem[e] + g1;
-                L.x_fl[e] = L.x_fl[e] | FL_FIRST;
+                // read once for the wave, then every lane stores the same values
+                const int rem_s = __builtin_amdgcn_readfirstlane(L.x_rem[e]);
+                const int fl_s = __builtin_amdgcn_readfirstlane((int)L.x_fl[e]);
+                L.x_ctx[e] = tgt_p - g1;
+                L.x_rem[e] = rem_s + g1;
+                L.x_fl[e] = fl_s | FL_FIRST;
               }
               id_s = __builtin_amdgcn_readfirstlane(id_s);
               RT[id_s].first = t_end;
@@ -1491,7 +1461,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
     pf_tok += TP;
     dec_tok += nD;
 
-    int nfin = 0, base = n_done, l_freed = 0;
+    int nfin = 0, l_freed = 0;
 #pragma nounroll
     for (int j = 0; j < nch; ++j) {
       Hot h = load_chunk<NCH>(L, h0, j, lane);
@@ -1541,9 +1511,8 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       }
       const uint64_t fm = ballot(fin);
       if (fm != 0) {
-        record_done(fin, s, t_end, h.gap, base + rank_below(fm));
+        record_done(fin, s, t_end, h.gap);
         if (fin) l_freed += divB(h.ctx + h.room);  // held blocks (ctx >= tgt here)
-        base += popc(fm);
         nfin += popc(fm);
       }
     }
@@ -1555,20 +1524,30 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
     t = t_end;
   }
 
-  // ---- per-point results (percentiles are filled by the statistics kernel)
+  // ---- a point stopped early (iteration cap, watchdog): the requests it
+  // has not finished keep "pending" records: the running ones, the
+  // preempted ones in the queue, and those never admitted (from next_new on)
+  if (status == TS_POINT_ITER_LIMIT || status == TS_POINT_TIME_LIMIT) {
+    ts_req_result o;
+    o.admit_ns = -1; o.first_token_ns = -1; o.finish_ns = -1; o.max_gap_ns = 0;
+    o.n_preempt = 0; o.status = TS_REQ_PENDING;
+    for (int s0 = 0; s0 < nrun; s0 += 64)
+      if (s0 + lane < nrun) RR[gid_of(L.id[s0 + lane])] = o;
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+    for (int k0 = 0; k0 < npre; k0 += 64)
+      if (k0 + lane < npre) RR[gid_of(Q[(qhead + k0 + lane) & (kQueueCap - 1)].id)] = o;
+    for (int i0 = next_new; i0 < N; i0 += 64) {
+      const int i = i0 + lane;
+      if (i < N && !(P.may_reject && rejected(rec[i].prompt, rec[i].output))) RR[gid_of(i)] = o;
+    }
+  }
+
+  // ---- per-point results (latency sums, SLO counts, percentiles and the
+  // digest are filled by the statistics kernel from the request records)
   if constexpr (MODE == kStagePrefill) {
     const int v = lane < nd_pd ? lane : nd_pd - 1;  // lanes past n_d repeat the last store
     X->sub_cnt[P.unit * kMaxDev + v] = (int)L.sub_cnt[v];
   }
-  __syncthreads();
-  const int64_t sum_ttft = (int64_t)L.sum_ttft;
-  const int64_t sum_e2e = (int64_t)L.sum_e2e;
-  const int64_t sum_tpot = (int64_t)L.sum_tpot;
-  const int slo_ok = (int)L.slo_ok;
-  const int slo_tpot_ok = (int)L.slo_tpot_ok;
-  const int64_t max_e2e = L.max_e2e;
-  const int64_t last_fin = L.last_fin;
-  const uint64_t digest = L.digest;
   __syncthreads();
   {
     // Every lane stores the same uniform record: no lane-dependent branch
@@ -1585,17 +1564,17 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
     o.decode_tokens = dec_tok;
     o.peak_used_blocks = peak;
     o.first_arrival_ns = N > 0 ? rec[0].arrival_ns : -1;
-    o.last_finish_ns = last_fin;
-    o.sum_ttft_ns = sum_ttft;
-    o.sum_e2e_ns = sum_e2e;
-    o.max_e2e_ns = max_e2e;
-    o.sum_tpot_num_ns = sum_tpot;
+    o.last_finish_ns = -1;
+    o.sum_ttft_ns = 0;
+    o.sum_e2e_ns = 0;
+    o.max_e2e_ns = -1;
+    o.sum_tpot_num_ns = 0;
     o.p50_e2e_ns = o.p90_e2e_ns = o.p99_e2e_ns = -1;
     o.p50_ttft_ns = o.p99_ttft_ns = -1;
-    o.slo_ok = slo_ok;
+    o.slo_ok = 0;
     o.used_block_ns = ubns;
-    o.digest = digest;
-    o.slo_tpot_ok = slo_tpot_ok;
+    o.digest = 0;
+    o.slo_tpot_ok = 0;
     A.res[oi] = o;
   }
 }
@@ -1700,51 +1679,108 @@ __device__ __forceinline__ int nearest_rank_index(int pct, int n) {
   return (int)(((int64_t)pct * n + 99) / 100) - 1;
 }
 
-__global__ __launch_bounds__(256) void stats_kernel(const int64_t* e2e, const int64_t* ttft,
-                                                    ts_point_result* res, int max_n,
-                                                    int n_points) {
+// The point's request statistics from its request records, one 256-thread
+// workgroup per point: latency sums (TTFT = first token - arrival, E2E =
+// finish - arrival, TPOT numerator = finish - first token), the largest E2E,
+// the last finish, the SLO counts (Sec. IV-B), the digest over finished and
+// rejected records, then nearest-rank percentiles of the finished requests'
+// latencies by radix select over a dense copy of them.  With pad_pending
+// (per-request output) the row's entries past the trace also get "pending"
+// records.
+__global__ __launch_bounds__(256) void stats_kernel(ts_req_result* rec, const TraceRec* recs,
+                                                    const PointInfo* pinfo,
+                                                    ts_point_result* res, int64_t* e2e,
+                                                    int64_t* ttft, int max_n, int n_points,
+                                                    int64_t slo_ttft_ns, int64_t slo_tpot_ns,
+                                                    int pad_pending) {
   __shared__ int hist[3 * 256];
   __shared__ int sh[9];
+  __shared__ unsigned long long acc_sum[4];  // TTFT, E2E, TPOT numerator, digest
+  __shared__ long long acc_max[2];           // largest E2E, last finish
+  __shared__ unsigned int acc_cnt[3];        // finished (dense index), slo_ok, slo_tpot_ok
   for (int p = blockIdx.x; p < n_points; p += gridDim.x) {
-    const int n = res[p].n_done;
-    int64_t r[5] = {-1, -1, -1, -1, -1};
+    const PointInfo pi = pinfo[p];
+    ts_req_result* R = rec + (size_t)p * (size_t)max_n;
+    int64_t* ve = e2e + (size_t)p * (size_t)max_n;
+    int64_t* vt = ttft + (size_t)p * (size_t)max_n;
+    if (threadIdx.x < 4) acc_sum[threadIdx.x] = 0;
+    if (threadIdx.x < 2) acc_max[threadIdx.x] = -1;
+    if (threadIdx.x < 3) acc_cnt[threadIdx.x] = 0;
+    __syncthreads();
+    uint64_t s_tt = 0, s_ee = 0, s_tp = 0, dig = 0;
+    int64_t mx = -1, lf = -1;
+    unsigned int n_slo = 0, n_slo_tpot = 0;
+    for (int g = threadIdx.x; g < pi.n; g += 256) {
+      const ts_req_result r = R[g];
+      if (r.status == TS_REQ_DONE) {
+        const int64_t arr = recs[pi.trace_off + g].arrival_ns;
+        const int64_t tt = r.first_token_ns - arr, ee = r.finish_ns - arr;
+        s_tt += (uint64_t)tt;
+        s_ee += (uint64_t)ee;
+        s_tp += (uint64_t)(r.finish_ns - r.first_token_ns);
+        mx = ee > mx ? ee : mx;
+        lf = r.finish_ns > lf ? r.finish_ns : lf;
+        n_slo += (tt <= slo_ttft_ns && r.max_gap_ns <= slo_tpot_ns) ? 1u : 0u;
+        n_slo_tpot += r.max_gap_ns <= slo_tpot_ns ? 1u : 0u;
+        const unsigned int pos = atomicAdd(&acc_cnt[0], 1u);
+        ve[pos] = ee;
+        vt[pos] = tt;
+      }
+      if (r.status == TS_REQ_DONE || r.status == TS_REQ_REJECTED)
+        dig += record_hash(g, r.admit_ns, r.first_token_ns, r.finish_ns, r.max_gap_ns,
+                           r.n_preempt, r.status);
+    }
+    if (pad_pending) {
+      ts_req_result o;
+      o.admit_ns = -1; o.first_token_ns = -1; o.finish_ns = -1; o.max_gap_ns = 0;
+      o.n_preempt = 0; o.status = TS_REQ_PENDING;
+      for (int g = pi.n + (int)threadIdx.x; g < max_n; g += 256) R[g] = o;
+    }
+    atomicAdd(&acc_sum[0], (unsigned long long)s_tt);
+    atomicAdd(&acc_sum[1], (unsigned long long)s_ee);
+    atomicAdd(&acc_sum[2], (unsigned long long)s_tp);
+    atomicAdd(&acc_sum[3], (unsigned long long)dig);
+    atomicMax(&acc_max[0], (long long)mx);
+    atomicMax(&acc_max[1], (long long)lf);
+    atomicAdd(&acc_cnt[1], n_slo);
+    atomicAdd(&acc_cnt[2], n_slo_tpot);
+    __syncthreads();
+    const int n = (int)acc_cnt[0];
+    const int64_t max_e2e = acc_max[0];
+    int64_t r5[5] = {-1, -1, -1, -1, -1};
     if (n > 0) {
-      const int64_t* ve = e2e + (size_t)p * (size_t)max_n;
-      const int64_t* vt = ttft + (size_t)p * (size_t)max_n;
       // every latency lies in [0, max_e2e] (a first token never comes after
       // the finish): digits above the top one are zero for all of them
-      const uint64_t mx = (uint64_t)res[p].max_e2e_ns;
-      const int bits = mx == 0 ? 1 : 64 - __builtin_clzll(mx);
+      const uint64_t m = (uint64_t)max_e2e;
+      const int bits = m == 0 ? 1 : 64 - __builtin_clzll(m);
       const int top_shift = ((bits - 1) / 8) * 8;
       const int ke[3] = {nearest_rank_index(50, n), nearest_rank_index(90, n),
                          nearest_rank_index(99, n)};
       const int kt[2] = {nearest_rank_index(50, n), nearest_rank_index(99, n)};
       if (threadIdx.x < 3) sh[6 + threadIdx.x] = ke[threadIdx.x];
       __syncthreads();
-      select_ranks<3>(ve, n, ke, top_shift, r, hist, sh);
+      select_ranks<3>(ve, n, ke, top_shift, r5, hist, sh);
       if (threadIdx.x < 2) sh[4 + threadIdx.x] = kt[threadIdx.x];
       __syncthreads();
-      select_ranks<2>(vt, n, kt, top_shift, r + 3, hist, sh);
+      select_ranks<2>(vt, n, kt, top_shift, r5 + 3, hist, sh);
     }
     if (threadIdx.x == 0) {
-      res[p].p50_e2e_ns = r[0];
-      res[p].p90_e2e_ns = r[1];
-      res[p].p99_e2e_ns = r[2];
-      res[p].p50_ttft_ns = r[3];
-      res[p].p99_ttft_ns = r[4];
+      ts_point_result& o = res[p];
+      o.sum_ttft_ns = (int64_t)acc_sum[0];
+      o.sum_e2e_ns = (int64_t)acc_sum[1];
+      o.sum_tpot_num_ns = (int64_t)acc_sum[2];
+      o.digest = acc_sum[3];
+      o.max_e2e_ns = max_e2e;
+      o.last_finish_ns = acc_max[1];
+      o.slo_ok = (int64_t)acc_cnt[1];
+      o.slo_tpot_ok = (int64_t)acc_cnt[2];
+      o.p50_e2e_ns = r5[0];
+      o.p90_e2e_ns = r5[1];
+      o.p99_e2e_ns = r5[2];
+      o.p50_ttft_ns = r5[3];
+      o.p99_ttft_ns = r5[4];
     }
     __syncthreads();
-  }
-}
-
-// Per-request records start as "pending" (kept by requests never finished).
-__global__ void fill_pending_kernel(ts_req_result* r, size_t n) {
-  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-       i += (size_t)gridDim.x * blockDim.x) {
-    ts_req_result o;
-    o.admit_ns = -1; o.first_token_ns = -1; o.finish_ns = -1; o.max_gap_ns = 0;
-    o.n_preempt = 0; o.status = TS_REQ_PENDING;
-    r[i] = o;
   }
 }
 
@@ -1797,91 +1833,50 @@ __global__ __launch_bounds__(256) void pd_merge_kernel(const PdAux* aux, int n_a
   }
 }
 
-// A disaggregated point's record from its devices' records: requests and
-// latency sums from the decode devices, rejections from the prefill devices,
-// iterations, tokens, the used-block integral (prefill devices first, then
-// decode devices, in index order) and the digest over all devices, the block
-// peak of the busiest decode device.  The decode devices' latencies are then
-// moved to the front of the point's row for the percentile pass.  One
-// 256-thread workgroup per point.
+// A disaggregated point's record from its devices' records: finished
+// requests from the decode devices, rejections from the prefill devices,
+// iterations, tokens and the used-block integral (prefill devices first,
+// then decode devices, in index order) over all devices, the block peak of
+// the busiest decode device.  The latency sums, SLO counts, percentiles and
+// digest come after, from the point's request records.  One thread per point.
 __global__ __launch_bounds__(256) void pd_combine_kernel(const PdAux* aux, int n_aux,
                                                          ts_point_result* res,
-                                                         const TraceRec* recs, int64_t* e2e,
-                                                         int64_t* ttft, int max_n) {
-  __shared__ int seg_n[kMaxDev];
-  for (int b = blockIdx.x; b < n_aux; b += gridDim.x) {
+                                                         const TraceRec* recs) {
+  for (int b = blockIdx.x * blockDim.x + threadIdx.x; b < n_aux; b += gridDim.x * blockDim.x) {
     const PdAux& X = aux[b];
-    if (threadIdx.x == 0) {
-      ts_point_result o;
-      const int nu = X.n_p + X.n_d;
-      o.status = TS_POINT_OK;
-      o.n_done = 0; o.n_rejected = 0; o.num_blocks = X.num_blocks_d;
-      o.n_iters = 0; o.n_preempt = 0; o.prefill_tokens = 0; o.decode_tokens = 0;
-      o.peak_used_blocks = 0;
-      o.first_arrival_ns = X.n > 0 ? recs[X.trace_off].arrival_ns : -1;
-      o.last_finish_ns = -1;
-      o.sum_ttft_ns = 0; o.sum_e2e_ns = 0; o.max_e2e_ns = -1; o.sum_tpot_num_ns = 0;
-      o.p50_e2e_ns = o.p90_e2e_ns = o.p99_e2e_ns = -1;
-      o.p50_ttft_ns = o.p99_ttft_ns = -1;
-      o.slo_ok = 0; o.slo_tpot_ok = 0;
-      o.used_block_ns = 0.0;
-      o.digest = 0;
-      for (int u = 0; u < nu; ++u) {
-        const ts_point_result& r = res[X.res0 + u];
-        const bool dec = u >= X.n_p;
-        o.status = r.status > o.status ? r.status : o.status;
-        o.n_iters += r.n_iters;
-        o.n_preempt += r.n_preempt;
-        o.prefill_tokens += r.prefill_tokens;
-        o.decode_tokens += r.decode_tokens;
-        o.used_block_ns = o.used_block_ns + r.used_block_ns;
-        o.digest += r.digest;
-        if (dec) {
-          o.n_done += r.n_done;
-          o.peak_used_blocks = r.peak_used_blocks > o.peak_used_blocks ? r.peak_used_blocks
-                                                                        : o.peak_used_blocks;
-          o.last_finish_ns = r.last_finish_ns > o.last_finish_ns ? r.last_finish_ns
-                                                                  : o.last_finish_ns;
-          o.sum_ttft_ns += r.sum_ttft_ns;
-          o.sum_e2e_ns += r.sum_e2e_ns;
-          o.max_e2e_ns = r.max_e2e_ns > o.max_e2e_ns ? r.max_e2e_ns : o.max_e2e_ns;
-          o.sum_tpot_num_ns += r.sum_tpot_num_ns;
-          o.slo_ok += r.slo_ok;
-          o.slo_tpot_ok += r.slo_tpot_ok;
-          seg_n[u - X.n_p] = r.n_done;
-        } else {
-          o.n_rejected += r.n_rejected;
-        }
+    ts_point_result o;
+    const int nu = X.n_p + X.n_d;
+    o.status = TS_POINT_OK;
+    o.n_done = 0; o.n_rejected = 0; o.num_blocks = X.num_blocks_d;
+    o.n_iters = 0; o.n_preempt = 0; o.prefill_tokens = 0; o.decode_tokens = 0;
+    o.peak_used_blocks = 0;
+    o.first_arrival_ns = X.n > 0 ? recs[X.trace_off].arrival_ns : -1;
+    o.last_finish_ns = -1;
+    o.sum_ttft_ns = 0; o.sum_e2e_ns = 0; o.max_e2e_ns = -1; o.sum_tpot_num_ns = 0;
+    o.p50_e2e_ns = o.p90_e2e_ns = o.p99_e2e_ns = -1;
+    o.p50_ttft_ns = o.p99_ttft_ns = -1;
+    o.slo_ok = 0; o.slo_tpot_ok = 0;
+    o.used_block_ns = 0.0;
+    o.digest = 0;
+    for (int u = 0; u < nu; ++u) {
+      const ts_point_result& r = res[X.res0 + u];
+      const bool dec = u >= X.n_p;
+      o.status = r.status > o.status ? r.status : o.status;
+      o.n_iters += r.n_iters;
+      o.n_preempt += r.n_preempt;
+      o.prefill_tokens += r.prefill_tokens;
+      o.decode_tokens += r.decode_tokens;
+      o.used_block_ns = o.used_block_ns + r.used_block_ns;
+      if (dec) {
+        o.n_done += r.n_done;
+        o.peak_used_blocks = r.peak_used_blocks > o.peak_used_blocks ? r.peak_used_blocks
+                                                                      : o.peak_used_blocks;
+      } else {
+        o.n_rejected += r.n_rejected;
       }
-      if (X.no_kv) o.status = TS_POINT_NO_KV;
-      res[X.point] = o;
     }
-    __syncthreads();
-    // decode device v's latencies: from pos_off[v] to the running total;
-    // destinations never pass their sources, and a chunk is read whole
-    // before it is written
-    int64_t* ve = e2e + (size_t)X.point * (size_t)max_n;
-    int64_t* vt = ttft + (size_t)X.point * (size_t)max_n;
-    int dst = 0;
-    for (int v = 0; v < X.n_d; ++v) {
-      const int n = seg_n[v], src = X.pos_off[v];
-      for (int k0 = 0; k0 < n; k0 += 256) {
-        const int k = k0 + (int)threadIdx.x;
-        int64_t a = 0, c = 0;
-        if (k < n) {
-          a = ve[src + k];
-          c = vt[src + k];
-        }
-        __syncthreads();
-        if (k < n) {
-          ve[dst + k] = a;
-          vt[dst + k] = c;
-        }
-        __syncthreads();
-      }
-      dst += n;
-    }
-    __syncthreads();
+    if (X.no_kv) o.status = TS_POINT_NO_KV;
+    res[X.point] = o;
   }
 }
 

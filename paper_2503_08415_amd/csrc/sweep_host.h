@@ -34,6 +34,7 @@ struct Plan {
   std::vector<DevPoint> dp;     // simulation units
   std::vector<int32_t> order;   // units per launch, longest expected first, concatenated
   std::vector<PdAux> aux;
+  std::vector<PointInfo> pinfo;  // per design point: its trace (statistics kernel)
   int class_off[kLaunches] = {}, class_n[kLaunches] = {};
   int grid[kLaunches] = {};     // persistent workgroups per launch
   int stats_grid = 1;
@@ -42,7 +43,7 @@ struct Plan {
 
 // Element counts of every device buffer of a plan.
 struct BufCounts {
-  size_t recs, points, order, counter, queue, times, res, req, lat, pd, s1, sub, gids;
+  size_t recs, points, order, counter, queue, times, res, req, lat, pd, s1, sub, gids, pinfo;
   double bytes() const;  // total, in bytes
 };
 BufCounts buf_counts(const Plan& P);
@@ -57,7 +58,7 @@ struct DevBufs {
   QEntry* queue = nullptr;          // kQueueCap per workgroup, shared by the launches
   ReqTimes* times = nullptr;        // max_n per workgroup, shared by the launches
   ts_point_result* res = nullptr;
-  ts_req_result* req = nullptr;     // only with TS_F_PER_REQUEST
+  ts_req_result* req = nullptr;     // the request records, max_n per point
   int64_t* e2e = nullptr;           // max_n per point: latencies for the percentile pass
   int64_t* ttft = nullptr;
   PdAux* pd = nullptr;
@@ -66,6 +67,7 @@ struct DevBufs {
   int64_t* sub_a2 = nullptr;
   int32_t* sub_gid = nullptr;
   int32_t* gids = nullptr;
+  PointInfo* pinfo = nullptr;
 };
 
 // HIP events around the launches (timing); any may be null.
@@ -86,9 +88,9 @@ int make_plan(const ts_model* model, const ts_trace* traces, int32_t n_traces,
 // stream s (the host vectors must then outlive the copies).
 int upload(const Plan& P, const DevBufs& B, bool async, hipStream_t s);
 
-// Enqueues one run on stream s: counter reset, per-request fill, the
-// simulation launches (with the merge and combine kernels of disaggregated
-// points), then the statistics kernel.
+// Enqueues one run on stream s: counter reset, the simulation launches
+// (with the merge and combine kernels of disaggregated points), then the
+// statistics kernel.
 int enqueue(const Plan& P, const DevBufs& B, hipStream_t s, const LaunchEvents* ev);
 
 // Error text for ts_status_str (per thread).

@@ -70,7 +70,12 @@ struct __attribute__((aligned(16))) PdAux {
   int32_t sub_off[kMaxDev * kMaxDev];  // (w, v) -> first entry of the sub-list
   int32_t sub_cnt[kMaxDev * kMaxDev];  // (w, v) -> entries written
   int32_t dec_off[kMaxDev];            // decode device v's trace records
-  int32_t pos_off[kMaxDev];            // decode device v's latency entries within the row
+};
+
+// Where a design point's requests are: its trace's first record and length
+// (the statistics kernel reads the arrivals there).
+struct PointInfo {
+  int32_t trace_off, n;
 };
 
 // Integer coefficients of the per-operator roofline (exact below 2^53):
@@ -121,12 +126,8 @@ struct SimArgs {
   QEntry* queue;               // kQueueCap entries per workgroup
   ReqTimes* times;             // max_n entries per workgroup
   ts_point_result* res;
-  ts_req_result* req;          // nullptr unless per-request records are requested
-  int64_t* e2e;                // max_n per point: end-to-end latency of finished requests
-  int64_t* ttft;               // max_n per point: time to first token
+  ts_req_result* rec;          // max_n per point: the request records (row = design point)
   int64_t iter_cap;
-  int64_t slo_ttft_ns;
-  int64_t slo_tpot_ns;
   uint64_t time_limit_ticks;   // 0 = none; 100 MHz device clock ticks per point
   double n_layers;
   LaneCoef lc;
