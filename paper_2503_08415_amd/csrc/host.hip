@@ -21,7 +21,7 @@
 #include "sweep_host.h"
 
 namespace tsw {
-template <int NCH, int MODE>
+template <int NCH, int MODE, bool SIMPLE>
 __global__ void sim_kernel(SimArgs A);
 __global__ void pd_merge_kernel(const PdAux* aux, int n_aux, const int64_t* sub_a2,
                                 const int32_t* sub_gid, TraceRec* recs, int32_t* gids,
@@ -43,18 +43,28 @@ thread_local char g_err[256];
 
 constexpr int kClassChunks[kClasses] = {1, 2, 4};
 
-const void* sim_kernel_fn(int launch) {
+// The kernel of launch 3 * stage + class; one-worker launches whose points
+// are all simple (continuous batching, recompute preemption, no admission
+// ratio, no watchdog) use the variant with that policy fixed at compile time.
+const void* sim_kernel_fn(int launch, bool simple) {
   const int st = launch / kClasses, c = launch % kClasses;
+  if (st == kStageOne && simple) {
+    switch (kClassChunks[c]) {
+      case 1: return (const void*)sim_kernel<1, kStageOne, true>;
+      case 2: return (const void*)sim_kernel<2, kStageOne, true>;
+      default: return (const void*)sim_kernel<4, kStageOne, true>;
+    }
+  }
   switch (st * 8 + kClassChunks[c]) {
-    case 0 * 8 + 1: return (const void*)sim_kernel<1, kStageOne>;
-    case 0 * 8 + 2: return (const void*)sim_kernel<2, kStageOne>;
-    case 0 * 8 + 4: return (const void*)sim_kernel<4, kStageOne>;
-    case 1 * 8 + 1: return (const void*)sim_kernel<1, kStagePrefill>;
-    case 1 * 8 + 2: return (const void*)sim_kernel<2, kStagePrefill>;
-    case 1 * 8 + 4: return (const void*)sim_kernel<4, kStagePrefill>;
-    case 2 * 8 + 1: return (const void*)sim_kernel<1, kStageDecode>;
-    case 2 * 8 + 2: return (const void*)sim_kernel<2, kStageDecode>;
-    default: return (const void*)sim_kernel<4, kStageDecode>;
+    case 0 * 8 + 1: return (const void*)sim_kernel<1, kStageOne, false>;
+    case 0 * 8 + 2: return (const void*)sim_kernel<2, kStageOne, false>;
+    case 0 * 8 + 4: return (const void*)sim_kernel<4, kStageOne, false>;
+    case 1 * 8 + 1: return (const void*)sim_kernel<1, kStagePrefill, false>;
+    case 1 * 8 + 2: return (const void*)sim_kernel<2, kStagePrefill, false>;
+    case 1 * 8 + 4: return (const void*)sim_kernel<4, kStagePrefill, false>;
+    case 2 * 8 + 1: return (const void*)sim_kernel<1, kStageDecode, false>;
+    case 2 * 8 + 2: return (const void*)sim_kernel<2, kStageDecode, false>;
+    default: return (const void*)sim_kernel<4, kStageDecode, false>;
   }
 }
 
@@ -572,6 +582,15 @@ int make_plan(const ts_model* model, const ts_trace* traces, int32_t n_traces,
                      [&](int32_t a, int32_t b) { return est[(size_t)a] > est[(size_t)b]; });
     P->class_off[l] = (int)order.size();
     P->class_n[l] = (int)cls.size();
+    // one-worker launches whose points are all simple take the kernel with
+    // the policy fixed at compile time
+    bool simple = l / kClasses == kStageOne && time_limit_ms == 0;
+    for (const int32_t u : cls) {
+      const DevPoint& d = dp[(size_t)u];
+      simple = simple && d.policy == TS_POLICY_MIXED && d.swap == 0 && d.adm_reserve == 0 &&
+               d.cap_prompt == d.cap_tokens;
+    }
+    P->simple[l] = simple;
     order.insert(order.end(), cls.begin(), cls.end());
   }
   P->count = count;
@@ -595,7 +614,8 @@ int make_plan(const ts_model* model, const ts_trace* traces, int32_t n_traces,
   for (int l = 0; l < kLaunches; ++l) {
     if (P->class_n[l] == 0) continue;
     int per_cu = 0;
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, sim_kernel_fn(l), 64, 0);
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, sim_kernel_fn(l, P->simple[l]), 64,
+                                                     0);
     if (e != hipSuccess) { return device_error(e, "occupancy query"); }
     per_cu = std::max(per_cu, 1);
     P->grid[l] = std::min(P->class_n[l], n_cu * per_cu);
@@ -693,16 +713,19 @@ int enqueue(const Plan& P, const DevBufs& B, hipStream_t s, const LaunchEvents* 
     e = record(ev ? ev->k0[l] : nullptr);
     if (e != hipSuccess) return device_error(e, "event record");
     const int g = P.grid[l];
-    switch (l) {
-      case 0: sim_kernel<1, kStageOne><<<g, 64, 0, s>>>(a); break;
-      case 1: sim_kernel<2, kStageOne><<<g, 64, 0, s>>>(a); break;
-      case 2: sim_kernel<4, kStageOne><<<g, 64, 0, s>>>(a); break;
-      case 3: sim_kernel<1, kStagePrefill><<<g, 64, 0, s>>>(a); break;
-      case 4: sim_kernel<2, kStagePrefill><<<g, 64, 0, s>>>(a); break;
-      case 5: sim_kernel<4, kStagePrefill><<<g, 64, 0, s>>>(a); break;
-      case 6: sim_kernel<1, kStageDecode><<<g, 64, 0, s>>>(a); break;
-      case 7: sim_kernel<2, kStageDecode><<<g, 64, 0, s>>>(a); break;
-      default: sim_kernel<4, kStageDecode><<<g, 64, 0, s>>>(a); break;
+    switch (l + (P.simple[l] ? 100 : 0)) {
+      case 0: sim_kernel<1, kStageOne, false><<<g, 64, 0, s>>>(a); break;
+      case 1: sim_kernel<2, kStageOne, false><<<g, 64, 0, s>>>(a); break;
+      case 2: sim_kernel<4, kStageOne, false><<<g, 64, 0, s>>>(a); break;
+      case 100: sim_kernel<1, kStageOne, true><<<g, 64, 0, s>>>(a); break;
+      case 101: sim_kernel<2, kStageOne, true><<<g, 64, 0, s>>>(a); break;
+      case 102: sim_kernel<4, kStageOne, true><<<g, 64, 0, s>>>(a); break;
+      case 3: sim_kernel<1, kStagePrefill, false><<<g, 64, 0, s>>>(a); break;
+      case 4: sim_kernel<2, kStagePrefill, false><<<g, 64, 0, s>>>(a); break;
+      case 5: sim_kernel<4, kStagePrefill, false><<<g, 64, 0, s>>>(a); break;
+      case 6: sim_kernel<1, kStageDecode, false><<<g, 64, 0, s>>>(a); break;
+      case 7: sim_kernel<2, kStageDecode, false><<<g, 64, 0, s>>>(a); break;
+      default: sim_kernel<4, kStageDecode, false><<<g, 64, 0, s>>>(a); break;
     }
     e = hipGetLastError();
     if (e != hipSuccess) return device_error(e, "sim kernel launch");

@@ -310,7 +310,7 @@ __device__ __forceinline__ void store_chunk(SlotLds<NCH>& L, Hot& h0, int j, int
 // device of a disaggregated point: requests leave when their prefill
 // completes and their KV crosses the device's link) or kStageDecode (a
 // decode device: requests arrive with their prompt's KV and first token).
-template <int NCH, int MODE>
+template <int NCH, int MODE, bool SIMPLE>
 __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
                                                SlotLds<NCH>& L, QEntry* Q, ReqTimes* RT,
                                                const int lane, const LaneRoof& roofc) {
@@ -318,10 +318,16 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
   const TraceRec* __restrict__ rec = A.recs + P.trace_off;
   const int N = P.n, NB = P.num_blocks, B = P.block, M = P.max_batch, K = P.chunk;
   const bool unlimited = (K == 0);
-  const int64_t cap_tok = P.cap_tokens, cap_prompt = P.cap_prompt;
-  const int policy = P.policy, adm_reserve = P.adm_reserve;
+  // SIMPLE: a one-worker point under continuous batching with recompute
+  // preemption, no admission ratio and no watchdog (the policy state folds
+  // away at compile time)
+  static_assert(!SIMPLE || MODE == kStageOne, "simple points are one-worker points");
+  const int64_t cap_tok = P.cap_tokens, cap_prompt = SIMPLE ? P.cap_tokens : P.cap_prompt;
+  const int policy = SIMPLE ? TS_POLICY_MIXED : P.policy;
+  const int adm_reserve = SIMPLE ? 0 : P.adm_reserve;
   const bool pff = policy == TS_POLICY_PREFILL_FIRST;
-  const bool swap = P.swap != 0;  // preemption by swap instead of recompute
+  const bool swap = SIMPLE ? false : P.swap != 0;  // preemption by swap instead of recompute
+  const uint64_t time_limit = SIMPLE ? 0 : A.time_limit_ticks;
   // a request that could never fit, alone or within the admission ratio (on
   // a prefill device: its prompt here, or the whole request on a decode device)
   auto rejected = [&](int32_t pr, int32_t ou) {
@@ -555,7 +561,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
     }
   };
 
-  const uint64_t clock0 = A.time_limit_ticks ? __builtin_amdgcn_s_memrealtime() : 0;
+  const uint64_t clock0 = time_limit ? __builtin_amdgcn_s_memrealtime() : 0;
   while (status == TS_POINT_OK) {
     // ---- 0. steady stretch.  As long as no request is admitted or
     // preempted and no prefill completes, an iteration advances every decode
@@ -625,7 +631,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       }
       constexpr int64_t kT52 = (int64_t)1 << 52;
       if (n_iters >= A.iter_cap || t >= kT52) go = false;
-      if (A.time_limit_ticks != 0 && (n_iters & 255) == 0) go = false;  // watchdog below
+      if (time_limit != 0 && (n_iters & 255) == 0) go = false;  // watchdog below
       int nchd = (nD + 63) >> 6;
       int nDa = nD, nruna = nrun;  // alive decodes and running requests
       // an admission would find a free slot and token budget (a swapped
@@ -655,11 +661,18 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
         // the iteration cap and the watchdog's clock checks
         int stop_fix = 0x3fffffff;
         if (A.iter_cap - n_iters < (int64_t)stop_fix) stop_fix = (int)(A.iter_cap - n_iters);
-        if (A.time_limit_ticks != 0) {
+        if (time_limit != 0) {
           const int wd = 256 - (int)(n_iters & 255);
           stop_fix = wd < stop_fix ? wd : stop_fix;
         }
-        int dG = 0, seg0 = 0, q = 0, fin_at = 0, stop = 0, stop_hard = 0, cd_seg = 0;
+        // every iteration is below 2^lg_iter ns: this many from the stretch
+        // start keep the fp64 clock below 2^52
+        int stop_hard = stop_fix;
+        {
+          const int64_t ks = (kT52 - t) >> P.lg_iter;
+          if (ks < (int64_t)stop_fix) stop_hard = ks > 0 ? (int)ks : 0;
+        }
+        int dG = 0, seg0 = 0, q = 0, fin_at = 0, stop = 0, cd_seg = 0;
         bool watch = false;
         double Fw = 0.0, Bw = 0.0, dF = 0.0, dB = 0.0;
         double k_t0 = 0.0, k_t3 = 0.0, k_t4 = 0.0, k_t5 = 0.0, k_lm = 0.0;
@@ -711,13 +724,14 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
           if (lane == 2) {
             L.segk[4] = Fw; L.segk[5] = Bw; L.segk[6] = dF; L.segk[7] = dB;
           }
-          // every iteration is below 2^lg_iter ns: this many keep the fp64
-          // clock below 2^52
-          const int64_t ks = (kT52 - (int64_t)rdl_f64(t_d, 1)) >> P.lg_iter;
-          stop_hard = ks < (int64_t)(stop_fix - dG) ? dG + (ks > 0 ? (int)ks : 0) : stop_fix;
           stop = stop_hard;
           if (q > 0) {  // the head prefill completes in iteration kc
-            const int kc = dG + (tgt_p - ctx_p - 1) / q;
+            // floor(n / q) for 0 <= n, q < 2^31: the correctly rounded fp64
+            // quotient is that or one more
+            const int n = tgt_p - ctx_p - 1;
+            int kq = (int)((double)n / (double)q);
+            if ((int64_t)kq * q > (int64_t)n) --kq;
+            const int kc = dG + kq;
             stop = kc < stop ? kc : stop;
           }
           // arrivals matter within the segment only if one could be admitted
@@ -898,8 +912,11 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
               nDa -= nfin;
               nruna -= nfin;
               t = (int64_t)rdl_f64(t_d, 1);  // arrivals up to the clock
-              intake();
-              thr = next < N ? __builtin_fmin((double)rdl64(w_arr, next - wbase), kT52d) : kT52d;
+              if (next < N && rdl64(w_arr, next - wbase) <= t) {
+                intake();
+                thr = next < N ? __builtin_fmin((double)rdl64(w_arr, next - wbase), kT52d)
+                               : kT52d;
+              }
               if (nruna == 0 ||
                   ((npre > 0 || nwait > 0) && adm_open() && !head_blocked(freeb))) {
                 more = false;  // nothing runs, or the freed slot or blocks may admit
@@ -1098,8 +1115,8 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       }
     }
     // watchdog: a point running longer than the wall-clock limit stops
-    if (A.time_limit_ticks != 0 && (n_iters & 255) == 0 &&
-        __builtin_amdgcn_s_memrealtime() - clock0 > A.time_limit_ticks) {
+    if (time_limit != 0 && (n_iters & 255) == 0 &&
+        __builtin_amdgcn_s_memrealtime() - clock0 > time_limit) {
       status = TS_POINT_TIME_LIMIT;
       break;
     }
@@ -1447,7 +1464,8 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       AP += wsum64(l_ap);
     }
     // swap transfers, priced by the host link's bandwidth
-    const double xfer = (double)((int64_t)xblk * P.block_bytes) * P.inv_link_ns;
+    const double xfer =
+        swap ? (double)((int64_t)xblk * P.block_bytes) * P.inv_link_ns : 0.0;
     double iter_d;
     const int64_t iter_ns = iteration_ns(roofc, A.n_layers, iF, iB, nD + TP, TP, AP, CP, nD,
                                          CD, nD + Rc, xfer, P.swap_overlap != 0, &iter_d);
@@ -1581,7 +1599,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
 
 // Persistent grid: each wave64 workgroup takes the next point from a ticket
 // counter until none is left.
-template <int NCH, int MODE>
+template <int NCH, int MODE, bool SIMPLE>
 __global__ __launch_bounds__(64, NCH == 4 ? 4 : 5) void sim_kernel(SimArgs A) {
   __shared__ SlotLds<NCH> L;
   const int lane = lane_id();
@@ -1608,19 +1626,22 @@ __global__ __launch_bounds__(64, NCH == 4 ? 4 : 5) void sim_kernel(SimArgs A) {
     const unsigned old = atomicAdd(A.counter, lane == 0 ? 1u : 0u);
     const int tk = __builtin_amdgcn_readfirstlane((int)old);
     if (tk >= A.n_order) break;
-    simulate_point<NCH, MODE>(A, A.order[tk], L, Q, RT, lane, roofc);
+    simulate_point<NCH, MODE, SIMPLE>(A, A.order[tk], L, Q, RT, lane, roofc);
   }
 }
 
-template __global__ void sim_kernel<1, kStageOne>(SimArgs);
-template __global__ void sim_kernel<2, kStageOne>(SimArgs);
-template __global__ void sim_kernel<4, kStageOne>(SimArgs);
-template __global__ void sim_kernel<1, kStagePrefill>(SimArgs);
-template __global__ void sim_kernel<2, kStagePrefill>(SimArgs);
-template __global__ void sim_kernel<4, kStagePrefill>(SimArgs);
-template __global__ void sim_kernel<1, kStageDecode>(SimArgs);
-template __global__ void sim_kernel<2, kStageDecode>(SimArgs);
-template __global__ void sim_kernel<4, kStageDecode>(SimArgs);
+template __global__ void sim_kernel<1, kStageOne, false>(SimArgs);
+template __global__ void sim_kernel<2, kStageOne, false>(SimArgs);
+template __global__ void sim_kernel<4, kStageOne, false>(SimArgs);
+template __global__ void sim_kernel<1, kStageOne, true>(SimArgs);
+template __global__ void sim_kernel<2, kStageOne, true>(SimArgs);
+template __global__ void sim_kernel<4, kStageOne, true>(SimArgs);
+template __global__ void sim_kernel<1, kStagePrefill, false>(SimArgs);
+template __global__ void sim_kernel<2, kStagePrefill, false>(SimArgs);
+template __global__ void sim_kernel<4, kStagePrefill, false>(SimArgs);
+template __global__ void sim_kernel<1, kStageDecode, false>(SimArgs);
+template __global__ void sim_kernel<2, kStageDecode, false>(SimArgs);
+template __global__ void sim_kernel<4, kStageDecode, false>(SimArgs);
 
 // ------------------------------------------------------------ statistics
 // Nearest-rank percentiles of the finished requests' latencies: the k-th

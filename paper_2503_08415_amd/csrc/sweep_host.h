@@ -37,6 +37,7 @@ struct Plan {
   std::vector<PointInfo> pinfo;  // per design point: its trace (statistics kernel)
   int class_off[kLaunches] = {}, class_n[kLaunches] = {};
   int grid[kLaunches] = {};     // persistent workgroups per launch
+  bool simple[kLaunches] = {};  // the launch's points are all simple (compile-time policy)
   int stats_grid = 1;
   int max_grid() const;
 };
