@@ -45,7 +45,8 @@ constexpr int kClassChunks[kClasses] = {1, 2, 4};
 
 // The kernel of launch 3 * stage + class; one-worker launches whose points
 // are all simple (continuous batching, recompute preemption, no admission
-// ratio, no watchdog) use the variant with that policy fixed at compile time.
+// ratio, no request that could never fit, no watchdog) use the variant with
+// that policy fixed at compile time.
 const void* sim_kernel_fn(int launch, bool simple) {
   const int st = launch / kClasses, c = launch % kClasses;
   if (st == kStageOne && simple) {
@@ -588,7 +589,7 @@ int make_plan(const ts_model* model, const ts_trace* traces, int32_t n_traces,
     for (const int32_t u : cls) {
       const DevPoint& d = dp[(size_t)u];
       simple = simple && d.policy == TS_POLICY_MIXED && d.swap == 0 && d.adm_reserve == 0 &&
-               d.cap_prompt == d.cap_tokens;
+               d.cap_prompt == d.cap_tokens && d.may_reject == 0;
     }
     P->simple[l] = simple;
     order.insert(order.end(), cls.begin(), cls.end());

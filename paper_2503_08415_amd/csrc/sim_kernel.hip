@@ -319,8 +319,8 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
   const int N = P.n, NB = P.num_blocks, B = P.block, M = P.max_batch, K = P.chunk;
   const bool unlimited = (K == 0);
   // SIMPLE: a one-worker point under continuous batching with recompute
-  // preemption, no admission ratio and no watchdog (the policy state folds
-  // away at compile time)
+  // preemption, no admission ratio, no request that could never fit and no
+  // watchdog (the policy state folds away at compile time)
   static_assert(!SIMPLE || MODE == kStageOne, "simple points are one-worker points");
   const int64_t cap_tok = P.cap_tokens, cap_prompt = SIMPLE ? P.cap_tokens : P.cap_prompt;
   const int policy = SIMPLE ? TS_POLICY_MIXED : P.policy;
@@ -328,6 +328,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
   const bool pff = policy == TS_POLICY_PREFILL_FIRST;
   const bool swap = SIMPLE ? false : P.swap != 0;  // preemption by swap instead of recompute
   const uint64_t time_limit = SIMPLE ? 0 : A.time_limit_ticks;
+  const bool may_reject = SIMPLE ? false : P.may_reject != 0;  // some request never fits
   // a request that could never fit, alone or within the admission ratio (on
   // a prefill device: its prompt here, or the whole request on a decode device)
   auto rejected = [&](int32_t pr, int32_t ou) {
@@ -368,7 +369,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
   int n_rej = 0;
 
   // Requests that could never fit are rejected up front.
-  if (P.may_reject) {
+  if (may_reject) {
     for (int base = 0; base < N; base += 64) {
       const int i = base + lane;
       bool rj = false;
@@ -416,7 +417,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       const int nn = wbase + cnt;
       if (nn > next) {
         int add = nn - next;
-        if (P.may_reject) {
+        if (may_reject) {
           const bool rj = lane >= next - wbase && lane < cnt && w_rj != 0;
           add -= popc(ballot(rj));
         }
@@ -678,7 +679,9 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
         double k_t0 = 0.0, k_t3 = 0.0, k_t4 = 0.0, k_t5 = 0.0, k_lm = 0.0;
         const double kT52d = 4503599627370496.0;
         double thr = next < N ? __builtin_fmin((double)rdl64(w_arr, next - wbase), kT52d) : kT52d;
-        double t_d = (double)t, ub = ubns, it = 0.0, em = 0.0;
+        // the clock (fp64, exact below 2^53), this lane's share of the
+        // stretch's used-block integral, the last and the largest iteration
+        double t_d = (double)t, ubl = 0.0, it = 0.0, em = 0.0;
         // Segment set-up at iteration dG: the alive decodes' first finishing
         // iteration and key sum, the head prefill's chunk, every operator's
         // work and its per-iteration step, and the segment's last iteration.
@@ -825,26 +828,13 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
                 Kb = k < Kb ? k : Kb;
               }
               const int last = Kb - 1;
-              // the used-block integral: one fp64 sum in iteration order; when
-              // every term and the total stay below 2^53 it is an exact
-              // integer sum, and any order gives it
+              // the used-block integral: each lane keeps its iterations' terms
+              // (summed over the wave when the stretch ends; an fp64 sum in
+              // another order than the sequential one, within 1e-9 of it)
               const double pv = (double)(NB - freeb + T) * itv;
-              const double ub0 = rdl_f64(ub, 1);
-              constexpr double kT53d = 9007199254740992.0;
-              double ubn = ub0;
-              bool exact = ub0 < kT53d && ballot(lane < Kb && !(pv < kT53d)) == 0;
-              if (exact) {
-                // integer terms: the tree sum is exact exactly when the true
-                // total stays below 2^53 (rounding is monotone, 2^53 exact)
-                const double sum = ub0 + rdl_f64(scan_f64(lane < Kb ? pv : 0.0), 63);
-                exact = sum < kT53d;
-                if (exact) ubn = sum;
-              }
-              if (!exact)
-                for (int k = 0; k < Kb; ++k) ubn = ubn + rdl_f64(pv, k);
+              ubl = ubl + (lane < Kb ? pv : 0.0);
               freeb -= rdl(T, last);
               t_d = rdl_f64(tend, last);
-              ub = ubn;
               it = rdl_f64(itv, last);
               const double kd = (double)Kb;
               Fw = Fw + kd * dF;
@@ -875,7 +865,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
             double tot = A.n_layers * lay;
             tot = tot + k_lm;
             it = __builtin_fmax(ceil(tot), 1.0);
-            ub = ub + used_d * it;
+            ubl = ubl + (lane == 1 ? used_d * it : 0.0);  // the layer sum runs in lane 1
             t_d = t_d + it;
             Fw = Fw + dF;
             Bw = Bw + dB;
@@ -951,7 +941,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
                 (R1 > 0 || (swap && npre > 0))) {
               if (npre > 0 || nrun >= 64 * NCH) break;  // queue candidates, full slots
               const TraceRec r = rec[next_new];
-              if (P.may_reject && rejected(r.prompt, r.output)) break;
+              if (may_reject && rejected(r.prompt, r.output)) break;
               need_h = divB(r.prompt + B - 1);
               if (need_h > freeb - nneed - adm_reserve) {
                 head_need = need_h;  // the head waits for blocks
@@ -981,7 +971,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
                                                  &iter_d);
             const int64_t t_beg = t;
             const int64_t t_end = t_beg + iter_ns;
-            ub = ub + (double)(NB - freeb) * iter_d;
+            ubl = ubl + (lane == 1 ? (double)(NB - freeb) * iter_d : 0.0);
             t_d = t_d + iter_d;
             if (NB - freeb > peak) peak = NB - freeb;
             pf_tok += TP;
@@ -1083,7 +1073,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
         close_segment();
         em = __builtin_fmax(em, it);
         t = (int64_t)rdl_f64(t_d, 1);
-        ubns = rdl_f64(ub, 1);
+        ubns = ubns + rdl_f64(scan_f64(ubl), 63);
         n_iters += dG;
         const int64_t gx = (int64_t)rdl_f64(em, 1);
 #pragma unroll
@@ -1150,7 +1140,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
         tgt_h = qc > qt ? qc : qt;
       } else {
         int i = next_new;  // the first candidate that is not rejected
-        while (P.may_reject && i < next - 1 && rejected(rec[i].prompt, rec[i].output)) ++i;
+        while (may_reject && i < next - 1 && rejected(rec[i].prompt, rec[i].output)) ++i;
         tgt_h = rec[i].prompt;
       }
       pf_iter = divB(tgt_h + B - 1) <= freeb - (npre > 0 ? 0 : adm_reserve);
@@ -1325,7 +1315,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
             const TraceRec r = rec[idx];
             c_tgt = r.prompt;
             c_rem = MODE == kStagePrefill ? 1 : r.output;  // a prefill device runs no decode
-            if (P.may_reject && rejected(r.prompt, r.output)) valid = false;
+            if (may_reject && rejected(r.prompt, r.output)) valid = false;
           }
           if constexpr (MODE == kStageDecode) {  // arrives with its prompt's KV, first token out
             c_ctx = c_tgt;
@@ -1556,7 +1546,7 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       if (k0 + lane < npre) RR[gid_of(Q[(qhead + k0 + lane) & (kQueueCap - 1)].id)] = o;
     for (int i0 = next_new; i0 < N; i0 += 64) {
       const int i = i0 + lane;
-      if (i < N && !(P.may_reject && rejected(rec[i].prompt, rec[i].output))) RR[gid_of(i)] = o;
+      if (i < N && !(may_reject && rejected(rec[i].prompt, rec[i].output))) RR[gid_of(i)] = o;
     }
   }
 
