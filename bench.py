@@ -98,11 +98,6 @@ def algorithmic_instructions(out):
     return U_ITER * out["n_iters"].astype(np.float64)
 
 
-def kernel_class(max_batch):
-    mb = np.asarray(max_batch)
-    return np.where(mb <= 64, 0, np.where(mb <= 128, 1, 2))
-
-
 def cpu_model() -> str:
     try:
         with open("/proc/cpuinfo") as f:
@@ -223,7 +218,7 @@ def main():
         torch.cuda.synchronize()
         log("warmup %d: %.3fs" % (i, time.perf_counter() - t0))
 
-    step_s, sim_ms, stats_ms, kms = [], [], [], []
+    step_s, sim_ms, stats_ms, kms, kwork = [], [], [], [], []
     torch.cuda.synchronize()
     t_all = time.perf_counter()
     for i in range(args.steps):
@@ -235,6 +230,7 @@ def main():
         sim_ms.append(a)
         stats_ms.append(b)
         kms.append([k[0] for k in sw.kernel_timing()])
+        kwork.append(sw.kernel_work())
         log("step %d: %.3fs (simulation %.1f ms, statistics %.1f ms, kernels %s)"
             % (i, step_s[-1], a, b, ["%.1f" % x for x in kms[-1]]))
     torch.cuda.synchronize()
@@ -253,13 +249,15 @@ def main():
     # so with any such point the figure covers all simulation launches
     kmean = np.mean(np.array(kms), axis=0)
     disagg = "n_prefill" in points and bool((np.asarray(points["n_prefill"]) > 0).any())
-    cls = kernel_class(points["max_batch"])
     w = algorithmic_instructions(out)
+    # iterations each launch simulated to completion (a point handed from the
+    # 64-slot launch to a wider one counts only where it completed)
+    work = np.array(kwork[-1], dtype=np.float64)
     if disagg:
         name, w_k, k_ms, traffic = "all simulation launches", float(w.sum()), float(kmean.sum()), None
     else:
         k = int(np.argmax(kmean))
-        name, w_k, k_ms = KERNEL_NAMES[k], float(w[cls == k].sum()), float(kmean[k])
+        name, w_k, k_ms = KERNEL_NAMES[k], U_ITER * float(work[k]), float(kmean[k])
         traffic = recorded_traffic(args.config, name)
     achieved = w_k / (k_ms * 1e-3)
     roofline = {"bound": "alu", "achieved": achieved / 1e9, "peak": VALU_ISSUE_PEAK / 1e9,
@@ -284,9 +282,8 @@ def main():
         "results_copy_ms": 1e3 * results_s,
         "frac_step": float(w.sum()) / (ms_per_step * 1e-3) / VALU_ISSUE_PEAK,
         "simulated_iterations": int(out["n_iters"].sum()),
-        "simulated_iterations_by_kernel": (
-            {} if disagg else {KERNEL_NAMES[i]: int(out["n_iters"][cls == i].sum())
-                               for i in range(3) if (cls == i).any()}),
+        "simulated_iterations_by_kernel": {KERNEL_NAMES[i]: int(work[i])
+                                           for i in range(len(work)) if work[i] > 0},
         "point_status_counts": status,
     }
     parity_ok = True

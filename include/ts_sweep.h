@@ -265,10 +265,24 @@ int ts_sweep_timing(ts_sweep *h, float *sim_ms, float *stats_ms);
  * devices and 2 for the decode devices of disaggregated points, class 0, 1,
  * 2 for max_batch <= 64, <= 128, <= 256.  ms[k] receives launch k's duration
  * in milliseconds from HIP events recorded around it on that stream (0 when
- * it has no work) and n_points[k] its number of simulated workers.  Waits
- * for the run.  TS_ERR_STATE before the first run. */
+ * it has no work) and n_points[k] its number of simulated workers (with the
+ * hand-over described at ts_sweep_kernel_work: for k = 0 every one-worker
+ * point, for k = 1, 2 the most it may be handed).  Waits for the run.
+ * TS_ERR_STATE before the first run. */
 #define TS_N_SIM_KERNELS 9
 int ts_sweep_kernel_timing(ts_sweep *h, float *ms, int32_t *n_points);
+
+/* Simulated iterations per launch of the last run: iters[k] receives the
+ * summed iteration counts of the points launch k simulated to completion
+ * (index as for ts_sweep_kernel_timing).  When every one-worker point is a
+ * simple one (continuous batching, recompute preemption, no admission ratio,
+ * no request that could never fit, no watchdog) and some allow more than 64
+ * running requests, the max_batch <= 64 launch (k = 0) takes all of them
+ * while at most 64 run at once; a point that needs more slots is handed to
+ * the launch of its own class (k = 1 or 2) and simulated again there from
+ * the start, which alone counts its iterations.  Waits for the run.
+ * TS_ERR_STATE before the first run. */
+int ts_sweep_kernel_work(ts_sweep *h, int64_t *iters);
 
 /* For callers that cannot allocate device memory (tight serving loops,
  * harnesses that forbid hipMalloc): the whole sweep of ts_sweep_create +

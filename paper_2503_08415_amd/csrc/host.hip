@@ -32,7 +32,7 @@ __global__ void stats_kernel(ts_req_result* rec, const TraceRec* recs, const Poi
                              ts_point_result* res, int64_t* e2e, int64_t* ttft, int max_n,
                              int n_points, int64_t slo_ttft_ns, int64_t slo_tpot_ns,
                              int pad_pending);
-__global__ void reset_counters_kernel(unsigned int* c, int n);
+__global__ void reset_counters_kernel(unsigned int* c, int n, unsigned long long* w, int nw);
 }  // namespace tsw
 
 using namespace tsw;
@@ -221,7 +221,9 @@ BufCounts buf_counts(const Plan& P) {
   c.recs = P.recs.size();
   c.points = P.dp.size();
   c.order = P.order.size();
-  c.counter = kLaunches;
+  c.counter = kLaunches + 2;  // tickets per launch, handed points per wider class
+  c.handed = P.hand_over ? (size_t)(P.class_n[1] + P.class_n[2]) : 0;
+  c.work = kLaunches;
   c.queue = (size_t)P.max_grid() * kQueueCap;
   c.times = (size_t)P.max_grid() * per_point;
   c.res = (size_t)(P.count + P.n_extra);
@@ -242,7 +244,8 @@ double BufCounts::bytes() const {
          (double)res * sizeof(ts_point_result) + (double)req * sizeof(ts_req_result) +
          2.0 * (double)lat * sizeof(int64_t) + (double)pd * sizeof(PdAux) +
          2.0 * (double)s1 * sizeof(int64_t) + (double)sub * (sizeof(int64_t) + sizeof(int32_t)) +
-         (double)gids * sizeof(int32_t) + (double)pinfo * sizeof(PointInfo);
+         (double)gids * sizeof(int32_t) + (double)pinfo * sizeof(PointInfo) +
+         (double)handed * sizeof(int32_t) + (double)work * sizeof(unsigned long long);
 }
 
 }  // namespace tsw
@@ -277,6 +280,8 @@ void release(ts_sweep* h) {
   (void)hipFree(b.sub_gid);
   (void)hipFree(b.gids);
   (void)hipFree(b.pinfo);
+  (void)hipFree(b.handed);
+  (void)hipFree(b.work);
   for (int c = 0; c < kLaunches; ++c) {
     if (h->ev.k0[c]) (void)hipEventDestroy(h->ev.k0[c]);
     if (h->ev.k1[c]) (void)hipEventDestroy(h->ev.k1[c]);
@@ -594,6 +599,24 @@ int make_plan(const ts_model* model, const ts_trace* traces, int32_t n_traces,
     P->simple[l] = simple;
     order.insert(order.end(), cls.begin(), cls.end());
   }
+  // One-worker points wider than 64 slots that are simple run first in the
+  // 64-slot launch (more waves per SIMD, fewer registers) while at most 64
+  // run at once; the few that need more are handed to their own class's
+  // launch and simulated again there from the start.
+  bool all_simple = true;
+  for (int c = 0; c < kClasses; ++c)
+    all_simple = all_simple && (P->class_n[c] == 0 || P->simple[c]);
+  if (all_simple && P->class_n[1] + P->class_n[2] > 0) {
+    std::vector<int32_t> all(order.begin(), order.begin() + P->class_n[0] + P->class_n[1] +
+                                                               P->class_n[2]);
+    std::stable_sort(all.begin(), all.end(),
+                     [&](int32_t a, int32_t b) { return est[(size_t)a] > est[(size_t)b]; });
+    std::copy(all.begin(), all.end(), order.begin());
+    P->class_off[0] = 0;
+    P->class_n[0] = (int)all.size();
+    P->simple[0] = true;
+    P->hand_over = true;
+  }
   P->count = count;
   P->n_pd = (int32_t)aux.size();
   P->max_n = (int32_t)std::max<int64_t>(max_n, 1);
@@ -678,7 +701,7 @@ int enqueue(const Plan& P, const DevBufs& B, hipStream_t s, const LaunchEvents* 
   };
   hipError_t e = record(ev ? ev->t0 : nullptr);
   if (e != hipSuccess) return device_error(e, "event record");
-  reset_counters_kernel<<<1, 64, 0, s>>>(B.counter, kLaunches);
+  reset_counters_kernel<<<1, 64, 0, s>>>(B.counter, kLaunches + 2, B.work, kLaunches);
   SimArgs a;
   a.recs = B.recs;
   a.points = B.points;
@@ -688,6 +711,12 @@ int enqueue(const Plan& P, const DevBufs& B, hipStream_t s, const LaunchEvents* 
   a.res = B.res;
   a.rec = B.req;
   a.iter_cap = P.iter_cap;
+  a.work = nullptr;
+  a.handed = B.handed;
+  a.handed_off[0] = 0;
+  a.handed_off[1] = P.class_n[1];
+  a.handed_n = B.counter + kLaunches;
+  a.n_dev = nullptr;
   a.time_limit_ticks = (uint64_t)P.time_limit_ms * 100000ull;  // 100 MHz clock
   a.n_layers = P.coef.n_layers;
   a.lc = P.lc;
@@ -710,7 +739,13 @@ int enqueue(const Plan& P, const DevBufs& B, hipStream_t s, const LaunchEvents* 
     if (P.class_n[l] == 0) continue;
     a.order = B.order + P.class_off[l];
     a.n_order = P.class_n[l];
+    a.n_dev = nullptr;
+    if (P.hand_over && (l == 1 || l == 2)) {  // the points launch 0 handed over
+      a.order = B.handed + a.handed_off[l - 1];
+      a.n_dev = B.counter + kLaunches + (l - 1);
+    }
     a.counter = B.counter + l;
+    a.work = B.work + l;
     e = record(ev ? ev->k0[l] : nullptr);
     if (e != hipSuccess) return device_error(e, "event record");
     const int g = P.grid[l];
@@ -807,6 +842,8 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
   if (ae == hipSuccess) ae = dev_alloc(&b.ttft, n.lat);
   if (ae == hipSuccess) ae = dev_alloc(&b.req, n.req);
   if (ae == hipSuccess) ae = dev_alloc(&b.pinfo, n.pinfo);
+  if (ae == hipSuccess) ae = dev_alloc(&b.handed, n.handed);
+  if (ae == hipSuccess) ae = dev_alloc(&b.work, n.work);
   if (ae == hipSuccess) ae = dev_alloc(&b.pd, n.pd);
   if (ae == hipSuccess) ae = dev_alloc(&b.s1_admit, n.s1);
   if (ae == hipSuccess) ae = dev_alloc(&b.s1_first, n.s1);
@@ -911,6 +948,17 @@ int ts_sweep_kernel_timing(ts_sweep* h, float* ms, int32_t* n_points) {
     if (h->P.class_n[c] > 0) e = hipEventElapsedTime(&ms[c], h->ev.k0[c], h->ev.k1[c]);
   }
   if (e != hipSuccess) return device_error(e, "event timing");
+  return TS_OK;
+}
+
+int ts_sweep_kernel_work(ts_sweep* h, int64_t* iters) {
+  if (!h || !iters) return TS_ERR_ARG;
+  if (!h->ran) return TS_ERR_STATE;
+  hipError_t e = hipSetDevice(h->P.device);
+  if (e == hipSuccess) e = hipEventSynchronize(h->ev.t2);
+  if (e == hipSuccess)
+    e = hipMemcpy(iters, h->B.work, kLaunches * sizeof(int64_t), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return device_error(e, "copy launch work");
   return TS_OK;
 }
 

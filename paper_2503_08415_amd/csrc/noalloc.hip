@@ -84,6 +84,8 @@ size_t carve(const tsw::Plan& P, unsigned char* base, tsw::DevBufs* B) {
   b.sub_gid = c.take<int32_t>(n.sub);
   b.gids = c.take<int32_t>(n.gids);
   b.pinfo = c.take<tsw::PointInfo>(n.pinfo);
+  b.handed = c.take<int32_t>(n.handed);
+  b.work = c.take<unsigned long long>(n.work);
   if (B) *B = b;
   return c.used;
 }

@@ -255,6 +255,8 @@ __device__ __forceinline__ int64_t iteration_ns(const LaneRoof& c, double n_laye
 //   gap   largest interval between consecutive tokens so far
 // Held blocks are (max(ctx, tgt) + room) / block and are never stored.
 enum : int { FL_FIRST = 1, FL_STALE = 2, FL_IDLE = 4 };
+// internal point status: the point is handed to a launch with more slots
+constexpr int kHandOver = -1;
 
 struct Hot {
   int ctx, tgt, rem, room, fl, q;
@@ -310,8 +312,11 @@ __device__ __forceinline__ void store_chunk(SlotLds<NCH>& L, Hot& h0, int j, int
 // device of a disaggregated point: requests leave when their prefill
 // completes and their KV crosses the device's link) or kStageDecode (a
 // decode device: requests arrive with their prompt's KV and first token).
+// Returns false when the point needs more slots than this kernel holds (a
+// narrow launch taking wider points): its simulation is abandoned, nothing
+// it wrote is final, and a wider launch simulates it again from the start.
 template <int NCH, int MODE, bool SIMPLE>
-__device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
+__device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
                                                SlotLds<NCH>& L, QEntry* Q, ReqTimes* RT,
                                                const int lane, const LaneRoof& roofc) {
   const DevPoint P = A.points[pidx];
@@ -1351,6 +1356,10 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
           head_need = rdl(need, (int)__builtin_ctzll(vm));
           break;
         }
+        if (nrun + a > 64 * NCH) {  // more running requests than this kernel's slots
+          status = kHandOver;
+          break;
+        }
         const int last_lane = 63 - (int)__builtin_clzll(am);
         const int qv =
             (swin || darr) ? 0 : (unlimited ? c_tgt : (c_tgt < R - ET ? c_tgt : R - ET));
@@ -1411,6 +1420,8 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
       nch = (nrun + 63) >> 6;
       nch = nch < NCH ? nch : NCH;
     }
+
+    if (status == kHandOver) break;
 
     // ---- 6. batch sums and the roofline iteration time (paused decodes of a
     // prefill-first iteration and requests swapped in now take no part)
@@ -1532,6 +1543,8 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
     t = t_end;
   }
 
+  if (status == kHandOver) return false;
+
   // ---- a point stopped early (iteration cap, watchdog): the requests it
   // has not finished keep "pending" records: the running ones, the
   // preempted ones in the queue, and those never admitted (from next_new on)
@@ -1585,6 +1598,10 @@ __device__ __forceinline__ void simulate_point(const SimArgs& A, const int pidx,
     o.slo_tpot_ok = 0;
     A.res[oi] = o;
   }
+  // the iterations this launch simulated to completion (every lane adds, lane
+  // 0 the count: no lane-dependent branch)
+  atomicAdd(A.work, (unsigned long long)(lane == 0 ? n_iters : 0));
+  return true;
 }
 
 // Persistent grid: each wave64 workgroup takes the next point from a ticket
@@ -1609,14 +1626,25 @@ __global__ __launch_bounds__(64, NCH == 4 ? 4 : 5) void sim_kernel(SimArgs A) {
   roofc.is_attp = lane == 1;
   roofc.is_attd = lane == 2;
   roofc.is_lm = lane == 6;
+  // the points of this launch: a host-side count, or the count of points a
+  // narrow launch handed over (written before this launch started)
+  const int n_order =
+      A.n_dev ? __builtin_amdgcn_readfirstlane((int)*A.n_dev) : A.n_order;
   // A workgroup never needs more tickets than there are points.
-  for (int taken = 0; taken <= A.n_order; ++taken) {
+  for (int taken = 0; taken <= n_order; ++taken) {
     // All lanes take part (lane 0 adds 1, the others 0) so the ticket is
     // read by the whole wave without a lane-dependent branch.
     const unsigned old = atomicAdd(A.counter, lane == 0 ? 1u : 0u);
     const int tk = __builtin_amdgcn_readfirstlane((int)old);
-    if (tk >= A.n_order) break;
-    simulate_point<NCH, MODE, SIMPLE>(A, A.order[tk], L, Q, RT, lane, roofc);
+    if (tk >= n_order) break;
+    const int pidx = A.order[tk];
+    if (!simulate_point<NCH, MODE, SIMPLE>(A, pidx, L, Q, RT, lane, roofc)) {
+      // hand the point to the launch of its own slot class (every lane
+      // stores the same index)
+      const int wc = A.points[pidx].max_batch <= 128 ? 0 : 1;
+      const unsigned slot = atomicAdd(A.handed_n + wc, lane == 0 ? 1u : 0u);
+      A.handed[A.handed_off[wc] + __builtin_amdgcn_readfirstlane((int)slot)] = pidx;
+    }
   }
 }
 
@@ -1893,8 +1921,9 @@ __global__ __launch_bounds__(256) void pd_combine_kernel(const PdAux* aux, int n
 
 // Work-queue counters are cleared by a kernel (no memset node in a captured
 // stream).
-__global__ void reset_counters_kernel(unsigned int* c, int n) {
+__global__ void reset_counters_kernel(unsigned int* c, int n, unsigned long long* w, int nw) {
   if ((int)threadIdx.x < n) c[threadIdx.x] = 0u;
+  if ((int)threadIdx.x < nw) w[threadIdx.x] = 0ull;
 }
 
 }  // namespace tsw

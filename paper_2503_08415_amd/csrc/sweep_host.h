@@ -38,13 +38,18 @@ struct Plan {
   int class_off[kLaunches] = {}, class_n[kLaunches] = {};
   int grid[kLaunches] = {};     // persistent workgroups per launch
   bool simple[kLaunches] = {};  // the launch's points are all simple (compile-time policy)
+  // The one-worker points are all simple and some are wider than 64 slots:
+  // launch 0 takes every one-worker point and hands those needing more than
+  // 64 running slots to launch 1 or 2 (class_n[1], class_n[2] bound them).
+  bool hand_over = false;
   int stats_grid = 1;
   int max_grid() const;
 };
 
 // Element counts of every device buffer of a plan.
 struct BufCounts {
-  size_t recs, points, order, counter, queue, times, res, req, lat, pd, s1, sub, gids, pinfo;
+  size_t recs, points, order, counter, queue, times, res, req, lat, pd, s1, sub, gids, pinfo,
+      handed, work;
   double bytes() const;  // total, in bytes
 };
 BufCounts buf_counts(const Plan& P);
@@ -55,7 +60,9 @@ struct DevBufs {
   TraceRec* recs = nullptr;
   DevPoint* points = nullptr;
   int32_t* order = nullptr;
-  unsigned int* counter = nullptr;  // work-queue tickets, one per launch
+  unsigned int* counter = nullptr;  // work-queue tickets, one per launch, then the handed counts
+  unsigned long long* work = nullptr;  // simulated iterations completed per launch
+  int32_t* handed = nullptr;        // points handed from launch 0 to launches 1 and 2
   QEntry* queue = nullptr;          // kQueueCap per workgroup, shared by the launches
   ReqTimes* times = nullptr;        // max_n per workgroup, shared by the launches
   ts_point_result* res = nullptr;

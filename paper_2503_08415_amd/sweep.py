@@ -74,7 +74,8 @@ POINT_DTYPE = np.dtype([
 
 # every entry point declared in include/ts_sweep.h
 EXPORTS = ("ts_sweep_create", "ts_sweep_run", "ts_sweep_results", "ts_sweep_shape",
-           "ts_sweep_timing", "ts_sweep_kernel_timing", "ts_sweep_run_static",
+           "ts_sweep_timing", "ts_sweep_kernel_timing", "ts_sweep_kernel_work",
+           "ts_sweep_run_static",
            "ts_sweep_destroy", "ts_status_str")
 STATIC_SCRATCH_BYTES = 64 << 20  # TS_STATIC_SCRATCH_BYTES
 # simulation launches, 3 * stage + class: stages one-worker points, prefill
@@ -114,6 +115,8 @@ def lib():
         L.ts_sweep_kernel_timing.argtypes = [C.c_void_p, C.POINTER(C.c_float),
                                              C.POINTER(C.c_int32)]
         L.ts_sweep_kernel_timing.restype = C.c_int
+        L.ts_sweep_kernel_work.argtypes = [C.c_void_p, C.POINTER(C.c_int64)]
+        L.ts_sweep_kernel_work.restype = C.c_int
         L.ts_sweep_run_static.argtypes = [C.POINTER(Model), C.POINTER(Trace), C.c_int32,
                                           C.POINTER(Point), C.c_int32, C.POINTER(Options),
                                           C.c_void_p, C.c_void_p, C.c_void_p]
@@ -240,6 +243,12 @@ class Sweep:
         n = (C.c_int32 * N_SIM_KERNELS)()
         _check(lib().ts_sweep_kernel_timing(self._h, ms, n), "ts_sweep_kernel_timing")
         return [(ms[k], n[k]) for k in range(N_SIM_KERNELS)]
+
+    def kernel_work(self):
+        """Per simulation kernel: simulated iterations of the points it completed."""
+        it = (C.c_int64 * N_SIM_KERNELS)()
+        _check(lib().ts_sweep_kernel_work(self._h, it), "ts_sweep_kernel_work")
+        return [int(it[k]) for k in range(N_SIM_KERNELS)]
 
     def close(self):
         if self._h:

@@ -530,3 +530,44 @@ def test_edge_cases(S, oracle):
     compare_points(g_cap, o_cap, "iter cap")
     compare_requests(g_rq, o_rq, "iter cap")
     assert (g_cap["status"][[1, 2, 3, 6]] == 2).all()
+
+
+def test_hand_over_to_wider_kernels(S, oracle):
+    """Simple one-worker points with room for more than 64 running requests
+    first run in the 64-slot kernel; those that need more slots (bursts of
+    300 arrivals) are handed to the 128- or 256-slot kernel and simulated
+    again there.  Every request against the oracle, and the launches'
+    completed iterations add up to the oracle's."""
+    m = W.MODELS["llama2-7b"]
+    rng = np.random.default_rng(3)
+    burst = {"arrival_ns": np.zeros(300, np.int64),
+             "prompt_len": rng.integers(16, 200, 300).astype(np.int32),
+             "output_len": rng.integers(5, 60, 300).astype(np.int32)}
+    n = 400
+    spread = {"arrival_ns": np.sort(rng.integers(0, 3_000_000_000, n)).astype(np.int64),
+              "prompt_len": rng.integers(16, 2000, n).astype(np.int32),
+              "output_len": rng.integers(5, 300, n).astype(np.int32)}
+    rows = [(256, 0, 0), (100, 0, 0), (64, 0, 0), (256, 512, 0), (130, 256, 1), (256, 0, 1),
+            (80, 0, 1), (256, 1024, 1)]
+    k = len(rows)
+    pts = {"peak_flops": np.full(k, 312e12), "mem_bw": np.full(k, 2e12),
+           "capacity_bytes": np.full(k, 80_000_000_000, np.int64),
+           "mem_util_permille": np.full(k, 900, np.int32), "block_size": np.full(k, 16, np.int32),
+           "max_batch": np.array([r[0] for r in rows], np.int32),
+           "chunk_size": np.array([r[1] for r in rows], np.int32),
+           "trace_id": np.array([r[2] for r in rows], np.int32)}
+    traces = [burst, spread]
+    o_out, o_req = oracle.run_points(m, traces, pts, per_request=True)
+    sw = S.Sweep(m, traces, pts, per_request=True, iter_cap=cap_from(o_out))
+    try:
+        sw.run()
+        out, req = sw.results()
+        work = sw.kernel_work()
+        per_launch = [kt[1] for kt in sw.kernel_timing()]
+    finally:
+        sw.close()
+    compare_points(out, o_out, "hand-over")
+    compare_requests(req, o_req, "hand-over")
+    assert per_launch[0] == k  # the 64-slot launch takes every point
+    assert work[1] > 0 and work[2] > 0  # bursts were handed to both wider kernels
+    assert sum(work) == int(o_out["n_iters"].sum())
