@@ -279,8 +279,9 @@ int ts_sweep_kernel_timing(ts_sweep *h, float *ms, int32_t *n_points);
  * no request that could never fit, no watchdog) and some allow more than 64
  * running requests, the max_batch <= 64 launch (k = 0) takes all of them
  * while at most 64 run at once; a point that needs more slots is handed to
- * the launch of its own class (k = 1 or 2) and simulated again there from
- * the start, which alone counts its iterations.  Waits for the run.
+ * the 128-slot launch (k = 1), and from there, if it needs more than 128, to
+ * the 256-slot launch (k = 2), each time simulated again from the start;
+ * only the launch that completes it counts its iterations.  Waits for the run.
  * TS_ERR_STATE before the first run. */
 int ts_sweep_kernel_work(ts_sweep *h, int64_t *iters);
 

@@ -222,6 +222,8 @@ BufCounts buf_counts(const Plan& P) {
   c.points = P.dp.size();
   c.order = P.order.size();
   c.counter = kLaunches + 2;  // tickets per launch, handed points per wider class
+  // the 64-slot launch hands at most class_n[1] points on, the 128-slot one
+  // at most class_n[2]
   c.handed = P.hand_over ? (size_t)(P.class_n[1] + P.class_n[2]) : 0;
   c.work = kLaunches;
   c.queue = (size_t)P.max_grid() * kQueueCap;
@@ -601,8 +603,9 @@ int make_plan(const ts_model* model, const ts_trace* traces, int32_t n_traces,
   }
   // One-worker points wider than 64 slots that are simple run first in the
   // 64-slot launch (more waves per SIMD, fewer registers) while at most 64
-  // run at once; the few that need more are handed to their own class's
-  // launch and simulated again there from the start.
+  // run at once; the few that need more are handed to the 128-slot launch,
+  // and from there those that need more than 128 to the 256-slot launch,
+  // each time simulated again from the start.
   bool all_simple = true;
   for (int c = 0; c < kClasses; ++c)
     all_simple = all_simple && (P->class_n[c] == 0 || P->simple[c]);
@@ -613,8 +616,10 @@ int make_plan(const ts_model* model, const ts_trace* traces, int32_t n_traces,
                      [&](int32_t a, int32_t b) { return est[(size_t)a] > est[(size_t)b]; });
     std::copy(all.begin(), all.end(), order.begin());
     P->class_off[0] = 0;
+    P->class_n[2] = P->class_n[2];                  // points that may reach the 256-slot launch
+    P->class_n[1] = P->class_n[1] + P->class_n[2];  // ... the 128-slot launch
     P->class_n[0] = (int)all.size();
-    P->simple[0] = true;
+    P->simple[0] = P->simple[1] = P->simple[2] = true;
     P->hand_over = true;
   }
   P->count = count;

@@ -1607,7 +1607,7 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
 // Persistent grid: each wave64 workgroup takes the next point from a ticket
 // counter until none is left.
 template <int NCH, int MODE, bool SIMPLE>
-__global__ __launch_bounds__(64, NCH == 4 ? 4 : 5) void sim_kernel(SimArgs A) {
+__global__ __launch_bounds__(64, NCH == 4 ? 4 : (NCH == 1 && SIMPLE ? 6 : 5)) void sim_kernel(SimArgs A) {
   __shared__ SlotLds<NCH> L;
   const int lane = lane_id();
   QEntry* Q = A.queue + (size_t)blockIdx.x * kQueueCap;
@@ -1639,9 +1639,9 @@ __global__ __launch_bounds__(64, NCH == 4 ? 4 : 5) void sim_kernel(SimArgs A) {
     if (tk >= n_order) break;
     const int pidx = A.order[tk];
     if (!simulate_point<NCH, MODE, SIMPLE>(A, pidx, L, Q, RT, lane, roofc)) {
-      // hand the point to the launch of its own slot class (every lane
+      // hand the point to the launch with twice the slots (every lane
       // stores the same index)
-      const int wc = A.points[pidx].max_batch <= 128 ? 0 : 1;
+      const int wc = NCH == 1 ? 0 : 1;
       const unsigned slot = atomicAdd(A.handed_n + wc, lane == 0 ? 1u : 0u);
       A.handed[A.handed_off[wc] + __builtin_amdgcn_readfirstlane((int)slot)] = pidx;
     }

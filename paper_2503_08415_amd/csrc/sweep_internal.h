@@ -131,10 +131,10 @@ struct SimArgs {
   uint64_t time_limit_ticks;   // 0 = none; 100 MHz device clock ticks per point
   unsigned long long* work;    // simulated iterations of the points completed by this launch
   // A narrow launch also takes points wider than its slots and hands those
-  // that need more running slots to the launch of their own class: handed
-  // (lists at handed_off[0] for max_batch <= 128, [1] above) and handed_n
-  // (their counts).  A launch taking over handed points reads its count at
-  // n_dev (nullptr otherwise).
+  // that need more running slots to the launch with twice the slots: handed
+  // (the list the 64-slot launch fills at handed_off[0], the 128-slot one at
+  // handed_off[1]) and handed_n (their counts).  A launch taking over handed
+  // points reads its count at n_dev (nullptr otherwise).
   int32_t* handed;
   int32_t handed_off[2];
   unsigned int* handed_n;
