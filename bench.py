@@ -13,16 +13,19 @@ mixture, bursty arrivals), generated from fixed seeds.
 roofline: the simulation is bound by instruction issue (integer scheduling
 and a short fp64 roofline per iteration; no dense contraction, negligible HBM
 traffic).  ``achieved`` is the algorithmic VALU instruction count of the
-dominant simulation kernel divided by its HIP-event duration, with
-  U = 9.5 wave64 VALU instructions per simulated iteration,
-what one steady iteration costs in this kernel's cheapest path: iterations
+dominant simulation launch divided by its HIP-event duration, with
+  U = 6.5 wave64 VALU instructions per simulated iteration,
+what one steady iteration costs in the kernels' cheapest path: iterations
 priced up to 64 at a time, one per lane, in blocks (measured with the
 SQ_INSTS_VALU counter on the u1 workload, 64 decodes with long outputs per
-point, where blocks run about 50 iterations on average; rounded down).  Scheduling events (admissions,
-finishes, prefill completions, preemptions) are not counted, so the fraction
-is the share of the issue peak the sweep would use if every iteration cost
-as little as a steady one.  Peak = 256 CUs x 4 SIMDs x 2.4 GHz / 4 cycles per
-wave64 instruction = 614.4 G instructions/s.
+point, where almost every iteration is such a one: 6.7 per iteration,
+rounded down).  Scheduling events (admissions, finishes, prefill
+completions, preemptions) are not counted, so the fraction is the share of
+the issue peak the sweep would use if every iteration cost as little as a
+steady one.  Peak = 256 CUs x 4 SIMDs x 2.4 GHz / 4 cycles per wave64
+instruction = 614.4 G instructions/s.  Every launch gets the same figure in
+``roofline_launches`` (iterations it simulated to completion, from the
+library's per-launch counters).
 """
 from __future__ import annotations
 
@@ -40,7 +43,7 @@ if ROOT not in sys.path:
 
 METRIC = "simulated requests/sec across sweep on 1 MI355X; % VALU-issue peak"
 VALU_ISSUE_PEAK = 256 * 4 * 2.4e9 / 4.0   # wave64 VALU instructions per second
-U_ITER = 9.5
+U_ITER = 6.5
 # simulation launches, 3 * stage + class (stages: one-worker points, prefill
 # devices, decode devices of disaggregated points; register-chunk classes
 # 1, 2, 4), named as rocprofv3 names the kernels
@@ -244,21 +247,25 @@ def main():
     value = n_req / (total_s / args.steps)
     status = np.bincount(out["status"], minlength=4).tolist()
 
-    # roofline of the dominant simulation kernel (longest mean duration); a
-    # disaggregated point's iterations are spread over its devices' launches,
-    # so with any such point the figure covers all simulation launches
+    # roofline of every simulation launch from the iterations it simulated to
+    # completion (a point handed from the 64-slot launch to a wider one counts
+    # only where it completed; a disaggregated point's iterations are those of
+    # its devices, each counted in its own stage's launch); the line's
+    # roofline is the dominant launch's (longest mean duration)
     kmean = np.mean(np.array(kms), axis=0)
-    disagg = "n_prefill" in points and bool((np.asarray(points["n_prefill"]) > 0).any())
     w = algorithmic_instructions(out)
-    # iterations each launch simulated to completion (a point handed from the
-    # 64-slot launch to a wider one counts only where it completed)
     work = np.array(kwork[-1], dtype=np.float64)
-    if disagg:
-        name, w_k, k_ms, traffic = "all simulation launches", float(w.sum()), float(kmean.sum()), None
-    else:
-        k = int(np.argmax(kmean))
-        name, w_k, k_ms = KERNEL_NAMES[k], U_ITER * float(work[k]), float(kmean[k])
-        traffic = recorded_traffic(args.config, name)
+    launches = []
+    for i in range(len(kmean)):
+        if kmean[i] <= 0 and work[i] == 0:
+            continue
+        a_i = U_ITER * work[i] / (kmean[i] * 1e-3) if kmean[i] > 0 else 0.0
+        launches.append({"kernel": KERNEL_NAMES[i], "iterations": int(work[i]),
+                         "kernel_ms": float(kmean[i]), "achieved": a_i / 1e9,
+                         "frac": a_i / VALU_ISSUE_PEAK})
+    k = int(np.argmax(kmean))
+    name, w_k, k_ms = KERNEL_NAMES[k], U_ITER * float(work[k]), float(kmean[k])
+    traffic = recorded_traffic(args.config, name)
     achieved = w_k / (k_ms * 1e-3)
     roofline = {"bound": "alu", "achieved": achieved / 1e9, "peak": VALU_ISSUE_PEAK / 1e9,
                 "unit": "G wave64 VALU instr/s", "frac": achieved / VALU_ISSUE_PEAK,
@@ -276,6 +283,7 @@ def main():
         "workload_sha256": {"traces": digest["traces"], "points": digest["points"],
                             "matches_committed": pinned},
         "roofline": roofline,
+        "roofline_launches": launches,
         "kernels_ms": {KERNEL_NAMES[i]: float(kmean[i]) for i in range(len(kmean))
                        if kmean[i] > 0},
         "simulation_phase_ms": float(np.mean(sim_ms)), "statistics_ms": float(np.mean(stats_ms)),

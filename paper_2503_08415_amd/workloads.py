@@ -24,7 +24,9 @@ Generator rules (all configs):
     gap that would cross a phase boundary restarts at the boundary with the
     new rate (exact for a memoryless process);
   * mixture prompts: component uniforms first, then all lognormal draws, then
-    all uniform-integer draws, then select.
+    all uniform-integer draws, then select;
+  * one-trace-per-point sweeps seed point i's trace with
+    ``1_000_000_000 + 1_000_000 * config + i`` (above every other seed).
 """
 from __future__ import annotations
 
@@ -273,78 +275,102 @@ def _c5(n_req):
     return "gqa-7b", traces, rows
 
 
-def _c6(n_req):
+def _c6(n_req, reps=1):
     """Scheduling policies and the admission memory ratio under memory
     pressure (the studies of Sec. IV-A and Sec. IV-B): 16 arrival rates x
-    3 policies x 4 ratios x 2 small capacities, 7B model, unchunked."""
-    traces = []
-    for r in range(16):
-        spec = {"arrival": ("poisson", float(r + 1)), "prompt": _LN_P_C2,
-                "output": _LN_O_C2}
-        traces.append(make_trace(spec, n_req, _seed(6, 0, r)))
-    rows = []
-    for r in range(16):
-        for policy in (0, 1, 2):
-            for ratio in (0, 600, 800, 950):
-                for cap in (24_000_000_000, 40_000_000_000):
-                    rows.append(dict(peak_flops=312e12, mem_bw=2e12, capacity_bytes=cap,
-                                     mem_util_permille=900, block_size=16, max_batch=64,
-                                     chunk_size=0, trace_id=r, policy=policy,
-                                     admit_mem_permille=ratio))
+    3 policies x 4 ratios x 2 small capacities, 7B model, unchunked; reps
+    replicates with their own traces (replicate 0 is the base sweep)."""
+    traces, rows = [], []
+    for rep in range(reps):
+        base = len(traces)
+        for r in range(16):
+            spec = {"arrival": ("poisson", float(r + 1)), "prompt": _LN_P_C2,
+                    "output": _LN_O_C2}
+            traces.append(make_trace(spec, n_req, _seed(6, rep, r)))
+        for r in range(16):
+            for policy in (0, 1, 2):
+                for ratio in (0, 600, 800, 950):
+                    for cap in (24_000_000_000, 40_000_000_000):
+                        rows.append(dict(peak_flops=312e12, mem_bw=2e12, capacity_bytes=cap,
+                                         mem_util_permille=900, block_size=16, max_batch=64,
+                                         chunk_size=0, trace_id=base + r, policy=policy,
+                                         admit_mem_permille=ratio))
     return "llama2-7b", traces, rows
 
 
-def _c7(n_req):
+def _c7(n_req, reps=1):
     """Preemption by recompute against preemption by swap (Sec. IV-B; the
     transfer priced by the communication model of Sec. III-B) under memory
     pressure: 16 arrival rates x {recompute, swap over 16 / 32 / 64 GB/s
     after the compute, swap over 64 GB/s overlapping it} x {20, 24} GB x
-    {unchunked, chunk 512}, 7B model."""
-    traces = []
-    for r in range(16):
-        spec = {"arrival": ("poisson", float(r + 1)), "prompt": _LN_P_C2,
-                "output": _LN_O_C2}
-        traces.append(make_trace(spec, n_req, _seed(7, 0, r)))
-    rows = []
-    for r in range(16):
-        for bw, overlap in ((0.0, 0), (16e9, 0), (32e9, 0), (64e9, 0), (64e9, 1)):
-            for cap in (20_000_000_000, 24_000_000_000):
-                for chunk in (0, 512):
-                    rows.append(dict(peak_flops=312e12, mem_bw=2e12, capacity_bytes=cap,
-                                     mem_util_permille=900, block_size=16, max_batch=64,
-                                     chunk_size=chunk, trace_id=r, swap_bw=bw,
-                                     swap_overlap=overlap))
+    {unchunked, chunk 512}, 7B model; reps replicates with their own traces."""
+    traces, rows = [], []
+    for rep in range(reps):
+        base = len(traces)
+        for r in range(16):
+            spec = {"arrival": ("poisson", float(r + 1)), "prompt": _LN_P_C2,
+                    "output": _LN_O_C2}
+            traces.append(make_trace(spec, n_req, _seed(7, rep, r)))
+        for r in range(16):
+            for bw, overlap in ((0.0, 0), (16e9, 0), (32e9, 0), (64e9, 0), (64e9, 1)):
+                for cap in (20_000_000_000, 24_000_000_000):
+                    for chunk in (0, 512):
+                        rows.append(dict(peak_flops=312e12, mem_bw=2e12, capacity_bytes=cap,
+                                         mem_util_permille=900, block_size=16, max_batch=64,
+                                         chunk_size=chunk, trace_id=base + r, swap_bw=bw,
+                                         swap_overlap=overlap))
     return "llama2-7b", traces, rows
 
 
-def _c8(n_req):
+def _c8(n_req, reps=1):
     """Disaggregated prefill and decode on an 8-device node (Sec. V: the best
     prefill-to-decode device ratio over input and output lengths, and the
     prefill device's compute, capacity and bandwidth): 4 length mixes
     (lognormal prompts around 128 or 1024 tokens x outputs around 128 or
     512) x 4 arrival rates x P/D splits {1/7, 2/6, 3/5, 4/4} x prefill
     hardware {A100-like, 2x FLOP/s, 1/4 capacity, 1/4 bandwidth}, 7B model,
-    decode devices A100-like, KV links of 25 GB/s."""
+    decode devices A100-like, KV links of 25 GB/s; reps replicates with
+    their own traces (replicate slot of the seed: 4 * rep + mix)."""
     mixes = [(4.85, 4.85), (4.85, 6.2), (6.9, 4.85), (6.9, 6.2)]  # log-means: ~128, ~512, ~1024
     rates = (5.0, 10.0, 20.0, 40.0)
-    traces = []
-    for m, (lp, lo) in enumerate(mixes):
-        for r, rate in enumerate(rates):
-            spec = {"arrival": ("poisson", rate), "prompt": ("lognormal", lp, 0.6, 4, 8192),
-                    "output": ("lognormal", lo, 0.6, 1, 4096)}
-            traces.append(make_trace(spec, n_req, _seed(8, m, r)))
     prefill_hw = [(312e12, 2e12, 80_000_000_000), (624e12, 2e12, 80_000_000_000),
                   (312e12, 2e12, 20_000_000_000), (312e12, 0.5e12, 80_000_000_000)]
-    rows = []
-    for k in range(len(traces)):
-        for n_p in (1, 2, 3, 4):
-            for pf, pb, pc in prefill_hw:
-                rows.append(dict(peak_flops=312e12, mem_bw=2e12, capacity_bytes=80_000_000_000,
-                                 mem_util_permille=900, block_size=16, max_batch=64,
-                                 chunk_size=0, trace_id=k, n_prefill=n_p, n_decode=8 - n_p,
-                                 p_peak_flops=pf, p_mem_bw=pb, p_capacity_bytes=pc,
-                                 kv_link_bw=25e9))
+    traces, rows = [], []
+    for rep in range(reps):
+        base = len(traces)
+        for m, (lp, lo) in enumerate(mixes):
+            for r, rate in enumerate(rates):
+                spec = {"arrival": ("poisson", rate),
+                        "prompt": ("lognormal", lp, 0.6, 4, 8192),
+                        "output": ("lognormal", lo, 0.6, 1, 4096)}
+                traces.append(make_trace(spec, n_req, _seed(8, 4 * rep + m, r)))
+        for k in range(len(mixes) * len(rates)):
+            for n_p in (1, 2, 3, 4):
+                for pf, pb, pc in prefill_hw:
+                    rows.append(dict(peak_flops=312e12, mem_bw=2e12,
+                                     capacity_bytes=80_000_000_000, mem_util_permille=900,
+                                     block_size=16, max_batch=64, chunk_size=0,
+                                     trace_id=base + k, n_prefill=n_p, n_decode=8 - n_p,
+                                     p_peak_flops=pf, p_mem_bw=pb, p_capacity_bytes=pc,
+                                     kv_link_bw=25e9))
     return "llama2-7b", traces, rows
+
+
+def _c4u(n_req):
+    """c4's grid with one trace per design point (trace_id = point): every
+    point reads its own 4000 records, so the sweep streams 1.05 GB of distinct
+    trace bytes from HBM.  Point i draws its trace at its row's rate with
+    seed 1_000_000_000 + 1_000_000 * 4 + i."""
+    _, _, rows = _c4(0)
+    traces = []
+    for i, row in enumerate(rows):
+        rate = 4.0 * (row["trace_id"] + 1)
+        spec = {"arrival": ("poisson", rate),
+                "prompt": ("lognormal", 6.0, 1.1, 4, 8192),
+                "output": ("lognormal", 5.3, 1.0, 1, 4096)}
+        traces.append(make_trace(spec, n_req, 1_000_000_000 + 1_000_000 * 4 + i))
+        row["trace_id"] = i
+    return "llama2-70b-kvonly", traces, rows
 
 
 def _u1(n_req):
@@ -382,6 +408,16 @@ CONFIGS = {
                     "(calibration of the steady path)"),
     "c8": (_c8, 2000, "256 disaggregated points x 2000 requests, 7B MHA, 4 length mixes x "
                       "4 rates x P/D {1/7, 2/6, 3/5, 4/4} x 4 prefill devices, 25 GB/s KV links"),
+    # the same studies at a size that fills the GPU (at least 8192 simulation
+    # units: one per one-worker point, one per device of a disaggregated one)
+    "c6x": (lambda n: _c6(n, 24), 2000, "9216 points x 2000 requests: c6 with 24 replicates "
+                                        "(own traces each)"),
+    "c7x": (lambda n: _c7(n, 26), 2000, "8320 points x 2000 requests: c7 with 26 replicates "
+                                        "(own traces each)"),
+    "c8x": (lambda n: _c8(n, 4), 2000, "1024 disaggregated points (8192 devices) x 2000 "
+                                       "requests: c8 with 4 replicates (own traces each)"),
+    "c4u": (_c4u, 4000, "16384 points x 4000 requests: c4 with one trace per point "
+                        "(1.05 GB of distinct trace records)"),
 }
 
 

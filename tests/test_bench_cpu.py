@@ -45,6 +45,48 @@ def test_c8_splits_an_eight_device_node():
     assert (p["policy"] == 0).all() and (p["kv_link_bw"] > 0).all()
 
 
+@pytest.mark.parametrize("base,wide,reps", [("c6", "c6x", 24), ("c7", "c7x", 26),
+                                             ("c8", "c8x", 4)])
+def test_gpu_filling_sweeps_replicate_the_studies(base, wide, reps):
+    """The wide sweeps are their study's grid repeated over replicates with
+    traces of their own: replicate 0 is the study itself, and every
+    replicate's traces differ from the others'."""
+    _, tb, pb = W.make_config(base)
+    _, tw, pw = W.make_config(wide)
+    nb, nt = len(pb["peak_flops"]), len(tb)
+    assert len(pw["peak_flops"]) == reps * nb and len(tw) == reps * nt
+    for k in pb:
+        assert np.array_equal(pw[k][:nb], pb[k])
+        if k != "trace_id":
+            assert np.array_equal(pw[k].reshape(reps, nb), np.tile(pb[k], (reps, 1)))
+    assert np.array_equal(pw["trace_id"].reshape(reps, nb),
+                          pb["trace_id"][None, :] + nt * np.arange(reps)[:, None])
+    for a, b in zip(tw[:nt], tb):
+        assert np.array_equal(a["arrival_ns"], b["arrival_ns"])
+    firsts = {int(t["arrival_ns"][0]) for t in tw}
+    assert len(firsts) == len(tw)
+    units = (pw["n_prefill"] + pw["n_decode"]).clip(min=1)
+    assert int(units.sum()) >= 8192
+
+
+def test_unique_trace_sweep_is_c4_with_one_trace_per_point():
+    _, t4, p4 = W.make_config("c4")
+    _, tu, pu = W.make_config("c4u")
+    n = len(p4["peak_flops"])
+    assert len(tu) == n and np.array_equal(pu["trace_id"], np.arange(n))
+    for k in p4:
+        if k != "trace_id":
+            assert np.array_equal(pu[k], p4[k])
+    assert all(len(t["arrival_ns"]) == 4000 for t in tu)
+    # 16 bytes per record (arrival int64, prompt and output int32)
+    assert sum(16 * len(t["arrival_ns"]) for t in tu) == 16384 * 4000 * 16
+    # each point's trace is drawn at its row's rate: mean gap near 1 / rate
+    for i in (0, n // 2, n - 1):
+        rate = 4.0 * (p4["trace_id"][i] + 1)
+        gap = tu[i]["arrival_ns"][-1] / 4000 / 1e9
+        assert abs(gap * rate - 1.0) < 0.1
+
+
 def test_u1_calibration_workload_is_one_steady_batch():
     _, t, p = W.make_config("u1")
     assert len(t) == 1 and len(p["peak_flops"]) == 8192
@@ -92,13 +134,13 @@ def test_workload_bytes_match_committed_digests(name):
 
 def test_iteration_work_unit_is_frozen_to_the_u1_calibration():
     """U, the algorithmic VALU instructions per simulated iteration behind
-    roofline.achieved, is 9.5 and never above what the committed u1 counter
+    roofline.achieved, is 6.5 and never above what the committed u1 counter
     run measured per iteration of the cheapest path (it may only move down,
     with a new u1 profile)."""
     import re
     sys.path.insert(0, ROOT)
     import bench
-    assert bench.U_ITER == 9.5
+    assert bench.U_ITER == 6.5
     with open(os.path.join(ROOT, "profiles", "sim_kernel_sq_counters_u1.md")) as f:
         text = f.read()
     m = re.search(r"\|\s*SQ_INSTS_VALU\s*\|\s*[0-9.e+]+\s*\|\s*([0-9.]+)\s*\|", text)

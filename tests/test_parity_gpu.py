@@ -349,6 +349,20 @@ def test_full_c4_points(S, oracle):
     compare_points(out, o_out, "c4")
 
 
+@pytest.mark.parametrize("name", ["c6x", "c7x", "c8x", "c4u"])
+def test_gpu_filling_sweeps_all_points(S, oracle, name):
+    """The policy, swap and disaggregation studies at a size that fills the
+    GPU (at least 8192 simulation units), and c4 with one trace per point:
+    every point's counters, sums, percentiles and request digest."""
+    m, traces, pts = W.make_config(name)
+    t0 = time.time()
+    o_out, _ = oracle.run_points(m, traces, pts)
+    say("%s: oracle on all %d points %.1fs" % (name, len(pts["peak_flops"]), time.time() - t0))
+    out, _ = gpu_run(S, m, traces, pts, iter_cap=cap_from(o_out))
+    compare_points(out, o_out, name)
+    assert (out["status"] == 0).all()
+
+
 def test_c5_all_points(S, oracle):
     """The full 65536-point x 10000-request c5 sweep, launched as the
     benchmark launches it: every point's counters, sums, percentiles and
