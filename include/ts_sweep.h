@@ -220,13 +220,13 @@ typedef struct {
  * call: TS_ERR_ARG for invalid input, TS_ERR_UNSUPPORTED when a cost-model
  * integer (a point's KV bytes, with swap) could exceed 2^53 (exact fp64) or a
  * block count exceeds 2^30.
- * Device memory it allocates: the traces (16 B per request), the latency
- * arrays of the percentile pass (16 B per point per request of its trace's
- * length, padded to the longest trace), a request-time table per workgroup
- * (24 B per request of the longest trace; the grid shrinks to keep these
- * tables within 16 GiB), and with TS_F_PER_REQUEST the request records
- * (40 B per point per request); TS_ERR_OOM, before any allocation, when
- * their sum exceeds the device's free memory (or an allocation fails).
+ * Device memory it allocates: the traces (16 B per request), the request
+ * records (40 B per point per request of the longest trace; the statistics
+ * are computed from them, so they are kept with or without
+ * TS_F_PER_REQUEST), the latency arrays of the percentile pass (16 B per
+ * point per request of the longest trace), and a preempted-request queue
+ * per workgroup (8 KiB); TS_ERR_OOM, before any allocation, when their sum
+ * exceeds the device's free memory (or an allocation fails).
  * The handle belongs to the device current at create time; every later call
  * selects that device itself.
  * On success *out receives the handle; on failure *out is NULL. */
@@ -299,7 +299,7 @@ int ts_sweep_kernel_work(ts_sweep *h, int64_t *iters);
  * work is enqueued on hip_stream (NULL = the default stream) and the call
  * returns after synchronising it.  TS_ERR_UNSUPPORTED when the sweep's
  * buffers exceed the array even at one workgroup per kernel launch (the
- * request-time tables take at most a quarter of it: the grid shrinks to fit);
+ * per-workgroup queues shrink with the grid);
  * TS_ERR_STATE for out_requests without TS_F_PER_REQUEST.  All calls share
  * the one array of their GPU and it keeps the last call's contents (each
  * call clears what must start at zero): calls inside one process are

@@ -227,7 +227,6 @@ BufCounts buf_counts(const Plan& P) {
   c.handed = P.hand_over ? (size_t)(P.class_n[1] + P.class_n[2]) : 0;
   c.work = kLaunches;
   c.queue = (size_t)P.max_grid() * kQueueCap;
-  c.times = (size_t)P.max_grid() * per_point;
   c.res = (size_t)(P.count + P.n_extra);
   c.req = (size_t)P.count * per_point;  // the request records (always)
   c.pinfo = P.pinfo.size();
@@ -242,7 +241,7 @@ BufCounts buf_counts(const Plan& P) {
 double BufCounts::bytes() const {
   return (double)recs * sizeof(TraceRec) + (double)points * sizeof(DevPoint) +
          (double)order * sizeof(int32_t) + (double)counter * sizeof(unsigned int) +
-         (double)queue * sizeof(QEntry) + (double)times * sizeof(ReqTimes) +
+         (double)queue * sizeof(QEntry) +
          (double)res * sizeof(ts_point_result) + (double)req * sizeof(ts_req_result) +
          2.0 * (double)lat * sizeof(int64_t) + (double)pd * sizeof(PdAux) +
          2.0 * (double)s1 * sizeof(int64_t) + (double)sub * (sizeof(int64_t) + sizeof(int32_t)) +
@@ -270,7 +269,6 @@ void release(ts_sweep* h) {
   (void)hipFree(b.order);
   (void)hipFree(b.counter);
   (void)hipFree(b.queue);
-  (void)hipFree(b.times);
   (void)hipFree(b.res);
   (void)hipFree(b.req);
   (void)hipFree(b.e2e);
@@ -306,8 +304,7 @@ hipError_t dev_alloc(T** p, size_t count) {
 namespace tsw {
 
 int make_plan(const ts_model* model, const ts_trace* traces, int32_t n_traces,
-              const ts_point* points, int32_t n_points, const ts_options* opt,
-              int64_t time_table_cap, Plan* P) {
+              const ts_point* points, int32_t n_points, const ts_options* opt, Plan* P) {
   // ---------------------------------------------------------- validation
   if (!model_ok(model)) return TS_ERR_ARG;
   if (!traces || n_traces < 1 || !points || n_points < 0) return TS_ERR_ARG;
@@ -648,13 +645,6 @@ int make_plan(const ts_model* model, const ts_trace* traces, int32_t n_traces,
     if (e != hipSuccess) { return device_error(e, "occupancy query"); }
     per_cu = std::max(per_cu, 1);
     P->grid[l] = std::min(P->class_n[l], n_cu * per_cu);
-    // per-workgroup request-time table: max_n entries; keep the tables under
-    // time_table_cap bytes (a full grid at 10^4 requests per point needs
-    // about 1.2 GB)
-    const int64_t cap = std::max<int64_t>(1, time_table_cap /
-                                                 ((int64_t)std::max<int64_t>(max_n, 1) *
-                                                  (int64_t)sizeof(ReqTimes)));
-    P->grid[l] = (int)std::min<int64_t>(P->grid[l], cap);
   }
   P->stats_grid = std::max(1, std::min(count, n_cu * 8));
 
@@ -712,7 +702,6 @@ int enqueue(const Plan& P, const DevBufs& B, hipStream_t s, const LaunchEvents* 
   a.points = B.points;
   a.max_n = P.max_n;
   a.queue = B.queue;
-  a.times = B.times;
   a.res = B.res;
   a.rec = B.req;
   a.iter_cap = P.iter_cap;
@@ -817,7 +806,7 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
   g_err[0] = 0;
   ts_sweep* h = new (std::nothrow) ts_sweep();
   if (!h) return TS_ERR_OOM;
-  int rc = make_plan(model, traces, n_traces, points, n_points, opt, (int64_t)1 << 34, &h->P);
+  int rc = make_plan(model, traces, n_traces, points, n_points, opt, &h->P);
   if (rc != TS_OK) {
     release(h);
     return rc;
@@ -841,7 +830,6 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
   if (ae == hipSuccess) ae = dev_alloc(&b.order, n.order);
   if (ae == hipSuccess) ae = dev_alloc(&b.counter, n.counter);
   if (ae == hipSuccess) ae = dev_alloc(&b.queue, n.queue);
-  if (ae == hipSuccess) ae = dev_alloc(&b.times, n.times);
   if (ae == hipSuccess) ae = dev_alloc(&b.res, n.res);
   if (ae == hipSuccess) ae = dev_alloc(&b.e2e, n.lat);
   if (ae == hipSuccess) ae = dev_alloc(&b.ttft, n.lat);
@@ -888,7 +876,7 @@ int ts_sweep_run(ts_sweep* h, void* hip_stream) {
   hipStream_t s = (hipStream_t)hip_stream;
   hipError_t e = hipSetDevice(h->P.device);
   if (e != hipSuccess) return device_error(e, "hipSetDevice");
-  // A re-run reuses the work-queue counters, queues, time tables and result
+  // A re-run reuses the work-queue counters, queues, request records and result
   // buffers of the previous run: on another stream it must wait for that
   // run's last kernel.
   if (h->ran && s != h->last_stream) {

@@ -1,8 +1,8 @@
 // noalloc.hip -- ts_sweep_run_static: a whole sweep in one call that
 // allocates no device memory.  Every buffer the kernels use (traces, units,
-// work order, ticket counters, preempted queues, request-time tables,
-// latency arrays, results, per-request records, the disaggregated points'
-// stage buffers) is carved out of one file-scope device array of
+// work order, ticket counters, preempted queues, latency arrays, results,
+// per-request records, the disaggregated points' stage buffers) is carved
+// out of one file-scope device array of
 // TS_STATIC_SCRATCH_BYTES, which each GPU the library runs on holds until
 // the process ends.  The kernels and the launch sequence are those of
 // ts_sweep_create + ts_sweep_run.
@@ -72,7 +72,6 @@ size_t carve(const tsw::Plan& P, unsigned char* base, tsw::DevBufs* B) {
   b.order = c.take<int32_t>(n.order);
   b.counter = c.take<unsigned int>(n.counter);
   b.queue = c.take<tsw::QEntry>(n.queue);
-  b.times = c.take<tsw::ReqTimes>(n.times);
   b.res = c.take<ts_point_result>(n.res);
   b.e2e = c.take<int64_t>(n.lat);
   b.ttft = c.take<int64_t>(n.lat);
@@ -99,15 +98,13 @@ extern "C" int ts_sweep_run_static(const ts_model* model, const ts_trace* traces
   tsw::clear_error_text();
   std::lock_guard<std::mutex> lock(g_mu);
   tsw::Plan P;
-  // the request-time tables share the scratch: at most a quarter of it
-  int rc = tsw::make_plan(model, traces, n_traces, points, n_points, opt,
-                          (int64_t)(kScratchBytes / 4), &P);
+  int rc = tsw::make_plan(model, traces, n_traces, points, n_points, opt, &P);
   if (rc != TS_OK) return rc;
   if (!out_points && P.count > 0) return TS_ERR_ARG;
   if (out_requests && !(P.flags & TS_F_PER_REQUEST)) return TS_ERR_STATE;
   if ((P.flags & TS_F_PER_REQUEST) && !out_requests && P.count > 0) return TS_ERR_ARG;
-  // The workgroup tables scale with the grid: shrink it until everything
-  // fits, down to one workgroup per launch.
+  // The per-workgroup queues scale with the grid: shrink it until
+  // everything fits, down to one workgroup per launch.
   while (carve(P, nullptr, nullptr) > kScratchBytes && P.max_grid() > 1) {
     const int g = std::max(1, P.max_grid() / 2);
     for (int l = 0; l < tsw::kLaunches; ++l) P.grid[l] = std::min(P.grid[l], g);

@@ -317,7 +317,7 @@ __device__ __forceinline__ void store_chunk(SlotLds<NCH>& L, Hot& h0, int j, int
 // it wrote is final, and a wider launch simulates it again from the start.
 template <int NCH, int MODE, bool SIMPLE>
 __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
-                                               SlotLds<NCH>& L, QEntry* Q, ReqTimes* RT,
+                                               SlotLds<NCH>& L, QEntry* Q,
                                                const int lane, const LaneRoof& roofc) {
   const DevPoint P = A.points[pidx];
   const TraceRec* __restrict__ rec = A.recs + P.trace_off;
@@ -449,17 +449,17 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
   const int lgB = (B & (B - 1)) == 0 ? 31 - __builtin_clz((unsigned)B) : -1;
   auto divB = [&](int x) { return lgB >= 0 ? x >> lgB : x / B; };
 
-  // A request finishing at t_end (lanes with fin): its record.  The point's
-  // latency sums, SLO counts, percentiles and digest are computed from the
-  // records after the simulation.
+  // A request finishing at t_end (lanes with fin): the rest of its record
+  // (its admission and first token are there already).  The point's latency
+  // sums, SLO counts, percentiles and digest are computed from the records
+  // after the simulation.
   auto record_done = [&](bool fin, int s, int64_t t_end, int64_t gap) {
     if (fin) {
-      const int id = L.id[s];
-      const ReqTimes rt = RT[id];
-      ts_req_result o;
-      o.admit_ns = rt.admit; o.first_token_ns = rt.first; o.finish_ns = t_end;
-      o.max_gap_ns = gap; o.n_preempt = L.npre[s]; o.status = TS_REQ_DONE;
-      RR[gid_of(id)] = o;
+      ts_req_result& o = RR[gid_of(L.id[s])];
+      o.finish_ns = t_end;
+      o.max_gap_ns = gap;
+      o.n_preempt = L.npre[s];
+      o.status = TS_REQ_DONE;
     }
   };
 
@@ -557,7 +557,7 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
       const int c = __builtin_amdgcn_readfirstlane((int)L.sub_cnt[v]);
       L.sub_cnt[v] = (unsigned int)(c + 1);  // every lane stores the same value
       const int pos = X->sub_off[P.unit * kMaxDev + v] + c;
-      const int64_t adm = RT[id_l].admit;
+      const int64_t adm = RR[g].admit_ns;
       if (lane == 0) {
         A.sub_a2[pos] = link_free;
         A.sub_gid[pos] = g;
@@ -941,21 +941,64 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
             thr = next < N ? __builtin_fmin((double)rdl64(w_arr, next - wbase), kT52d) : kT52d;
             const int left = tgt_p - ctx_p;
             const int R1 = K - nDa - left;  // budget left after the completing prefill
-            int adm = 0, id_h = 0, tgt_h = 0, o_h = 0, need_h = 0;
+            // FCFS admissions into the rest of the budget, in place, from the
+            // waiting trace requests at the queue head.  When the first one's
+            // prompt exceeds the budget it becomes the new head prefill;
+            // otherwise, over a window of 64, each takes its whole prompt
+            // while the budget lasts (those complete in this iteration and
+            // join the decodes), the last one possibly a part of it (the new
+            // head prefill).  Preempted requests, a rejected request among
+            // those admitted, a second window and a full slot set go to the
+            // general path.
+            int a = 0, c = 0, q_new = 0, sq = 0, need_sum = 0, id_h = 0, tgt_h = 0, o_h = 0;
+            int64_t ap_new = 0;
+            int c_p = 0, c_o = 0, c_need = 0, c_qv = 0;
+            bool c_ok = false, c_comp = false;
             if (policy != TS_POLICY_STATIC && (npre > 0 || nwait > 0) && nruna < M &&
                 (R1 > 0 || (swap && npre > 0))) {
               if (npre > 0 || nrun >= 64 * NCH) break;  // queue candidates, full slots
               const TraceRec r = rec[next_new];
               if (may_reject && rejected(r.prompt, r.output)) break;
-              need_h = divB(r.prompt + B - 1);
+              const int need_h = divB(r.prompt + B - 1);
               if (need_h > freeb - nneed - adm_reserve) {
                 head_need = need_h;  // the head waits for blocks
-              } else {
-                if (r.prompt <= R1) break;  // it would complete at once
-                adm = 1;
+              } else if (r.prompt > R1) {  // the new head prefill
+                a = 1;
+                q_new = R1;
+                sq = R1;
+                ap_new = ((int64_t)R1 * (R1 + 1)) / 2;
+                need_sum = need_h;
                 id_h = next_new;
                 tgt_h = r.prompt;
                 o_h = r.output;
+                head_need = -1;
+              } else {
+                const int idx = next_new + lane;
+                if (idx < next) {
+                  const TraceRec rc = rec[idx];
+                  c_p = rc.prompt;
+                  c_o = rc.output;
+                }
+                // candidates up to the first rejected one
+                const uint64_t rjm = ballot(may_reject && idx < next && rejected(c_p, c_o));
+                const int lim = rjm != 0 ? (int)__builtin_ctzll(rjm) : 64;
+                c_need = idx < next && lane < lim ? divB(c_p + B - 1) : 0;
+                const int SN = scan_i32(c_need);
+                const int SP = scan_i32(lane < lim ? c_p : 0);
+                const int ET = SP - (lane < lim ? c_p : 0);  // prompt tokens of those before
+                c_ok = idx < next && lane < lim && lane < M - nruna &&
+                       SN <= freeb - nneed - adm_reserve && ET < R1;
+                a = popc(ballot(c_ok));  // >= 1: the first one fits
+                if ((rjm != 0 && a == lim) || a == 64 || nrun + a > 64 * NCH)
+                  break;  // a rejected request, a second window, full slots
+                c_comp = c_ok && SP <= R1;
+                c = popc(ballot(c_comp));  // >= 1
+                c_qv = c_ok ? (c_comp ? c_p : R1 - ET) : 0;
+                sq = wsum(c_qv);
+                ap_new = wsum64(c_ok ? ((int64_t)c_qv * (c_qv + 1)) / 2 : 0);
+                need_sum = rdl(SN, a - 1);
+                q_new = a > c ? rdl(c_qv, a - 1) : 0;
+                head_need = a < next - next_new ? rdl(c_need, a) : -1;
               }
             }
             // reserve, admit, price the iteration with both prefills
@@ -965,14 +1008,12 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
               for (int j = 0; j < NCH; ++j)
                 if (j < nchd) rr[j] += rr[j] == dG ? B : 0;
             }
-            if (adm) freeb -= need_h;
-            const int q_new = adm ? R1 : 0;
-            const int TP = left + q_new;
-            const int64_t AP = (int64_t)left * ctx_p + ((int64_t)left * (left + 1)) / 2 +
-                               ((int64_t)q_new * (q_new + 1)) / 2;
+            freeb -= need_sum;
+            const int TP = left + sq;
+            const int64_t AP = (int64_t)left * ctx_p + ((int64_t)left * (left + 1)) / 2 + ap_new;
             double iter_d;
             const int64_t iter_ns = iteration_ns(roofc, A.n_layers, iF, iB, nDa + TP, TP, AP,
-                                                 tgt_p + q_new, nDa, CD, nDa + 1, 0.0, false,
+                                                 tgt_p + sq, nDa, CD, nDa + 1 + c, 0.0, false,
                                                  &iter_d);
             const int64_t t_beg = t;
             const int64_t t_end = t_beg + iter_ns;
@@ -1023,7 +1064,7 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
                 L.x_fl[e] = fl_s | FL_FIRST;
               }
               id_s = __builtin_amdgcn_readfirstlane(id_s);
-              RT[id_s].first = t_end;
+              RR[gid_of(id_s)].first_token_ns = t_end;
 #pragma unroll
               for (int j = 0; j < NCH; ++j)
                 if (j == js) rr[j] = lane == ls ? room_s + g1 : rr[j];
@@ -1031,14 +1072,66 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
               ++nDa;
               nchd = (nD + 63) >> 6;
             }
-            if (adm) {
+            if (c > 0) {
+              // the admitted requests take slots nrun.. in order: those whose
+              // prompt completes emit their first token and join the decodes
+              // at iteration dG + 1 (stored shifted by it, like the head
+              // above), the last one may stay as the new head prefill
+              const int g1 = dG + 1;
+              const int s0 = nrun;
+              if (c_ok) {
+                const int idx = next_new + lane;
+                StageSlot st;
+                st.tgt = c_p;
+                st.ctx = c_comp ? c_p - g1 : c_qv;
+                st.rem = c_comp ? c_o + g1 : c_o;
+                st.room = c_need * B - c_p;
+                st.fl = c_comp ? FL_FIRST : 0;
+                st.q = 0;
+                st.gap = 0;
+                L.u.stage[lane] = st;
+                L.id[s0 + lane] = idx;
+                L.npre[s0 + lane] = 0;
+                RR[gid_of(idx)].admit_ns = t_beg;  // first admission
+                if (c_comp) RR[gid_of(idx)].first_token_ns = t_end;
+              }
+              __syncthreads();
+#pragma unroll
+              for (int j = 0; j < NCH; ++j) {
+                const int sl = j * 64 + lane;
+                if (sl >= s0 && sl < s0 + a) {
+                  const StageSlot st = L.u.stage[sl - s0];
+                  Hot h;
+                  h.ctx = st.ctx; h.tgt = st.tgt; h.rem = st.rem; h.room = st.room;
+                  h.fl = st.fl; h.q = st.q; h.gap = st.gap;
+                  store_chunk<NCH>(L, h0, j, lane, h);
+                  if (sl < s0 + c) rr[j] = st.room + g1;
+                }
+              }
+              __syncthreads();
+              nrun += a;
+              nruna += a;
+              nD += c;
+              nDa += c;
+              nchd = (nD + 63) >> 6;
+              next_new += a;
+              nwait -= a;
+              if (nwait == 0) next_new = next;
+              if (a > c) {  // the new head prefill, in slot s0 + c
+                ctx_p = q_new;
+                tgt_p = rdl(c_p, a - 1);
+                fl_p = 0;
+              } else {
+                npf = 0;
+              }
+            } else if (a > 0) {
               // the admitted request becomes the head prefill in slot nrun
               const int js = nrun >> 6, ls = nrun & 63;
               if (NCH == 1 || js == 0) {
                 h0.ctx = lane == ls ? q_new : h0.ctx;
                 h0.tgt = lane == ls ? tgt_h : h0.tgt;
                 h0.rem = lane == ls ? o_h : h0.rem;
-                h0.room = lane == ls ? need_h * B - tgt_h : h0.room;
+                h0.room = lane == ls ? need_sum * B - tgt_h : h0.room;
                 h0.fl = lane == ls ? 0 : h0.fl;
                 h0.q = lane == ls ? 0 : h0.q;
                 h0.gap = lane == ls ? 0 : h0.gap;
@@ -1047,19 +1140,18 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
                 L.x_ctx[e] = q_new;
                 L.x_tgt[e] = tgt_h;
                 L.x_rem[e] = o_h;
-                L.x_room[e] = need_h * B - tgt_h;
+                L.x_room[e] = need_sum * B - tgt_h;
                 L.x_fl[e] = 0;
                 L.x_q[e] = 0;
                 L.x_gap[e] = 0;
               }
               L.id[nrun] = id_h;
               L.npre[nrun] = 0;
-              RT[id_h].admit = t_beg;  // first admission
+              RR[gid_of(id_h)].admit_ns = t_beg;  // first admission
               ++nrun;
               ++nruna;
               ++next_new;
               if (--nwait == 0) next_new = next;
-              head_need = -1;
               ctx_p = q_new;
               tgt_p = tgt_h;
               fl_p = 0;
@@ -1213,7 +1305,7 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
           int fl = h.fl;
           if ((fl & FL_FIRST) && !(fl & FL_STALE)) {
             // the last token is the one emitted at the end of the previous iteration
-            if (h.ctx >= h.tgt) RT[id].last = t;
+            if (h.ctx >= h.tgt) RR[gid_of(id)].finish_ns = t;  // last token, until it finishes
             fl |= FL_STALE;
           }
           QEntry e;
@@ -1371,14 +1463,13 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
           if constexpr (MODE == kStageDecode) {
             if (!fromq) {  // its times so far come from the prefill device
               const int g = gid_of(c_id);
-              ReqTimes rt;
-              rt.admit = A.s1_admit[req_base + g];
-              rt.first = A.s1_first[req_base + g];
-              rt.last = rt.first;
-              RT[c_id] = rt;
+              ts_req_result& o = RR[g];
+              o.admit_ns = A.s1_admit[req_base + g];
+              o.first_token_ns = A.s1_first[req_base + g];
+              o.finish_ns = o.first_token_ns;  // the last token, until it finishes
             }
           } else {
-            if (!fromq) RT[c_id].admit = t;  // first admission
+            if (!fromq) RR[gid_of(c_id)].admit_ns = t;  // first admission
           }
           L.id[nrun + rank] = c_id;  // rank < M - nrun: a free slot
           L.npre[nrun + rank] = c_npre;
@@ -1490,7 +1581,7 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
       bool fin = false, pfin = false;
       if (pf_iter && act && h.ctx >= h.tgt && !(h.fl & FL_STALE)) {
         // a paused decode: its last token ended the previous iteration
-        RT[L.id[s]].last = t;
+        RR[gid_of(L.id[s])].finish_ns = t;  // the last token, until it finishes
         h.fl |= FL_STALE;
       }
       if (dec) {
@@ -1501,7 +1592,7 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
         // the gap reaches back to the token before the preemption
         int64_t g = iter_ns;
         if (h.fl & FL_STALE) {
-          g = t_end - RT[L.id[s]].last;
+          g = t_end - RR[gid_of(L.id[s])].finish_ns;
           h.fl &= ~FL_STALE;
         }
         h.gap = g > h.gap ? g : h.gap;
@@ -1510,7 +1601,7 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
         h.ctx += h.q;
         if (h.ctx == h.tgt && !(h.fl & FL_FIRST)) {  // the full prefill emits a token
           h.fl |= FL_FIRST;
-          RT[L.id[s]].first = t_end;
+          RR[gid_of(L.id[s])].first_token_ns = t_end;
           if constexpr (MODE == kStagePrefill) {  // and leaves the prefill device
             h.rem = 0;
             pfin = true;
@@ -1607,11 +1698,10 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
 // Persistent grid: each wave64 workgroup takes the next point from a ticket
 // counter until none is left.
 template <int NCH, int MODE, bool SIMPLE>
-__global__ __launch_bounds__(64, NCH == 4 ? 4 : (NCH == 1 && SIMPLE ? 6 : 5)) void sim_kernel(SimArgs A) {
+__global__ __launch_bounds__(64, NCH == 4 ? 4 : (SIMPLE ? 6 : 5)) void sim_kernel(SimArgs A) {
   __shared__ SlotLds<NCH> L;
   const int lane = lane_id();
   QEntry* Q = A.queue + (size_t)blockIdx.x * kQueueCap;
-  ReqTimes* RT = A.times + (size_t)blockIdx.x * (size_t)A.max_n;
   __shared__ double coef[32];
   if (lane < 8) {
     coef[lane] = A.lc.f[lane];
@@ -1638,7 +1728,7 @@ __global__ __launch_bounds__(64, NCH == 4 ? 4 : (NCH == 1 && SIMPLE ? 6 : 5)) vo
     const int tk = __builtin_amdgcn_readfirstlane((int)old);
     if (tk >= n_order) break;
     const int pidx = A.order[tk];
-    if (!simulate_point<NCH, MODE, SIMPLE>(A, pidx, L, Q, RT, lane, roofc)) {
+    if (!simulate_point<NCH, MODE, SIMPLE>(A, pidx, L, Q, lane, roofc)) {
       // hand the point to the launch with twice the slots (every lane
       // stores the same index)
       const int wc = NCH == 1 ? 0 : 1;

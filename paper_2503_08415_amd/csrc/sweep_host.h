@@ -48,7 +48,7 @@ struct Plan {
 
 // Element counts of every device buffer of a plan.
 struct BufCounts {
-  size_t recs, points, order, counter, queue, times, res, req, lat, pd, s1, sub, gids, pinfo,
+  size_t recs, points, order, counter, queue, res, req, lat, pd, s1, sub, gids, pinfo,
       handed, work;
   double bytes() const;  // total, in bytes
 };
@@ -64,9 +64,8 @@ struct DevBufs {
   unsigned long long* work = nullptr;  // simulated iterations completed per launch
   int32_t* handed = nullptr;        // points handed from launch 0 to launches 1 and 2
   QEntry* queue = nullptr;          // kQueueCap per workgroup, shared by the launches
-  ReqTimes* times = nullptr;        // max_n per workgroup, shared by the launches
   ts_point_result* res = nullptr;
-  ts_req_result* req = nullptr;     // the request records, max_n per point
+  ts_req_result* req = nullptr;     // the request records, max_n per point (always)
   int64_t* e2e = nullptr;           // max_n per point: latencies for the percentile pass
   int64_t* ttft = nullptr;
   PdAux* pd = nullptr;
@@ -86,11 +85,9 @@ struct LaunchEvents {
 };
 
 // Validates every input on the host, before any device call, then derives
-// the plan (the grid sizes query the current device).  time_table_cap bounds
-// the per-workgroup request-time tables in bytes (the grid shrinks to fit).
+// the plan (the grid sizes query the current device).
 int make_plan(const ts_model* model, const ts_trace* traces, int32_t n_traces,
-              const ts_point* points, int32_t n_points, const ts_options* opt,
-              int64_t time_table_cap, Plan* P);
+              const ts_point* points, int32_t n_points, const ts_options* opt, Plan* P);
 
 // Copies the plan's records to the device buffers: synchronously, or on
 // stream s (the host vectors must then outlive the copies).

@@ -101,13 +101,6 @@ struct __attribute__((aligned(16))) QEntry {
   int64_t gap;
 };
 
-// Per-request times kept by the workgroup simulating a point, indexed by
-// request: first admission, first token, and the last token before the
-// latest preemption.  Written once per event, read when the request ends.
-struct ReqTimes {
-  int64_t admit, first, last;
-};
-
 // Per-lane roofline coefficients (doubles holding exact integers): lane j < 7
 // prices operator j as F = f * X_j, B = (b0 + b1 * Y_j) + b2 * Z_j.
 struct LaneCoef {
@@ -124,9 +117,12 @@ struct SimArgs {
   int32_t max_n;               // row stride of the per-request buffers
   unsigned int* counter;       // work queue ticket counter (zeroed before launch)
   QEntry* queue;               // kQueueCap entries per workgroup
-  ReqTimes* times;             // max_n entries per workgroup
   ts_point_result* res;
-  ts_req_result* rec;          // max_n per point: the request records (row = design point)
+  // max_n per point (row = design point): the request records.  Admission
+  // and first token are written when they happen, the rest at the finish;
+  // until then finish_ns holds the time of the request's last token before a
+  // preemption.
+  ts_req_result* rec;
   int64_t iter_cap;
   uint64_t time_limit_ticks;   // 0 = none; 100 MHz device clock ticks per point
   unsigned long long* work;    // simulated iterations of the points completed by this launch
