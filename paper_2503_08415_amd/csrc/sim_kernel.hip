@@ -772,6 +772,15 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
             if (j < nchd) nneed += popc(ballot(rr[j] == dG));
           return nneed <= freeb;
         };
+        // An iteration whose FCFS admissions may run in place: only trace
+        // requests wait (none preempted), no prefill runs, a chunked budget,
+        // continuous batching on one worker.  It is priced like a head
+        // prefill's completion, with no head.
+        bool adm_next = false;
+        auto adm_here = [&]() {
+          return NCH > 1 && MODE == kStageOne && !unlimited && npf == 0 && npre == 0 &&
+                 policy != TS_POLICY_STATIC && dG < stop_hard;
+        };
         bool more = true;
         while (more) {
           // steady iterations up to the segment's last
@@ -912,12 +921,21 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
                 thr = next < N ? __builtin_fmin((double)rdl64(w_arr, next - wbase), kT52d)
                                : kT52d;
               }
-              if (nruna == 0 ||
-                  ((npre > 0 || nwait > 0) && adm_open() && !head_blocked(freeb))) {
-                more = false;  // nothing runs, or the freed slot or blocks may admit
+              if (nruna == 0) {
+                more = false;  // nothing runs
                 break;
               }
-              setup();
+              const bool want = (npre > 0 || nwait > 0) && adm_open() && !head_blocked(freeb);
+              if (want && !adm_here()) {
+                more = false;  // the freed slot or blocks may admit: general path
+                break;
+              }
+              if (want) {  // the next iteration admits in place (it needs no segment)
+                stop = dG;
+                adm_next = true;
+              } else {
+                setup();
+              }
             } else {
               ++dG;
             }
@@ -927,19 +945,37 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
             }
           }
           if (!more) break;
-            // The head prefill completes in this iteration (or the cap /
-            // watchdog is reached).  Its first completion, with no decode
-            // finishing here, is handled in place; everything else runs on
-            // the general path.
-            if (stop >= stop_hard || npf != 1 || dG == fin_at ||
-                (fl_p & (FL_FIRST | FL_STALE)) != 0 || MODE == kStagePrefill)
+            // The head prefill completes in this iteration, or an admission
+            // iteration was scheduled (or the cap / watchdog is reached).  A
+            // head's first completion and the admissions are handled in place,
+            // with the decodes that finish here; everything else runs on the
+            // general path.
+            const bool head = npf == 1;
+            if (stop >= stop_hard || MODE == kStagePrefill || npf > 1 ||
+                (head && (fl_p & (FL_FIRST | FL_STALE)) != 0) || (!head && !adm_next))
               break;
-            const int CD = cd_seg + nDa * (dG - seg0);  // decode keys at this iteration
+            adm_next = false;
+            // decode keys at this iteration (an admission iteration has no
+            // segment: summed over the alive decodes)
+            int CD;
+            if (head) {
+              CD = cd_seg + nDa * (dG - seg0);
+            } else {
+              int csl = 0;
+#pragma unroll
+              for (int j = 0; j < NCH; ++j) {
+                if (j < nchd) {
+                  const int ctx0 = j == 0 ? h0.ctx : L.x_ctx[(j - 1) * 64 + lane];
+                  csl += rr[j] >= 0 ? ctx0 + 1 : 0;
+                }
+              }
+              CD = wsum(csl) + nDa * dG;
+            }
             close_segment();
             t = (int64_t)rdl_f64(t_d, 1);  // arrivals up to the clock
             intake();
             thr = next < N ? __builtin_fmin((double)rdl64(w_arr, next - wbase), kT52d) : kT52d;
-            const int left = tgt_p - ctx_p;
+            const int left = head ? tgt_p - ctx_p : 0;
             const int R1 = K - nDa - left;  // budget left after the completing prefill
             // FCFS admissions into the rest of the budget, in place, from the
             // waiting trace requests at the queue head.  When the first one's
@@ -1010,11 +1046,12 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
             }
             freeb -= need_sum;
             const int TP = left + sq;
-            const int64_t AP = (int64_t)left * ctx_p + ((int64_t)left * (left + 1)) / 2 + ap_new;
+            const int64_t AP =
+                (head ? (int64_t)left * ctx_p + ((int64_t)left * (left + 1)) / 2 : 0) + ap_new;
             double iter_d;
-            const int64_t iter_ns = iteration_ns(roofc, A.n_layers, iF, iB, nDa + TP, TP, AP,
-                                                 tgt_p + sq, nDa, CD, nDa + 1 + c, 0.0, false,
-                                                 &iter_d);
+            const int64_t iter_ns =
+                iteration_ns(roofc, A.n_layers, iF, iB, nDa + TP, TP, AP, (head ? tgt_p : 0) + sq,
+                             nDa, CD, nDa + (head ? 1 : 0) + c, 0.0, false, &iter_d);
             const int64_t t_beg = t;
             const int64_t t_end = t_beg + iter_ns;
             ubl = ubl + (lane == 1 ? (double)(NB - freeb) * iter_d : 0.0);
@@ -1041,9 +1078,35 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
             }
             em = 0.0;
             it = 0.0;
+            if (!head || dG == fin_at) {
+              // alive decodes emitting their last token finish here (their
+              // blocks are free from the next iteration on)
+              int nfin = 0, l_freed = 0;
+#pragma unroll
+              for (int j = 0; j < NCH; ++j) {
+                if (j < nchd) {
+                  const int e = (j - 1) * 64 + lane;
+                  const int rem0 = j == 0 ? h0.rem : L.x_rem[e];
+                  const bool fin = rr[j] >= 0 && rem0 - 1 == dG;
+                  const uint64_t fm = ballot(fin);
+                  if (fm != 0) {
+                    const int ctx0 = j == 0 ? h0.ctx : L.x_ctx[e];
+                    const int64_t gap0 = j == 0 ? h0.gap : L.x_gap[e];  // folded above
+                    record_done(fin, j * 64 + lane, t_end, gap0);
+                    l_freed += fin ? divB(ctx0 + rr[j]) : 0;  // held blocks
+                    rr[j] = fin ? -0x40000000 : rr[j];
+                    nfin += popc(fm);
+                  }
+                }
+              }
+              freeb += wsum(l_freed);
+              n_done += nfin;
+              nDa -= nfin;
+              nruna -= nfin;
+            }
             // the completed prefill emits its first token and joins the
             // decodes at iteration dG + 1
-            {
+            if (head) {
               const int js = nD >> 6, ls = nD & 63, g1 = dG + 1;
               int room_s, id_s;
               if (NCH == 1 || js == 0) {
@@ -1118,6 +1181,7 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
               nwait -= a;
               if (nwait == 0) next_new = next;
               if (a > c) {  // the new head prefill, in slot s0 + c
+                npf = 1;
                 ctx_p = q_new;
                 tgt_p = rdl(c_p, a - 1);
                 fl_p = 0;
@@ -1152,6 +1216,7 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
               ++nruna;
               ++next_new;
               if (--nwait == 0) next_new = next;
+              npf = 1;
               ctx_p = q_new;
               tgt_p = tgt_h;
               fl_p = 0;
@@ -1160,9 +1225,14 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
             }
             ++dG;
             seg0 = dG;
-            if ((npre > 0 || nwait > 0) && adm_open() && !head_blocked(freeb))
-              break;  // the head may be admitted next
-            setup();
+            const bool want = (npre > 0 || nwait > 0) && adm_open() && !head_blocked(freeb);
+            if (want && !adm_here()) break;  // the head may be admitted next: general path
+            if (want) {  // the next iteration admits in place (it needs no segment)
+              stop = dG;
+              adm_next = true;
+            } else {
+              setup();
+            }
           if (!next_ok()) break;
         }
         // the last segment's bookkeeping, the point's counters, the decodes
