@@ -973,8 +973,10 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
             }
             close_segment();
             t = (int64_t)rdl_f64(t_d, 1);  // arrivals up to the clock
-            intake();
-            thr = next < N ? __builtin_fmin((double)rdl64(w_arr, next - wbase), kT52d) : kT52d;
+            if (next < N && rdl64(w_arr, next - wbase) <= t) {
+              intake();
+              thr = next < N ? __builtin_fmin((double)rdl64(w_arr, next - wbase), kT52d) : kT52d;
+            }
             const int left = head ? tgt_p - ctx_p : 0;
             const int R1 = K - nDa - left;  // budget left after the completing prefill
             // FCFS admissions into the rest of the budget, in place, from the
