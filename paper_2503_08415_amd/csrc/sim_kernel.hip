@@ -1880,42 +1880,111 @@ __device__ __forceinline__ int nearest_rank_index(int pct, int n) {
   return (int)(((int64_t)pct * n + 99) / 100) - 1;
 }
 
+// Latency buckets for the percentile search: 16 per octave, monotone in the
+// value (values below 16 are their own bucket; a value of bit length bl >= 5
+// goes to 16 * bl + its next 4 bits below the leading one).
+constexpr int kBuckets = 1040;   // 16 * 64 + 16
+constexpr int kCandCap = 512;    // a rank's candidates kept in LDS
+__device__ __forceinline__ int lat_bucket(uint64_t v) {
+  if (v < 16) return (int)v;
+  const int bl = 64 - __builtin_clzll(v);
+  return (bl << 4) | (int)((v >> (bl - 5)) & 15u);
+}
+
+// For each of NR ranks (0-based, below the count), the bucket holding the
+// rank-th smallest value and the rank within that bucket, from a bucket
+// histogram: a block-wide prefix sum over 5 buckets per thread.
+template <int NR>
+__device__ void locate_ranks(const int* hist, const int* ks, int* wsum_sh, int* out_b,
+                             int* out_k) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  int loc[5];
+  int tot = 0;
+#pragma unroll
+  for (int i = 0; i < 5; ++i) {
+    const int b = tid * 5 + i;
+    loc[i] = b < kBuckets ? hist[b] : 0;
+    tot += loc[i];
+  }
+  const int inc = scan_i32(tot);
+  if (lane == 63) wsum_sh[w] = inc;
+  __syncthreads();
+  int before = inc - tot;
+  for (int v = 0; v < w; ++v) before += wsum_sh[v];
+#pragma unroll
+  for (int r = 0; r < NR; ++r) {
+    const int k = ks[r];
+    if (k >= before && k < before + tot) {
+      int acc = before, bsel = -1, ksel = 0;
+#pragma unroll
+      for (int i = 0; i < 5; ++i) {
+        if (bsel < 0 && k < acc + loc[i]) {
+          bsel = i;
+          ksel = k - acc;
+        }
+        acc += loc[i];
+      }
+      out_b[r] = tid * 5 + bsel;
+      out_k[r] = ksel;
+    }
+  }
+  __syncthreads();
+}
+
 // The point's request statistics from its request records, one 256-thread
 // workgroup per point: latency sums (TTFT = first token - arrival, E2E =
 // finish - arrival, TPOT numerator = finish - first token), the largest E2E,
 // the last finish, the SLO counts (Sec. IV-B), the digest over finished and
 // rejected records, then nearest-rank percentiles of the finished requests'
-// latencies by radix select over a dense copy of them.  With pad_pending
-// (per-request output) the row's entries past the trace also get "pending"
-// records.
+// latencies.  The record pass also builds a bucket histogram of each
+// latency and copies the latencies densely to HBM; the buckets of the ranks
+// are located, one pass over the dense copy gathers each rank's bucket into
+// LDS, and a radix select there finds the exact value (a bucket too full for
+// LDS is selected by radix passes over the dense copy instead).  With
+// pad_pending (per-request output) the row's entries past the trace also
+// get "pending" records.
 __global__ __launch_bounds__(256) void stats_kernel(ts_req_result* rec, const TraceRec* recs,
                                                     const PointInfo* pinfo,
                                                     ts_point_result* res, int64_t* e2e,
                                                     int64_t* ttft, int max_n, int n_points,
                                                     int64_t slo_ttft_ns, int64_t slo_tpot_ns,
                                                     int pad_pending) {
-  __shared__ int hist[3 * 256];
-  __shared__ int sh[9];
+  __shared__ int hist[2 * kBuckets];           // E2E buckets, then TTFT buckets
+  __shared__ int64_t cand[5][kCandCap];        // candidates of the 5 ranks
+  __shared__ int sh[16];
+  __shared__ int rb[5], rk[5];                 // rank bucket, rank within it
+  __shared__ int ks[5];                        // the ranks (0-based)
+  __shared__ int64_t r5[5];                    // the percentiles
+  __shared__ unsigned int ccount[5];
   __shared__ unsigned long long acc_sum[4];  // TTFT, E2E, TPOT numerator, digest
   __shared__ long long acc_max[2];           // largest E2E, last finish
   __shared__ unsigned int acc_cnt[3];        // finished (dense index), slo_ok, slo_tpot_ok
+  const int tid = threadIdx.x, lane = tid & 63;
   for (int p = blockIdx.x; p < n_points; p += gridDim.x) {
     const PointInfo pi = pinfo[p];
     ts_req_result* R = rec + (size_t)p * (size_t)max_n;
     int64_t* ve = e2e + (size_t)p * (size_t)max_n;
     int64_t* vt = ttft + (size_t)p * (size_t)max_n;
-    if (threadIdx.x < 4) acc_sum[threadIdx.x] = 0;
-    if (threadIdx.x < 2) acc_max[threadIdx.x] = -1;
-    if (threadIdx.x < 3) acc_cnt[threadIdx.x] = 0;
+    if (tid < 4) acc_sum[tid] = 0;
+    if (tid < 2) acc_max[tid] = -1;
+    if (tid < 3) acc_cnt[tid] = 0;
+    if (tid < 5) ccount[tid] = 0;
+    for (int b = tid; b < 2 * kBuckets; b += 256) hist[b] = 0;
     __syncthreads();
     uint64_t s_tt = 0, s_ee = 0, s_tp = 0, dig = 0;
     int64_t mx = -1, lf = -1;
     unsigned int n_slo = 0, n_slo_tpot = 0;
-    for (int g = threadIdx.x; g < pi.n; g += 256) {
-      const ts_req_result r = R[g];
-      if (r.status == TS_REQ_DONE) {
+    for (int g0 = 0; g0 < pi.n; g0 += 256) {  // whole waves, so the ballots see every lane
+      const int g = g0 + tid;
+      ts_req_result r;
+      r.status = TS_REQ_PENDING;
+      if (g < pi.n) r = R[g];
+      const bool done = r.status == TS_REQ_DONE;
+      int64_t tt = 0, ee = 0;
+      if (done) {
         const int64_t arr = recs[pi.trace_off + g].arrival_ns;
-        const int64_t tt = r.first_token_ns - arr, ee = r.finish_ns - arr;
+        tt = r.first_token_ns - arr;
+        ee = r.finish_ns - arr;
         s_tt += (uint64_t)tt;
         s_ee += (uint64_t)ee;
         s_tp += (uint64_t)(r.finish_ns - r.first_token_ns);
@@ -1923,11 +1992,20 @@ __global__ __launch_bounds__(256) void stats_kernel(ts_req_result* rec, const Tr
         lf = r.finish_ns > lf ? r.finish_ns : lf;
         n_slo += (tt <= slo_ttft_ns && r.max_gap_ns <= slo_tpot_ns) ? 1u : 0u;
         n_slo_tpot += r.max_gap_ns <= slo_tpot_ns ? 1u : 0u;
-        const unsigned int pos = atomicAdd(&acc_cnt[0], 1u);
+        atomicAdd(&hist[lat_bucket((uint64_t)ee)], 1);
+        atomicAdd(&hist[kBuckets + lat_bucket((uint64_t)tt)], 1);
+      }
+      // dense positions: one counter update per wave
+      const uint64_t dm = ballot(done);
+      unsigned int base = 0;
+      if (lane == 0 && dm != 0) base = atomicAdd(&acc_cnt[0], (unsigned int)popc(dm));
+      base = (unsigned int)__builtin_amdgcn_readfirstlane((int)base);
+      if (done) {
+        const unsigned int pos = base + (unsigned int)rank_below(dm);
         ve[pos] = ee;
         vt[pos] = tt;
       }
-      if (r.status == TS_REQ_DONE || r.status == TS_REQ_REJECTED)
+      if (done || r.status == TS_REQ_REJECTED)
         dig += record_hash(g, r.admit_ns, r.first_token_ns, r.finish_ns, r.max_gap_ns,
                            r.n_preempt, r.status);
     }
@@ -1935,7 +2013,7 @@ __global__ __launch_bounds__(256) void stats_kernel(ts_req_result* rec, const Tr
       ts_req_result o;
       o.admit_ns = -1; o.first_token_ns = -1; o.finish_ns = -1; o.max_gap_ns = 0;
       o.n_preempt = 0; o.status = TS_REQ_PENDING;
-      for (int g = pi.n + (int)threadIdx.x; g < max_n; g += 256) R[g] = o;
+      for (int g = pi.n + tid; g < max_n; g += 256) R[g] = o;
     }
     atomicAdd(&acc_sum[0], (unsigned long long)s_tt);
     atomicAdd(&acc_sum[1], (unsigned long long)s_ee);
@@ -1948,24 +2026,55 @@ __global__ __launch_bounds__(256) void stats_kernel(ts_req_result* rec, const Tr
     __syncthreads();
     const int n = (int)acc_cnt[0];
     const int64_t max_e2e = acc_max[0];
-    int64_t r5[5] = {-1, -1, -1, -1, -1};
+    if (tid < 5) r5[tid] = -1;
     if (n > 0) {
+      // ranks: p50, p90, p99 of E2E, then p50, p99 of TTFT
+      if (tid < 5) ks[tid] = nearest_rank_index(tid == 0 || tid == 3 ? 50 : (tid == 1 ? 90 : 99), n);
+      __syncthreads();
+      locate_ranks<3>(hist, ks, sh, rb, rk);
+      locate_ranks<2>(hist + kBuckets, ks + 3, sh, rb + 3, rk + 3);
+      // gather each rank's bucket
+      for (int i = tid; i < n; i += 256) {
+        const int64_t e = ve[i], tv = vt[i];
+        const int be = lat_bucket((uint64_t)e), bt = lat_bucket((uint64_t)tv);
+#pragma unroll
+        for (int r = 0; r < 5; ++r) {
+          const int64_t v = r < 3 ? e : tv;
+          if ((r < 3 ? be : bt) == rb[r]) {
+            const unsigned int c = atomicAdd(&ccount[r], 1u);
+            if (c < (unsigned int)kCandCap) cand[r][c] = v;
+          }
+        }
+      }
+      __syncthreads();
       // every latency lies in [0, max_e2e] (a first token never comes after
       // the finish): digits above the top one are zero for all of them
       const uint64_t m = (uint64_t)max_e2e;
       const int bits = m == 0 ? 1 : 64 - __builtin_clzll(m);
-      const int top_shift = ((bits - 1) / 8) * 8;
-      const int ke[3] = {nearest_rank_index(50, n), nearest_rank_index(90, n),
-                         nearest_rank_index(99, n)};
-      const int kt[2] = {nearest_rank_index(50, n), nearest_rank_index(99, n)};
-      if (threadIdx.x < 3) sh[6 + threadIdx.x] = ke[threadIdx.x];
-      __syncthreads();
-      select_ranks<3>(ve, n, ke, top_shift, r5, hist, sh);
-      if (threadIdx.x < 2) sh[4 + threadIdx.x] = kt[threadIdx.x];
-      __syncthreads();
-      select_ranks<2>(vt, n, kt, top_shift, r5 + 3, hist, sh);
+      const int top_all = ((bits - 1) / 8) * 8;
+#pragma unroll 1
+      for (int r = 0; r < 5; ++r) {
+        const int cnt = (int)ccount[r];
+        const int b = rb[r];
+        if (b < 16) {  // a bucket of one value
+          if (tid == 0) r5[r] = b;
+          continue;
+        }
+        // the bucket's values are below 2^(b / 16)
+        const int top = ((b / 16 - 1) / 8) * 8;
+        if (tid == 0) sh[2] = cnt <= kCandCap ? rk[r] : ks[r];
+        __syncthreads();
+        const int kk = cnt <= kCandCap ? rk[r] : ks[r];
+        int64_t v;
+        if (cnt <= kCandCap)
+          select_ranks<1>(cand[r], cnt, &kk, top, &v, hist, sh);
+        else
+          select_ranks<1>(r < 3 ? ve : vt, n, &kk, top_all, &v, hist, sh);
+        if (tid == 0) r5[r] = v;
+      }
     }
-    if (threadIdx.x == 0) {
+    __syncthreads();
+    if (tid == 0) {
       ts_point_result& o = res[p];
       o.sum_ttft_ns = (int64_t)acc_sum[0];
       o.sum_e2e_ns = (int64_t)acc_sum[1];

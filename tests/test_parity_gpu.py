@@ -497,6 +497,35 @@ def test_sweep_subsets_per_request(S, oracle, name, nreq):
     assert len(set(pts["max_batch"].tolist())) > 1 or name == "c4"
 
 
+def test_percentiles_when_many_latencies_are_equal(S, oracle):
+    """Requests served one at a time with equal lengths have equal latencies:
+    far more of them share a latency bucket than the statistics kernel keeps
+    in LDS, so those percentiles come from radix passes over the whole
+    latency array; one point has a few longer requests, so its p99 lies in
+    another bucket."""
+    m = W.MODELS["llama2-7b"]
+    n = 1500
+    rng = np.random.default_rng(7)
+    gaps = np.arange(n, dtype=np.int64) * 10_000_000_000
+    same = {"arrival_ns": gaps, "prompt_len": np.full(n, 100, np.int32),
+            "output_len": np.full(n, 50, np.int32)}
+    out_len = np.full(n, 50, np.int32)
+    out_len[rng.choice(n, 40, replace=False)] = 400
+    mixed = {"arrival_ns": gaps, "prompt_len": np.full(n, 100, np.int32), "output_len": out_len}
+    pts = {"peak_flops": np.full(2, 312e12), "mem_bw": np.full(2, 2e12),
+           "capacity_bytes": np.full(2, 80_000_000_000, np.int64),
+           "mem_util_permille": np.full(2, 900, np.int32), "block_size": np.full(2, 16, np.int32),
+           "max_batch": np.full(2, 64, np.int32), "chunk_size": np.zeros(2, np.int32),
+           "trace_id": np.array([0, 1], np.int32)}
+    traces = [same, mixed]
+    o_out, o_req = oracle.run_points(m, traces, pts, per_request=True)
+    out, req = gpu_run(S, m, traces, pts, per_request=True, iter_cap=cap_from(o_out))
+    compare_points(out, o_out, "equal latencies")
+    compare_requests(req, o_req, "equal latencies")
+    assert out["p50_e2e_ns"][0] == out["p99_e2e_ns"][0]
+    assert out["p99_e2e_ns"][1] > out["p50_e2e_ns"][1]
+
+
 def test_determinism_and_point_order(S):
     m, traces, pts = W.make_config("c3", n_requests=300)
     n = len(pts["peak_flops"])
