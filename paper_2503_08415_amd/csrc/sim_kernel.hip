@@ -734,11 +734,15 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
           }
           stop = stop_hard;
           if (q > 0) {  // the head prefill completes in iteration kc
-            // floor(n / q) for 0 <= n, q < 2^31: the correctly rounded fp64
-            // quotient is that or one more
+            // floor(n / q) for 0 <= n < 2^21 and 1 <= q <= 2^20 (a target
+            // below 2^21 tokens, a budget of at most 2^20): n times the fp32
+            // reciprocal of q (relative error below 2^-22) is within 1/2 of
+            // n / q, so its truncation is off by at most one, corrected by
+            // the remainder
             const int n = tgt_p - ctx_p - 1;
-            int kq = (int)((double)n / (double)q);
-            if ((int64_t)kq * q > (int64_t)n) --kq;
+            int kq = (int)((float)n * __builtin_amdgcn_rcpf((float)q));
+            const int rm = n - kq * q;
+            kq = rm < 0 ? kq - 1 : (rm >= q ? kq + 1 : kq);
             const int kc = dG + kq;
             stop = kc < stop ? kc : stop;
           }
