@@ -794,7 +794,7 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
             int W = stop - dG;
             W = W < 64 ? W : 64;
             W = fin_at - dG + 1 < W ? fin_at - dG + 1 : W;
-            if (W >= 2) {
+            if (W >= 3) {  // (two iterations cost less one at a time)
               // A block of consecutive iterations, lane i pricing iteration
               // dG + i exactly as one iteration at a time would (the
               // operators' FLOPs and bytes are exact integers, stepped by
