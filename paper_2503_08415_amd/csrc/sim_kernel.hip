@@ -1884,29 +1884,33 @@ __device__ __forceinline__ int nearest_rank_index(int pct, int n) {
   return (int)(((int64_t)pct * n + 99) / 100) - 1;
 }
 
-// Latency buckets for the percentile search: 16 per octave, monotone in the
-// value (values below 16 are their own bucket; a value of bit length bl >= 5
-// goes to 16 * bl + its next 4 bits below the leading one).
-constexpr int kBuckets = 1040;   // 16 * 64 + 16
+// Latency buckets for the percentile search: 2^kSubBits per octave,
+// monotone in the value (values below 2^kSubBits are their own bucket; a
+// value of bit length bl > kSubBits goes to 2^kSubBits * bl + its next
+// kSubBits bits below the leading one).
+constexpr int kSubBits = 5;
+constexpr int kSub = 1 << kSubBits;
+constexpr int kBuckets = kSub * 65;
+constexpr int kPerThread = (kBuckets + 255) / 256;  // buckets per thread in the prefix sum
 constexpr int kCandCap = 512;    // a rank's candidates kept in LDS
 __device__ __forceinline__ int lat_bucket(uint64_t v) {
-  if (v < 16) return (int)v;
+  if (v < (uint64_t)kSub) return (int)v;
   const int bl = 64 - __builtin_clzll(v);
-  return (bl << 4) | (int)((v >> (bl - 5)) & 15u);
+  return (bl << kSubBits) | (int)((v >> (bl - 1 - kSubBits)) & (uint64_t)(kSub - 1));
 }
 
 // For each of NR ranks (0-based, below the count), the bucket holding the
 // rank-th smallest value and the rank within that bucket, from a bucket
-// histogram: a block-wide prefix sum over 5 buckets per thread.
+// histogram: a block-wide prefix sum over kPerThread buckets per thread.
 template <int NR>
 __device__ void locate_ranks(const int* hist, const int* ks, int* wsum_sh, int* out_b,
                              int* out_k) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  int loc[5];
+  int loc[kPerThread];
   int tot = 0;
 #pragma unroll
-  for (int i = 0; i < 5; ++i) {
-    const int b = tid * 5 + i;
+  for (int i = 0; i < kPerThread; ++i) {
+    const int b = tid * kPerThread + i;
     loc[i] = b < kBuckets ? hist[b] : 0;
     tot += loc[i];
   }
@@ -1921,14 +1925,14 @@ __device__ void locate_ranks(const int* hist, const int* ks, int* wsum_sh, int* 
     if (k >= before && k < before + tot) {
       int acc = before, bsel = -1, ksel = 0;
 #pragma unroll
-      for (int i = 0; i < 5; ++i) {
+      for (int i = 0; i < kPerThread; ++i) {
         if (bsel < 0 && k < acc + loc[i]) {
           bsel = i;
           ksel = k - acc;
         }
         acc += loc[i];
       }
-      out_b[r] = tid * 5 + bsel;
+      out_b[r] = tid * kPerThread + bsel;
       out_k[r] = ksel;
     }
   }
@@ -2060,12 +2064,12 @@ __global__ __launch_bounds__(256) void stats_kernel(ts_req_result* rec, const Tr
       for (int r = 0; r < 5; ++r) {
         const int cnt = (int)ccount[r];
         const int b = rb[r];
-        if (b < 16) {  // a bucket of one value
+        if (b < kSub) {  // a bucket of one value
           if (tid == 0) r5[r] = b;
           continue;
         }
-        // the bucket's values are below 2^(b / 16)
-        const int top = ((b / 16 - 1) / 8) * 8;
+        // the bucket's values are below 2^(b / kSub)
+        const int top = ((b / kSub - 1) / 8) * 8;
         if (tid == 0) sh[2] = cnt <= kCandCap ? rk[r] : ks[r];
         __syncthreads();
         const int kk = cnt <= kCandCap ? rk[r] : ks[r];
