@@ -273,16 +273,18 @@ int ts_sweep_timing(ts_sweep *h, float *sim_ms, float *stats_ms);
 int ts_sweep_kernel_timing(ts_sweep *h, float *ms, int32_t *n_points);
 
 /* Simulated iterations per launch of the last run: iters[k] receives the
- * summed iteration counts of the points launch k simulated to completion
- * (index as for ts_sweep_kernel_timing).  When every one-worker point is a
- * simple one (continuous batching, recompute preemption, no admission ratio,
- * no request that could never fit, no watchdog) and some allow more than 64
+ * iterations launch k simulated (index as for ts_sweep_kernel_timing); they
+ * add up to the points' n_iters.  When every one-worker point is a simple
+ * one (continuous batching, recompute preemption, no admission ratio, no
+ * request that could never fit, no watchdog) and some allow more than 64
  * running requests, the max_batch <= 64 launch (k = 0) takes all of them
- * while at most 64 run at once; a point that needs more slots is handed to
- * the 128-slot launch (k = 1), and from there, if it needs more than 128, to
- * the 256-slot launch (k = 2), each time simulated again from the start;
- * only the launch that completes it counts its iterations.  Waits for the run.
- * TS_ERR_STATE before the first run. */
+ * while at most 64 run at once; a point whose admissions need more slots is
+ * handed to the 128-slot launch (k = 1), and from there, if it needs more
+ * than 128, to the 256-slot launch (k = 2).  The wider launch continues the
+ * point from the start of that iteration (each launch counts the iterations
+ * it simulated), or, when the iteration had already admitted a full window,
+ * simulates it again from the start (then only the launch that does counts
+ * those iterations).  Waits for the run.  TS_ERR_STATE before the first run. */
 int ts_sweep_kernel_work(ts_sweep *h, int64_t *iters);
 
 /* For callers that cannot allocate device memory (tight serving loops,

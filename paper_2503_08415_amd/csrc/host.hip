@@ -226,6 +226,7 @@ BufCounts buf_counts(const Plan& P) {
   // at most class_n[2]
   c.handed = P.hand_over ? (size_t)(P.class_n[1] + P.class_n[2]) : 0;
   c.work = kLaunches;
+  c.resume = (size_t)P.n_resume;
   c.queue = (size_t)P.max_grid() * kQueueCap;
   c.res = (size_t)(P.count + P.n_extra);
   c.req = (size_t)P.count * per_point;  // the request records (always)
@@ -246,7 +247,8 @@ double BufCounts::bytes() const {
          2.0 * (double)lat * sizeof(int64_t) + (double)pd * sizeof(PdAux) +
          2.0 * (double)s1 * sizeof(int64_t) + (double)sub * (sizeof(int64_t) + sizeof(int32_t)) +
          (double)gids * sizeof(int32_t) + (double)pinfo * sizeof(PointInfo) +
-         (double)handed * sizeof(int32_t) + (double)work * sizeof(unsigned long long);
+         (double)handed * sizeof(int32_t) + (double)work * sizeof(unsigned long long) +
+         (double)resume * (double)kResumeBytes;
 }
 
 }  // namespace tsw
@@ -282,6 +284,7 @@ void release(ts_sweep* h) {
   (void)hipFree(b.pinfo);
   (void)hipFree(b.handed);
   (void)hipFree(b.work);
+  (void)hipFree(b.resume);
   for (int c = 0; c < kLaunches; ++c) {
     if (h->ev.k0[c]) (void)hipEventDestroy(h->ev.k0[c]);
     if (h->ev.k1[c]) (void)hipEventDestroy(h->ev.k1[c]);
@@ -602,7 +605,7 @@ int make_plan(const ts_model* model, const ts_trace* traces, int32_t n_traces,
   // 64-slot launch (more waves per SIMD, fewer registers) while at most 64
   // run at once; the few that need more are handed to the 128-slot launch,
   // and from there those that need more than 128 to the 256-slot launch,
-  // each time simulated again from the start.
+  // each continuing from its hand-over record.
   bool all_simple = true;
   for (int c = 0; c < kClasses; ++c)
     all_simple = all_simple && (P->class_n[c] == 0 || P->simple[c]);
@@ -613,11 +616,18 @@ int make_plan(const ts_model* model, const ts_trace* traces, int32_t n_traces,
                      [&](int32_t a, int32_t b) { return est[(size_t)a] > est[(size_t)b]; });
     std::copy(all.begin(), all.end(), order.begin());
     P->class_off[0] = 0;
-    P->class_n[2] = P->class_n[2];                  // points that may reach the 256-slot launch
-    P->class_n[1] = P->class_n[1] + P->class_n[2];  // ... the 128-slot launch
+    // class_n[2]: the points that may reach the 256-slot launch; class_n[1]:
+    // those that may reach the 128-slot one
+    P->class_n[1] = P->class_n[1] + P->class_n[2];
     P->class_n[0] = (int)all.size();
     P->simple[0] = P->simple[1] = P->simple[2] = true;
     P->hand_over = true;
+  }
+  // a hand-over state slot for each point a launch may hand on
+  P->n_resume = 0;
+  for (size_t u = 0; u < dp.size(); ++u) {
+    const bool wide = P->hand_over && stage[u] == kStageOne && dp[u].max_batch > 64;
+    dp[u].resume = wide ? P->n_resume++ : -1;
   }
   P->count = count;
   P->n_pd = (int32_t)aux.size();
@@ -711,6 +721,7 @@ int enqueue(const Plan& P, const DevBufs& B, hipStream_t s, const LaunchEvents* 
   a.handed_off[1] = P.class_n[1];
   a.handed_n = B.counter + kLaunches;
   a.n_dev = nullptr;
+  a.resume = P.hand_over ? B.resume : nullptr;
   a.time_limit_ticks = (uint64_t)P.time_limit_ms * 100000ull;  // 100 MHz clock
   a.n_layers = P.coef.n_layers;
   a.lc = P.lc;
@@ -837,6 +848,7 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
   if (ae == hipSuccess) ae = dev_alloc(&b.pinfo, n.pinfo);
   if (ae == hipSuccess) ae = dev_alloc(&b.handed, n.handed);
   if (ae == hipSuccess) ae = dev_alloc(&b.work, n.work);
+  if (ae == hipSuccess) ae = dev_alloc(&b.resume, n.resume * kResumeBytes);
   if (ae == hipSuccess) ae = dev_alloc(&b.pd, n.pd);
   if (ae == hipSuccess) ae = dev_alloc(&b.s1_admit, n.s1);
   if (ae == hipSuccess) ae = dev_alloc(&b.s1_first, n.s1);

@@ -85,6 +85,7 @@ size_t carve(const tsw::Plan& P, unsigned char* base, tsw::DevBufs* B) {
   b.pinfo = c.take<tsw::PointInfo>(n.pinfo);
   b.handed = c.take<int32_t>(n.handed);
   b.work = c.take<unsigned long long>(n.work);
+  b.resume = c.take<unsigned char>(n.resume * tsw::kResumeBytes);
   if (B) *B = b;
   return c.used;
 }

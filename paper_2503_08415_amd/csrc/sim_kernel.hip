@@ -255,8 +255,10 @@ __device__ __forceinline__ int64_t iteration_ns(const LaneRoof& c, double n_laye
 //   gap   largest interval between consecutive tokens so far
 // Held blocks are (max(ctx, tgt) + room) / block and are never stored.
 enum : int { FL_FIRST = 1, FL_STALE = 2, FL_IDLE = 4 };
-// internal point status: the point is handed to a launch with more slots
+// internal point status: the point is handed to a launch with more slots,
+// which continues from the hand-over state, or starts it over
 constexpr int kHandOver = -1;
+constexpr int kHandOverRedo = -2;
 
 struct Hot {
   int ctx, tgt, rem, room, fl, q;
@@ -313,8 +315,9 @@ __device__ __forceinline__ void store_chunk(SlotLds<NCH>& L, Hot& h0, int j, int
 // completes and their KV crosses the device's link) or kStageDecode (a
 // decode device: requests arrive with their prompt's KV and first token).
 // Returns false when the point needs more slots than this kernel holds (a
-// narrow launch taking wider points): its simulation is abandoned, nothing
-// it wrote is final, and a wider launch simulates it again from the start.
+// narrow launch taking wider points): its state at the start of the
+// iteration that needed them goes to its hand-over record, and a wider
+// launch continues from there (or starts it over when the record says so).
 template <int NCH, int MODE, bool SIMPLE>
 __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
                                                SlotLds<NCH>& L, QEntry* Q,
@@ -412,6 +415,70 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
   Hot h0;  // chunk 0 in registers
   h0.ctx = h0.tgt = h0.rem = h0.room = h0.fl = h0.q = 0;
   h0.gap = 0;
+
+  // A launch taking points handed over by a narrower one continues each
+  // from its hand-over state: the start of the general-path iteration whose
+  // admissions needed more slots (or starts it over when there is none).
+  // n_it0: the iterations the narrower launches counted as theirs.
+  int64_t n_it0 = 0;
+  if constexpr (SIMPLE && NCH > 1) {
+    if (A.n_dev != nullptr) {
+      const unsigned char* base = A.resume + (size_t)P.resume * kResumeBytes;
+      const ResumeHead* hp = reinterpret_cast<const ResumeHead*>(base);
+      auto u64 = [](int64_t v) -> int64_t {
+        const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)v);
+        const uint32_t hi =
+            (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)((uint64_t)v >> 32));
+        return (int64_t)(((uint64_t)hi << 32) | lo);
+      };
+      auto u32 = [](int v) -> int { return __builtin_amdgcn_readfirstlane(v); };
+      n_it0 = u64(hp->counted);
+      if (u32(hp->valid) != 0) {
+        t = u64(hp->t);
+        n_iters = u64(hp->n_iters);
+        n_pre_tot = u64(hp->n_pre_tot);
+        pf_tok = u64(hp->pf_tok);
+        dec_tok = u64(hp->dec_tok);
+        ubns = __builtin_bit_cast(double, u64(__builtin_bit_cast(int64_t, hp->ubns)));
+        freeb = u32(hp->freeb);
+        nrun = u32(hp->nrun);
+        npre = u32(hp->npre);
+        next = u32(hp->next);
+        next_new = u32(hp->next_new);
+        nwait = u32(hp->nwait);
+        wbase = u32(hp->wbase);
+        head_need = u32(hp->head_need);
+        peak = u32(hp->peak);
+        n_done = u32(hp->n_done);
+        const ResumeSlot* rs = reinterpret_cast<const ResumeSlot*>(base + kResumeHead);
+#pragma unroll
+        for (int j = 0; j < NCH; ++j) {
+          const int sl = j * 64 + lane;
+          if (sl < nrun) {
+            const ResumeSlot o = rs[sl];
+            Hot h;
+            h.ctx = o.ctx; h.tgt = o.tgt; h.rem = o.rem; h.room = o.room; h.fl = o.fl;
+            h.q = o.q; h.gap = o.gap;
+            store_chunk<NCH>(L, h0, j, lane, h);
+            L.id[sl] = o.id;
+            L.npre[sl] = o.npre;
+          }
+        }
+        const QEntry* rq = reinterpret_cast<const QEntry*>(base + kResumeHead +
+                                                           kResumeSlots * sizeof(ResumeSlot));
+        for (int i = lane; i < npre; i += 64) Q[i] = rq[i];
+        qhead = 0;
+        w_arr = INT64_MAX;
+        w_rj = 0;
+        if (wbase + lane < N) {
+          const TraceRec r = rec[wbase + lane];
+          w_arr = r.arrival_ns;
+          w_rj = rejected(r.prompt, r.output) ? 1 : 0;
+        }
+        __syncthreads();
+      }
+    }
+  }
 
   // intake: every request with arrival <= t joins the waiting set
   auto intake = [&]() {
@@ -1300,7 +1367,6 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
       status = TS_POINT_ITER_LIMIT;
       break;
     }
-
     // Prefill-first: when the waiting head can be admitted now the
     // iteration admits and prefills only and the decodes pause; otherwise it
     // runs every decode and admits nothing.
@@ -1460,6 +1526,7 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
     // prefill-first only in a prefill iteration).  A first admission leaves
     // the admission-ratio reserve free.
     int n_darr = 0;  // decode device: arrivals admitted, decoding in this iteration
+    bool adm_before = false;  // an earlier window of this iteration admitted
     if (!preempted && (!pff || pf_iter) && (policy != TS_POLICY_STATIC || nrun == 0)) {
       int guard = M + N / 64 + 4;  // each pass admits or advances a window
       while (nrun < M && (unlimited || R > 0 || (swap && npre > 0)) && (npre > 0 || nwait > 0) &&
@@ -1569,6 +1636,7 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
         }
         __syncthreads();
         nrun += a;
+        adm_before = true;
         if (darr) n_darr += a;
         if (fromq) {
           qhead = (qhead + a) & (kQueueCap - 1);
@@ -1588,7 +1656,11 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
       nch = nch < NCH ? nch : NCH;
     }
 
-    if (status == kHandOver) break;
+    if (status == kHandOver) {
+      freeb += nneed;  // undo this iteration's reservations (the rooms: below)
+      if (adm_before) status = kHandOverRedo;
+      break;
+    }
 
     // ---- 6. batch sums and the roofline iteration time (paused decodes of a
     // prefill-first iteration and requests swapped in now take no part)
@@ -1710,7 +1782,61 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
     t = t_end;
   }
 
-  if (status == kHandOver) return false;
+  if (status == kHandOver || status == kHandOverRedo) {
+    if constexpr (SIMPLE && NCH < 4) {
+      // The state at the hand-over iteration's start for the wider launch:
+      // its reservations undone (nothing else has changed, unless an earlier
+      // window admitted: then the wider launch starts over).  At an
+      // iteration's start every slot has less than a block of free room, so
+      // the decodes that reserved are those with a block of it now.
+      unsigned char* base = A.resume + (size_t)P.resume * kResumeBytes;
+      const bool valid = A.resume != nullptr && status == kHandOver;
+      if (valid) {
+        ResumeSlot* rs = reinterpret_cast<ResumeSlot*>(base + kResumeHead);
+#pragma unroll
+        for (int j = 0; j < NCH; ++j) {
+          const int sl = j * 64 + lane;
+          if (sl < nrun) {
+            const Hot h = load_chunk<NCH>(L, h0, j, lane);
+            ResumeSlot o;
+            o.ctx = h.ctx; o.tgt = h.tgt; o.rem = h.rem; o.room = h.room == B ? 0 : h.room;
+            o.fl = h.fl; o.q = 0; o.id = L.id[sl]; o.npre = L.npre[sl]; o.gap = h.gap;
+            rs[sl] = o;
+          }
+        }
+        QEntry* rq =
+            reinterpret_cast<QEntry*>(base + kResumeHead + kResumeSlots * sizeof(ResumeSlot));
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+        for (int i = lane; i < npre; i += 64) rq[i] = Q[(qhead + i) & (kQueueCap - 1)];
+      }
+      if (A.resume != nullptr && lane == 0) {
+        ResumeHead hd;
+        hd.t = t;
+        hd.n_iters = n_iters;
+        hd.n_pre_tot = n_pre_tot;
+        hd.pf_tok = pf_tok;
+        hd.dec_tok = dec_tok;
+        hd.ubns = ubns;
+        hd.freeb = freeb;
+        hd.nrun = nrun;
+        hd.npre = npre;
+        hd.next = next;
+        hd.next_new = next_new;
+        hd.nwait = nwait;
+        hd.wbase = wbase;
+        hd.head_need = head_need;
+        hd.peak = peak;
+        hd.n_done = n_done;
+        hd.valid = valid ? 1 : 0;
+        hd.counted = valid ? n_iters : n_it0;
+        *reinterpret_cast<ResumeHead*>(base) = hd;
+      }
+      if (!valid) n_iters = n_it0;  // the wider launch simulates these again
+    }
+    // the iterations simulated here, up to the hand-over state
+    atomicAdd(A.work, (unsigned long long)(lane == 0 ? n_iters - n_it0 : 0));
+    return false;
+  }
 
   // ---- a point stopped early (iteration cap, watchdog): the requests it
   // has not finished keep "pending" records: the running ones, the
@@ -1767,7 +1893,7 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
   }
   // the iterations this launch simulated to completion (every lane adds, lane
   // 0 the count: no lane-dependent branch)
-  atomicAdd(A.work, (unsigned long long)(lane == 0 ? n_iters : 0));
+  atomicAdd(A.work, (unsigned long long)(lane == 0 ? n_iters - n_it0 : 0));
   return true;
 }
 

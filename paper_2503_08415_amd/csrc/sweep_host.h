@@ -42,6 +42,7 @@ struct Plan {
   // launch 0 takes every one-worker point and hands those needing more than
   // 64 running slots to launch 1 or 2 (class_n[1], class_n[2] bound them).
   bool hand_over = false;
+  int n_resume = 0;             // hand-over state slots (points a launch may hand on)
   int stats_grid = 1;
   int max_grid() const;
 };
@@ -49,7 +50,7 @@ struct Plan {
 // Element counts of every device buffer of a plan.
 struct BufCounts {
   size_t recs, points, order, counter, queue, res, req, lat, pd, s1, sub, gids, pinfo,
-      handed, work;
+      handed, work, resume;
   double bytes() const;  // total, in bytes
 };
 BufCounts buf_counts(const Plan& P);
@@ -63,6 +64,7 @@ struct DevBufs {
   unsigned int* counter = nullptr;  // work-queue tickets, one per launch, then the handed counts
   unsigned long long* work = nullptr;  // simulated iterations completed per launch
   int32_t* handed = nullptr;        // points handed from launch 0 to launches 1 and 2
+  unsigned char* resume = nullptr;  // their hand-over states, kResumeBytes each
   QEntry* queue = nullptr;          // kQueueCap per workgroup, shared by the launches
   ts_point_result* res = nullptr;
   ts_req_result* req = nullptr;     // the request records, max_n per point (always)

@@ -45,7 +45,7 @@ struct __attribute__((aligned(16))) DevPoint {
   int32_t out_point;    // the design point's row (latencies, per-request records)
   int32_t pd;           // disaggregated point's PdAux index, -1 for a one-worker point
   int32_t unit;         // prefill or decode device index within its point
-  int32_t pad;
+  int32_t resume;       // hand-over state slot of a point a launch may hand on, else -1
 };
 
 constexpr int kMaxDev = TS_MAX_DEVICES;
@@ -109,6 +109,28 @@ struct LaneCoef {
 
 constexpr int kQueueCap = 256;  // >= max_batch: queue + running never exceed max_batch
 
+// Hand-over state: a point's simulation at the start of the general-path
+// iteration whose admissions needed more running slots than its launch has.
+// The wider launch continues from this state instead of simulating the
+// point again from the start.  Per slot: the head below,
+// then up to kResumeSlots running requests, then the preempted queue.
+struct __attribute__((aligned(16))) ResumeHead {
+  int64_t t, n_iters, n_pre_tot, pf_tok, dec_tok;
+  double ubns;
+  int64_t counted;  // iterations the narrower launches counted as theirs
+  int32_t freeb, nrun, npre, next, next_new, nwait, wbase, head_need, peak, n_done;
+  int32_t valid;    // 0: the point starts over in the wider launch
+};
+struct __attribute__((aligned(8))) ResumeSlot {
+  int32_t ctx, tgt, rem, room, fl, q, id, npre;
+  int64_t gap;
+};
+constexpr int kResumeSlots = 128;  // the widest launch that hands points on has 128 slots
+constexpr size_t kResumeHead = 128;
+constexpr size_t kResumeBytes =
+    kResumeHead + kResumeSlots * sizeof(ResumeSlot) + kQueueCap * sizeof(QEntry);
+static_assert(sizeof(ResumeHead) <= kResumeHead, "hand-over head fits its space");
+
 struct SimArgs {
   TraceRec* recs;              // traces, prefill devices' shares, decode devices' arrivals
   const DevPoint* points;
@@ -135,6 +157,9 @@ struct SimArgs {
   int32_t handed_off[2];
   unsigned int* handed_n;
   const unsigned int* n_dev;
+  // hand-over states (kResumeBytes per DevPoint::resume slot), nullptr when
+  // no launch hands points on
+  unsigned char* resume;
   double n_layers;
   LaneCoef lc;
   // disaggregated points
