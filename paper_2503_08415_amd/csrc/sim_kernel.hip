@@ -15,7 +15,15 @@
 //     over a 64-candidate window;
 //   * the batch sums that feed the roofline are wave reductions (DPP);
 //   * finished requests are found by ballot and removed by a stable
-//     compaction through LDS.
+//     compaction through LDS;
+//   * steady stretches advance decodes lazily and price up to 64 iterations
+//     at once, one per lane; a head prefill's completion, the admissions
+//     behind it and the finishes in the same iteration are handled in place;
+//   * a finish writes the request's record, from which the statistics
+//     kernel derives every latency statistic and percentile;
+//   * a narrow launch takes points wider than its slots and hands those that
+//     need more running requests to a wider launch, with a record of their
+//     state.
 // Scheduling state is integer; only the roofline is fp64, evaluated in a
 // fixed order with contraction disabled.
 #include <hip/hip_runtime.h>

@@ -497,6 +497,55 @@ def test_sweep_subsets_per_request(S, oracle, name, nreq):
     assert len(set(pts["max_batch"].tolist())) > 1 or name == "c4"
 
 
+@pytest.mark.parametrize("seed", [3, 4, 5, 6])
+def test_hand_over_records_under_memory_pressure(S, oracle, seed):
+    """Simple points of every width up to 256 slots under bursts of up to
+    260 simultaneous arrivals and small KV budgets: points continue in the
+    wider launches from their hand-over records with running requests,
+    reserved blocks and preempted requests waiting (or start over when a
+    window had already admitted).  Every request against the oracle; the
+    launches' iteration counts add up to the oracle's."""
+    m = {"n_layers": 2, "d_model": 64, "n_heads": 4, "n_kv_heads": 2, "ffn_dim": 128,
+         "ffn_gated": 1, "vocab": 100, "w_bytes": 2, "kv_bytes": 2, "weights_in_capacity": 0}
+    rng = np.random.default_rng(seed)
+    traces = []
+    for _ in range(6):
+        groups = rng.integers(1, 260, size=8)
+        arr = np.sort(np.concatenate([np.full(g, int(rng.integers(0, 2_000_000_000)))
+                                      for g in groups]))[:int(rng.integers(150, 400))]
+        n = len(arr)
+        traces.append({"arrival_ns": arr.astype(np.int64),
+                       "prompt_len": rng.integers(1, 300, n).astype(np.int32),
+                       "output_len": rng.integers(1, 120, n).astype(np.int32)})
+    k = 60
+    kv_tok = 2 * 2 * (64 // 4 * 2) * 2
+    pts = {"peak_flops": rng.choice([1e12, 5e12, 2e13], k),
+           "mem_bw": rng.choice([1e11, 5e11, 2e12], k),
+           "capacity_bytes": (rng.integers(200, 6000, k) * kv_tok * 16).astype(np.int64),
+           "mem_util_permille": np.full(k, 1000, np.int32),
+           "block_size": rng.choice([1, 4, 16], k).astype(np.int32),
+           "max_batch": rng.choice([64, 65, 100, 128, 129, 200, 256], k).astype(np.int32),
+           "trace_id": rng.integers(0, len(traces), k).astype(np.int32)}
+    ch = rng.choice([0, 256, 512, 1024], k)
+    pts["chunk_size"] = np.where(ch == 0, 0, np.maximum(ch, pts["max_batch"])).astype(np.int32)
+    # only points that reject nothing (the hand-over needs every point simple)
+    o_all, _ = oracle.run_points(m, traces, pts)
+    pts = W.subset_points(pts, np.nonzero(o_all["n_rejected"] == 0)[0])
+    o_out, o_req = oracle.run_points(m, traces, pts, per_request=True)
+    sw = S.Sweep(m, traces, pts, per_request=True, iter_cap=cap_from(o_out))
+    try:
+        sw.run()
+        out, req = sw.results()
+        work = sw.kernel_work()
+    finally:
+        sw.close()
+    compare_points(out, o_out, "hand-over records")
+    compare_requests(req, o_req, "hand-over records")
+    assert work[1] > 0 and work[2] > 0
+    assert int(o_out["n_preempt"].sum()) > 50
+    assert sum(work) == int(o_out["n_iters"].sum())
+
+
 def test_percentiles_when_many_latencies_are_equal(S, oracle):
     """Requests served one at a time with equal lengths have equal latencies:
     far more of them share a latency bucket than the statistics kernel keeps
