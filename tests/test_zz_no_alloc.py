@@ -2,7 +2,7 @@
 (every buffer in the library's static scratch), against the handle entry
 points ts_sweep_create + ts_sweep_run + ts_sweep_results on the same inputs:
 two calls in a row, the second with a smaller sweep, every point record and
-every request record bit for bit."""
+every request record bit for bit, also for points handed between launches."""
 import numpy as np
 import pytest
 
@@ -63,6 +63,28 @@ def test_static_entry_matches_handle_entry(S):
     e, re_ = S.run_static(m1, t1, p1, iter_cap=CAP, stream=0)
     f, rf = handle_run(S, m1, t1, p1, False)
     same(e, f, re_, rf)
+    # points wider than 64 slots under bursts: the 64-slot launch hands some
+    # on to the wider ones with hand-over records (in the scratch too)
+    rng = np.random.default_rng(3)
+    burst = {"arrival_ns": np.zeros(300, np.int64),
+             "prompt_len": rng.integers(16, 200, 300).astype(np.int32),
+             "output_len": rng.integers(5, 60, 300).astype(np.int32)}
+    spread = {"arrival_ns": np.sort(rng.integers(0, 3_000_000_000, 400)).astype(np.int64),
+              "prompt_len": rng.integers(16, 2000, 400).astype(np.int32),
+              "output_len": rng.integers(5, 300, 400).astype(np.int32)}
+    rows = [(256, 0, 0), (100, 0, 0), (64, 0, 0), (256, 512, 0), (130, 256, 1), (256, 0, 1)]
+    k = len(rows)
+    p4 = {"peak_flops": np.full(k, 312e12), "mem_bw": np.full(k, 2e12),
+          "capacity_bytes": np.full(k, 80_000_000_000, np.int64),
+          "mem_util_permille": np.full(k, 900, np.int32), "block_size": np.full(k, 16, np.int32),
+          "max_batch": np.array([r[0] for r in rows], np.int32),
+          "chunk_size": np.array([r[1] for r in rows], np.int32),
+          "trace_id": np.array([r[2] for r in rows], np.int32)}
+    m4 = W.MODELS["llama2-7b"]
+    print("call 4: 6 points wider than 64 slots, bursts of 300, per request", flush=True)
+    g, rg = S.run_static(m4, [burst, spread], p4, per_request=True, iter_cap=CAP)
+    h, rh = handle_run(S, m4, [burst, spread], p4, True)
+    same(g, h, rg, rh)
 
 
 def test_static_entry_limits(S):
