@@ -280,7 +280,8 @@ int ts_sweep_kernel_timing(ts_sweep *h, float *ms, int32_t *n_points);
  * running requests, the max_batch <= 64 launch (k = 0) takes all of them
  * while at most 64 run at once; a point whose admissions need more slots is
  * handed to the 128-slot launch (k = 1), and from there, if it needs more
- * than 128, to the 256-slot launch (k = 2).  The wider launch continues the
+ * than 128, to the 256-slot launch (k = 2), which take the handed points
+ * with the most requests left first.  The wider launch continues the
  * point from the start of that iteration (each launch counts the iterations
  * it simulated), or, when the iteration had already admitted a full window,
  * simulates it again from the start (then only the launch that does counts

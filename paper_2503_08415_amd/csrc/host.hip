@@ -221,10 +221,11 @@ BufCounts buf_counts(const Plan& P) {
   c.recs = P.recs.size();
   c.points = P.dp.size();
   c.order = P.order.size();
-  c.counter = kLaunches + 2;  // tickets per launch, handed points per wider class
+  // tickets per launch, then the handed points per wider class and bucket
+  c.counter = kLaunches + 2 * kHandBuckets;
   // the 64-slot launch hands at most class_n[1] points on, the 128-slot one
   // at most class_n[2]
-  c.handed = P.hand_over ? (size_t)(P.class_n[1] + P.class_n[2]) : 0;
+  c.handed = P.hand_over ? (size_t)kHandBuckets * (P.class_n[1] + P.class_n[2]) : 0;
   c.work = kLaunches;
   c.resume = (size_t)P.n_resume;
   c.queue = (size_t)P.max_grid() * kQueueCap;
@@ -706,7 +707,8 @@ int enqueue(const Plan& P, const DevBufs& B, hipStream_t s, const LaunchEvents* 
   };
   hipError_t e = record(ev ? ev->t0 : nullptr);
   if (e != hipSuccess) return device_error(e, "event record");
-  reset_counters_kernel<<<1, 64, 0, s>>>(B.counter, kLaunches + 2, B.work, kLaunches);
+  reset_counters_kernel<<<1, 64, 0, s>>>(B.counter, kLaunches + 2 * kHandBuckets, B.work,
+                                          kLaunches);
   SimArgs a;
   a.recs = B.recs;
   a.points = B.points;
@@ -718,7 +720,10 @@ int enqueue(const Plan& P, const DevBufs& B, hipStream_t s, const LaunchEvents* 
   a.work = nullptr;
   a.handed = B.handed;
   a.handed_off[0] = 0;
-  a.handed_off[1] = P.class_n[1];
+  a.handed_off[1] = kHandBuckets * P.class_n[1];
+  a.hand_cap[0] = P.class_n[1];
+  a.hand_cap[1] = P.class_n[2];
+  a.hand_cap_in = 0;
   a.handed_n = B.counter + kLaunches;
   a.n_dev = nullptr;
   a.resume = P.hand_over ? B.resume : nullptr;
@@ -747,7 +752,8 @@ int enqueue(const Plan& P, const DevBufs& B, hipStream_t s, const LaunchEvents* 
     a.n_dev = nullptr;
     if (P.hand_over && (l == 1 || l == 2)) {  // the points launch 0 handed over
       a.order = B.handed + a.handed_off[l - 1];
-      a.n_dev = B.counter + kLaunches + (l - 1);
+      a.n_dev = B.counter + kLaunches + (l - 1) * kHandBuckets;
+      a.hand_cap_in = a.hand_cap[l - 1];
     }
     a.counter = B.counter + l;
     a.work = B.work + l;

@@ -322,12 +322,14 @@ __device__ __forceinline__ void store_chunk(SlotLds<NCH>& L, Hot& h0, int j, int
 // device of a disaggregated point: requests leave when their prefill
 // completes and their KV crosses the device's link) or kStageDecode (a
 // decode device: requests arrive with their prompt's KV and first token).
-// Returns false when the point needs more slots than this kernel holds (a
-// narrow launch taking wider points): its state at the start of the
-// iteration that needed them goes to its hand-over record, and a wider
-// launch continues from there (or starts it over when the record says so).
+// Returns -1 when the point is done, else (a narrow launch taking wider
+// points, and the point needs more slots than this kernel holds) the bucket
+// of its remaining work, 0 .. kHandBuckets - 1 by the share of its requests
+// not finished: its state at the start of the iteration that needed the
+// slots goes to its hand-over record, and a wider launch continues from
+// there (or starts it over when the record says so).
 template <int NCH, int MODE, bool SIMPLE>
-__device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
+__device__ __forceinline__ int simulate_point(const SimArgs& A, const int pidx,
                                                SlotLds<NCH>& L, QEntry* Q,
                                                const int lane, const LaneRoof& roofc) {
   const DevPoint P = A.points[pidx];
@@ -1843,7 +1845,7 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
     }
     // the iterations simulated here, up to the hand-over state
     atomicAdd(A.work, (unsigned long long)(lane == 0 ? n_iters - n_it0 : 0));
-    return false;
+    return (int)(((int64_t)(N - n_done) * kHandBuckets) / (N + 1));
   }
 
   // ---- a point stopped early (iteration cap, watchdog): the requests it
@@ -1902,7 +1904,7 @@ __device__ __forceinline__ bool simulate_point(const SimArgs& A, const int pidx,
   // the iterations this launch simulated to completion (every lane adds, lane
   // 0 the count: no lane-dependent branch)
   atomicAdd(A.work, (unsigned long long)(lane == 0 ? n_iters - n_it0 : 0));
-  return true;
+  return -1;
 }
 
 // Persistent grid: each wave64 workgroup takes the next point from a ticket
@@ -1926,10 +1928,15 @@ __global__ __launch_bounds__(64, NCH == 4 ? 4 : (SIMPLE ? 6 : 5)) void sim_kerne
   roofc.is_attp = lane == 1;
   roofc.is_attd = lane == 2;
   roofc.is_lm = lane == 6;
-  // the points of this launch: a host-side count, or the count of points a
-  // narrow launch handed over (written before this launch started)
-  const int n_order =
-      A.n_dev ? __builtin_amdgcn_readfirstlane((int)*A.n_dev) : A.n_order;
+  // the points of this launch: a host-side count, or the points a narrow
+  // launch handed over (its bucket counts were written before this launch
+  // started), taken bucket by bucket, the most remaining work first
+  int n_order = A.n_order;
+  if (A.n_dev != nullptr) {
+    n_order = 0;
+    for (int k = 0; k < kHandBuckets; ++k)
+      n_order += __builtin_amdgcn_readfirstlane((int)A.n_dev[k]);
+  }
   // A workgroup never needs more tickets than there are points.
   for (int taken = 0; taken <= n_order; ++taken) {
     // All lanes take part (lane 0 adds 1, the others 0) so the ticket is
@@ -1937,13 +1944,26 @@ __global__ __launch_bounds__(64, NCH == 4 ? 4 : (SIMPLE ? 6 : 5)) void sim_kerne
     const unsigned old = atomicAdd(A.counter, lane == 0 ? 1u : 0u);
     const int tk = __builtin_amdgcn_readfirstlane((int)old);
     if (tk >= n_order) break;
-    const int pidx = A.order[tk];
-    if (!simulate_point<NCH, MODE, SIMPLE>(A, pidx, L, Q, lane, roofc)) {
-      // hand the point to the launch with twice the slots (every lane
-      // stores the same index)
+    int pos = tk;
+    if (A.n_dev != nullptr) {  // bucket kHandBuckets - 1 first
+      int k = kHandBuckets - 1;
+      for (; k > 0; --k) {
+        const int c = __builtin_amdgcn_readfirstlane((int)A.n_dev[k]);
+        if (pos < c) break;
+        pos -= c;
+      }
+      pos += k * A.hand_cap_in;
+    }
+    const int pidx = A.order[pos];
+    const int bucket = simulate_point<NCH, MODE, SIMPLE>(A, pidx, L, Q, lane, roofc);
+    if (bucket >= 0) {
+      // hand the point to the launch with twice the slots, in its bucket's
+      // list (every lane stores the same index)
       const int wc = NCH == 1 ? 0 : 1;
-      const unsigned slot = atomicAdd(A.handed_n + wc, lane == 0 ? 1u : 0u);
-      A.handed[A.handed_off[wc] + __builtin_amdgcn_readfirstlane((int)slot)] = pidx;
+      const unsigned slot = atomicAdd(A.handed_n + wc * kHandBuckets + bucket,
+                                      lane == 0 ? 1u : 0u);
+      A.handed[A.handed_off[wc] + bucket * A.hand_cap[wc] +
+               __builtin_amdgcn_readfirstlane((int)slot)] = pidx;
     }
   }
 }

@@ -108,6 +108,7 @@ struct LaneCoef {
 };
 
 constexpr int kQueueCap = 256;  // >= max_batch: queue + running never exceed max_batch
+constexpr int kHandBuckets = 8;  // hand-over lists, by a point's remaining share of requests
 
 // Hand-over state: a point's simulation at the start of the general-path
 // iteration whose admissions needed more running slots than its launch has.
@@ -150,13 +151,16 @@ struct SimArgs {
   unsigned long long* work;    // simulated iterations of the points completed by this launch
   // A narrow launch also takes points wider than its slots and hands those
   // that need more running slots to the launch with twice the slots: handed
-  // (the list the 64-slot launch fills at handed_off[0], the 128-slot one at
-  // handed_off[1]) and handed_n (their counts).  A launch taking over handed
-  // points reads its count at n_dev (nullptr otherwise).
+  // (the lists the 64-slot launch fills at handed_off[0], the 128-slot one at
+  // handed_off[1], one per remaining-work bucket, hand_cap entries apart) and
+  // handed_n (their counts).  A launch taking over handed points reads its
+  // bucket counts at n_dev (nullptr otherwise).
   int32_t* handed;
   int32_t handed_off[2];
-  unsigned int* handed_n;
-  const unsigned int* n_dev;
+  int32_t hand_cap[2];         // entries per bucket list of each hand-over level
+  int32_t hand_cap_in;         // ... of the lists this launch takes its points from
+  unsigned int* handed_n;      // [2][kHandBuckets] counts
+  const unsigned int* n_dev;   // kHandBuckets counts of this launch's points
   // hand-over states (kResumeBytes per DevPoint::resume slot), nullptr when
   // no launch hands points on
   unsigned char* resume;
