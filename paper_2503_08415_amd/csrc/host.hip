@@ -657,7 +657,12 @@ int make_plan(const ts_model* model, const ts_trace* traces, int32_t n_traces,
     per_cu = std::max(per_cu, 1);
     P->grid[l] = std::min(P->class_n[l], n_cu * per_cu);
   }
-  P->stats_grid = std::max(1, std::min(count, n_cu * 8));
+  {
+    int per_cu = 0;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, stats_kernel, 256, 0);
+    if (e != hipSuccess) { return device_error(e, "occupancy query"); }
+    P->stats_grid = std::max(1, std::min(count, n_cu * std::max(per_cu, 1)));
+  }
 
   std::vector<TraceRec>& recs = P->recs;
   recs.assign((size_t)std::max<int64_t>(total_recs + extra_recs, 1), TraceRec{});

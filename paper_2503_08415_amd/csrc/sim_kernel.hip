@@ -2093,26 +2093,94 @@ __device__ void locate_ranks(const int* hist, const int* ks, int* wsum_sh, int* 
   __syncthreads();
 }
 
+// The k-th smallest (0-based) of a rank's cnt <= kCandCap candidates c[] in
+// LDS, found by one wave: the candidates stay in registers, and each pass
+// takes the next 8-bit digit from bit `shift` down by a 256-bin histogram
+// of the candidates still in the race (the wave's own bins wh[]) and a wave
+// prefix sum over the bins.  `known` holds the bits every candidate shares
+// (the bucket's leading bits); shift is the top unknown bit's digit.
+__device__ int64_t wave_select(const int64_t* c, int cnt, int k, uint64_t known, int shift,
+                               int* wh) {
+  constexpr int kPer = kCandCap / 64;
+  const int lane = threadIdx.x & 63;
+  uint64_t v[kPer];
+  uint32_t live = 0;
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {
+    const int i = u * 64 + lane;
+    v[u] = i < cnt ? (uint64_t)c[i] : 0ull;
+    live |= i < cnt ? 1u << u : 0u;
+  }
+  uint64_t prefix = known;
+  for (; shift >= 0; shift -= 8) {
+    *reinterpret_cast<int4*>(&wh[lane * 4]) = make_int4(0, 0, 0, 0);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int u = 0; u < kPer; ++u)
+      if ((live >> u) & 1u) atomicAdd(&wh[(int)((v[u] >> shift) & 255u)], 1);
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "workgroup");
+    __builtin_amdgcn_wave_barrier();
+    const int4 h = *reinterpret_cast<const int4*>(&wh[lane * 4]);
+    const int sum = (h.x + h.y) + (h.z + h.w);
+    const int inc = scan_i32(sum);
+    const int before = inc - sum;
+    // the one lane whose four bins hold the k-th live candidate
+    const uint64_t m = ballot(k >= before && k < inc);
+    const int L = m != 0 ? (int)__builtin_ctzll(m) : 0;
+    int kk = k - before, d = lane * 4;
+    if (kk >= h.x) {
+      kk -= h.x;
+      ++d;
+      if (kk >= h.y) {
+        kk -= h.y;
+        ++d;
+        if (kk >= h.z) {
+          kk -= h.z;
+          ++d;
+        }
+      }
+    }
+    d = rdl(d, L);
+    k = rdl(kk, L);
+    prefix |= (uint64_t)d << shift;
+#pragma unroll
+    for (int u = 0; u < kPer; ++u)
+      if ((int)((v[u] >> shift) & 255u) != d) live &= ~(1u << u);
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "workgroup");
+    __builtin_amdgcn_wave_barrier();
+  }
+  return (int64_t)prefix;
+}
+
 // The point's request statistics from its request records, one 256-thread
 // workgroup per point: latency sums (TTFT = first token - arrival, E2E =
 // finish - arrival, TPOT numerator = finish - first token), the largest E2E,
 // the last finish, the SLO counts (Sec. IV-B), the digest over finished and
 // rejected records, then nearest-rank percentiles of the finished requests'
-// latencies.  The record pass also builds a bucket histogram of each
-// latency and copies the latencies densely to HBM; the buckets of the ranks
-// are located, one pass over the dense copy gathers each rank's bucket into
-// LDS, and a radix select there finds the exact value (a bucket too full for
-// LDS is selected by radix passes over the dense copy instead).  With
-// pad_pending (per-request output) the row's entries past the trace also
-// get "pending" records.
-__global__ __launch_bounds__(256) void stats_kernel(ts_req_result* rec, const TraceRec* recs,
+// latencies.  The record pass (two records per thread in flight) also
+// builds a bucket histogram of each latency and copies the latencies
+// densely to HBM; the buckets of the ranks are located, one pass over the
+// dense copy gathers each rank's bucket into LDS (over the histograms,
+// which are done by then), and one wave per rank selects the exact value
+// there (a bucket too full for LDS is selected by the whole workgroup in
+// radix passes over the dense copy instead).  With pad_pending (per-request
+// output) the row's entries past the trace also get "pending" records.
+constexpr int kStatsBatch = 2;  // records per thread in flight (5 waves per SIMD: 96 VGPRs)
+constexpr int kStatsUnion =
+    (2 * kBuckets * 4 > 5 * kCandCap * 8) ? 2 * kBuckets * 4 : 5 * kCandCap * 8;
+__global__ __launch_bounds__(256, 5) void stats_kernel(ts_req_result* rec, const TraceRec* recs,
                                                     const PointInfo* pinfo,
                                                     ts_point_result* res, int64_t* e2e,
                                                     int64_t* ttft, int max_n, int n_points,
                                                     int64_t slo_ttft_ns, int64_t slo_tpot_ns,
                                                     int pad_pending) {
-  __shared__ int hist[2 * kBuckets];           // E2E buckets, then TTFT buckets
-  __shared__ int64_t cand[5][kCandCap];        // candidates of the 5 ranks
+  // the latency histograms (E2E buckets, then TTFT buckets) until the ranks'
+  // buckets are located, then the 5 ranks' candidates
+  __shared__ __attribute__((aligned(16))) unsigned char ubuf[kStatsUnion];
+  int* const hist = reinterpret_cast<int*>(ubuf);
+  int64_t(*const cand)[kCandCap] = reinterpret_cast<int64_t(*)[kCandCap]>(ubuf);
+  __shared__ __attribute__((aligned(16))) int whist[4][256];  // select bins, per wave
   __shared__ int sh[16];
   __shared__ int rb[5], rk[5];                 // rank bucket, rank within it
   __shared__ int ks[5];                        // the ranks (0-based)
@@ -2121,7 +2189,7 @@ __global__ __launch_bounds__(256) void stats_kernel(ts_req_result* rec, const Tr
   __shared__ unsigned long long acc_sum[4];  // TTFT, E2E, TPOT numerator, digest
   __shared__ long long acc_max[2];           // largest E2E, last finish
   __shared__ unsigned int acc_cnt[3];        // finished (dense index), slo_ok, slo_tpot_ok
-  const int tid = threadIdx.x, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   for (int p = blockIdx.x; p < n_points; p += gridDim.x) {
     const PointInfo pi = pinfo[p];
     ts_req_result* R = rec + (size_t)p * (size_t)max_n;
@@ -2136,40 +2204,55 @@ __global__ __launch_bounds__(256) void stats_kernel(ts_req_result* rec, const Tr
     uint64_t s_tt = 0, s_ee = 0, s_tp = 0, dig = 0;
     int64_t mx = -1, lf = -1;
     unsigned int n_slo = 0, n_slo_tpot = 0;
-    for (int g0 = 0; g0 < pi.n; g0 += 256) {  // whole waves, so the ballots see every lane
-      const int g = g0 + tid;
-      ts_req_result r;
-      r.status = TS_REQ_PENDING;
-      if (g < pi.n) r = R[g];
-      const bool done = r.status == TS_REQ_DONE;
-      int64_t tt = 0, ee = 0;
-      if (done) {
-        const int64_t arr = recs[pi.trace_off + g].arrival_ns;
-        tt = r.first_token_ns - arr;
-        ee = r.finish_ns - arr;
-        s_tt += (uint64_t)tt;
-        s_ee += (uint64_t)ee;
-        s_tp += (uint64_t)(r.finish_ns - r.first_token_ns);
-        mx = ee > mx ? ee : mx;
-        lf = r.finish_ns > lf ? r.finish_ns : lf;
-        n_slo += (tt <= slo_ttft_ns && r.max_gap_ns <= slo_tpot_ns) ? 1u : 0u;
-        n_slo_tpot += r.max_gap_ns <= slo_tpot_ns ? 1u : 0u;
-        atomicAdd(&hist[lat_bucket((uint64_t)ee)], 1);
-        atomicAdd(&hist[kBuckets + lat_bucket((uint64_t)tt)], 1);
+    for (int g0 = 0; g0 < pi.n; g0 += 256 * kStatsBatch) {
+      // whole waves, so the ballots see every lane
+      ts_req_result rr[kStatsBatch];
+      int64_t arr[kStatsBatch];
+#pragma unroll
+      for (int u = 0; u < kStatsBatch; ++u) {
+        const int g = g0 + u * 256 + tid;
+        if (g < pi.n) {
+          rr[u] = R[g];
+          arr[u] = recs[pi.trace_off + g].arrival_ns;
+        } else {
+          rr[u].admit_ns = -1; rr[u].first_token_ns = -1; rr[u].finish_ns = -1;
+          rr[u].max_gap_ns = 0; rr[u].n_preempt = 0; rr[u].status = TS_REQ_PENDING;
+          arr[u] = 0;
+        }
       }
-      // dense positions: one counter update per wave
-      const uint64_t dm = ballot(done);
-      unsigned int base = 0;
-      if (lane == 0 && dm != 0) base = atomicAdd(&acc_cnt[0], (unsigned int)popc(dm));
-      base = (unsigned int)__builtin_amdgcn_readfirstlane((int)base);
-      if (done) {
-        const unsigned int pos = base + (unsigned int)rank_below(dm);
-        ve[pos] = ee;
-        vt[pos] = tt;
+#pragma unroll
+      for (int u = 0; u < kStatsBatch; ++u) {
+        const ts_req_result& r = rr[u];
+        const int g = g0 + u * 256 + tid;
+        const bool done = r.status == TS_REQ_DONE;
+        int64_t tt = 0, ee = 0;
+        if (done) {
+          tt = r.first_token_ns - arr[u];
+          ee = r.finish_ns - arr[u];
+          s_tt += (uint64_t)tt;
+          s_ee += (uint64_t)ee;
+          s_tp += (uint64_t)(r.finish_ns - r.first_token_ns);
+          mx = ee > mx ? ee : mx;
+          lf = r.finish_ns > lf ? r.finish_ns : lf;
+          n_slo += (tt <= slo_ttft_ns && r.max_gap_ns <= slo_tpot_ns) ? 1u : 0u;
+          n_slo_tpot += r.max_gap_ns <= slo_tpot_ns ? 1u : 0u;
+          atomicAdd(&hist[lat_bucket((uint64_t)ee)], 1);
+          atomicAdd(&hist[kBuckets + lat_bucket((uint64_t)tt)], 1);
+        }
+        // dense positions: one counter update per wave
+        const uint64_t dm = ballot(done);
+        unsigned int base = 0;
+        if (lane == 0 && dm != 0) base = atomicAdd(&acc_cnt[0], (unsigned int)popc(dm));
+        base = (unsigned int)__builtin_amdgcn_readfirstlane((int)base);
+        if (done) {
+          const unsigned int pos = base + (unsigned int)rank_below(dm);
+          ve[pos] = ee;
+          vt[pos] = tt;
+        }
+        if (done || r.status == TS_REQ_REJECTED)
+          dig += record_hash(g, r.admit_ns, r.first_token_ns, r.finish_ns, r.max_gap_ns,
+                             r.n_preempt, r.status);
       }
-      if (done || r.status == TS_REQ_REJECTED)
-        dig += record_hash(g, r.admit_ns, r.first_token_ns, r.finish_ns, r.max_gap_ns,
-                           r.n_preempt, r.status);
     }
     if (pad_pending) {
       ts_req_result o;
@@ -2195,18 +2278,48 @@ __global__ __launch_bounds__(256) void stats_kernel(ts_req_result* rec, const Tr
       __syncthreads();
       locate_ranks<3>(hist, ks, sh, rb, rk);
       locate_ranks<2>(hist + kBuckets, ks + 3, sh, rb + 3, rk + 3);
+      // (the histograms are dead from here: their LDS takes the candidates)
       // gather each rank's bucket
-      for (int i = tid; i < n; i += 256) {
-        const int64_t e = ve[i], tv = vt[i];
-        const int be = lat_bucket((uint64_t)e), bt = lat_bucket((uint64_t)tv);
+      for (int i0 = 0; i0 < n; i0 += 256 * kStatsBatch) {
+        int64_t ev[kStatsBatch], tv[kStatsBatch];
 #pragma unroll
-        for (int r = 0; r < 5; ++r) {
-          const int64_t v = r < 3 ? e : tv;
-          if ((r < 3 ? be : bt) == rb[r]) {
-            const unsigned int c = atomicAdd(&ccount[r], 1u);
-            if (c < (unsigned int)kCandCap) cand[r][c] = v;
+        for (int u = 0; u < kStatsBatch; ++u) {
+          const int i = i0 + u * 256 + tid;
+          ev[u] = i < n ? ve[i] : -1;
+          tv[u] = i < n ? vt[i] : -1;
+        }
+#pragma unroll
+        for (int u = 0; u < kStatsBatch; ++u) {
+          if (ev[u] < 0) continue;  // past the count (latencies are >= 0)
+          const int be = lat_bucket((uint64_t)ev[u]), bt = lat_bucket((uint64_t)tv[u]);
+#pragma unroll
+          for (int r = 0; r < 5; ++r) {
+            if ((r < 3 ? be : bt) == rb[r]) {
+              const unsigned int c = atomicAdd(&ccount[r], 1u);
+              if (c < (unsigned int)kCandCap) cand[r][c] = r < 3 ? ev[u] : tv[u];
+            }
           }
         }
+      }
+      __syncthreads();
+      // one wave per rank whose bucket fits in LDS (wave 0 also takes rank 4)
+      for (int r = wv; r < 5; r += 4) {
+        const int cnt = (int)ccount[r];
+        const int b = rb[r];
+        if (b < kSub) {  // a bucket of one value
+          if (lane == 0) r5[r] = b;
+          continue;
+        }
+        if (cnt > kCandCap) continue;
+        // values of bit length bl whose leading 1 + kSubBits bits are the
+        // bucket's: bl - 1 - kSubBits bits below them are unknown
+        const int bl = b >> kSubBits;
+        const int unk = bl - 1 - kSubBits;
+        const uint64_t known = (uint64_t)(kSub | (b & (kSub - 1))) << unk;
+        const int64_t v = unk > 0 ? wave_select(cand[r], cnt, rk[r], known, ((unk - 1) / 8) * 8,
+                                                whist[wv])
+                                  : (int64_t)known;
+        if (lane == 0) r5[r] = v;
       }
       __syncthreads();
       // every latency lies in [0, max_e2e] (a first token never comes after
@@ -2216,22 +2329,12 @@ __global__ __launch_bounds__(256) void stats_kernel(ts_req_result* rec, const Tr
       const int top_all = ((bits - 1) / 8) * 8;
 #pragma unroll 1
       for (int r = 0; r < 5; ++r) {
-        const int cnt = (int)ccount[r];
-        const int b = rb[r];
-        if (b < kSub) {  // a bucket of one value
-          if (tid == 0) r5[r] = b;
-          continue;
-        }
-        // the bucket's values are below 2^(b / kSub)
-        const int top = ((b / kSub - 1) / 8) * 8;
-        if (tid == 0) sh[2] = cnt <= kCandCap ? rk[r] : ks[r];
+        if (rb[r] < kSub || (int)ccount[r] <= kCandCap) continue;
+        if (tid == 0) sh[2] = ks[r];
         __syncthreads();
-        const int kk = cnt <= kCandCap ? rk[r] : ks[r];
+        const int kk = ks[r];
         int64_t v;
-        if (cnt <= kCandCap)
-          select_ranks<1>(cand[r], cnt, &kk, top, &v, hist, sh);
-        else
-          select_ranks<1>(r < 3 ? ve : vt, n, &kk, top_all, &v, hist, sh);
+        select_ranks<1>(r < 3 ? ve : vt, n, &kk, top_all, &v, &whist[0][0], sh);
         if (tid == 0) r5[r] = v;
       }
     }
