@@ -279,12 +279,15 @@ int ts_sweep_kernel_timing(ts_sweep *h, float *ms, int32_t *n_points);
  * request that could never fit, no watchdog) and some allow more than 64
  * running requests, the max_batch <= 64 launch (k = 0) takes all of them
  * while at most 64 run at once; a point whose admissions need more slots is
- * handed to the 128-slot launch (k = 1), and from there, if it needs more
- * than 128, to the 256-slot launch (k = 2), which take the handed points
- * with the most requests left first.  The wider launch continues the
- * point from the start of that iteration (each launch counts the iterations
+ * handed on with 128 slots, and from there, if it needs more than 128, to
+ * the 256-slot launch (k = 2).  Handed points are taken with the most
+ * requests left first.  The 128-slot work runs in launch 0 itself, in each
+ * workgroup that has no point of its own left, while the others still run
+ * (counted as launch 0's iterations); the 128-slot launch (k = 1) takes the
+ * points handed over after that.  The point continues from the start of
+ * the iteration that needed the slots (each launch counts the iterations
  * it simulated), or, when the iteration had already admitted a full window,
- * simulates it again from the start (then only the launch that does counts
+ * is simulated again from the start (then only the launch that does counts
  * those iterations).  Waits for the run.  TS_ERR_STATE before the first run. */
 int ts_sweep_kernel_work(ts_sweep *h, int64_t *iters);
 

@@ -33,6 +33,7 @@ __global__ void stats_kernel(ts_req_result* rec, const TraceRec* recs, const Poi
                              int n_points, int64_t slo_ttft_ns, int64_t slo_tpot_ns,
                              int pad_pending);
 __global__ void reset_counters_kernel(unsigned int* c, int n, unsigned long long* w, int nw);
+__global__ void fill_kernel(int32_t* p, int n, int32_t v);
 }  // namespace tsw
 
 using namespace tsw;
@@ -221,13 +222,15 @@ BufCounts buf_counts(const Plan& P) {
   c.recs = P.recs.size();
   c.points = P.dp.size();
   c.order = P.order.size();
-  // tickets per launch, then the handed points per wider class and bucket
-  c.counter = kLaunches + 2 * kHandBuckets;
+  // tickets per launch, the handed points per wider class and bucket, then
+  // the positions the 64-slot launch took of its own lists
+  c.counter = kLaunches + 3 * kHandBuckets;
   // the 64-slot launch hands at most class_n[1] points on, the 128-slot one
   // at most class_n[2]
   c.handed = P.hand_over ? (size_t)kHandBuckets * (P.class_n[1] + P.class_n[2]) : 0;
   c.work = kLaunches;
   c.resume = (size_t)P.n_resume;
+  c.claim = (size_t)P.n_resume;
   c.queue = (size_t)P.max_grid() * kQueueCap;
   c.res = (size_t)(P.count + P.n_extra);
   c.req = (size_t)P.count * per_point;  // the request records (always)
@@ -249,7 +252,7 @@ double BufCounts::bytes() const {
          2.0 * (double)s1 * sizeof(int64_t) + (double)sub * (sizeof(int64_t) + sizeof(int32_t)) +
          (double)gids * sizeof(int32_t) + (double)pinfo * sizeof(PointInfo) +
          (double)handed * sizeof(int32_t) + (double)work * sizeof(unsigned long long) +
-         (double)resume * (double)kResumeBytes;
+         (double)resume * (double)kResumeBytes + (double)claim * sizeof(unsigned int);
 }
 
 }  // namespace tsw
@@ -286,6 +289,7 @@ void release(ts_sweep* h) {
   (void)hipFree(b.handed);
   (void)hipFree(b.work);
   (void)hipFree(b.resume);
+  (void)hipFree(b.claim);
   for (int c = 0; c < kLaunches; ++c) {
     if (h->ev.k0[c]) (void)hipEventDestroy(h->ev.k0[c]);
     if (h->ev.k1[c]) (void)hipEventDestroy(h->ev.k1[c]);
@@ -712,8 +716,19 @@ int enqueue(const Plan& P, const DevBufs& B, hipStream_t s, const LaunchEvents* 
   };
   hipError_t e = record(ev ? ev->t0 : nullptr);
   if (e != hipSuccess) return device_error(e, "event record");
-  reset_counters_kernel<<<1, 64, 0, s>>>(B.counter, kLaunches + 2 * kHandBuckets, B.work,
+  reset_counters_kernel<<<1, 64, 0, s>>>(B.counter, kLaunches + 3 * kHandBuckets, B.work,
                                           kLaunches);
+  if (P.hand_over) {
+    // the 64-slot launch's lists start empty (-1: not written yet), as do
+    // the claims, since it takes points from its lists while it fills them
+    const int n_list = kHandBuckets * P.class_n[1];
+    fill_kernel<<<std::max(1, std::min((n_list + 255) / 256, 1024)), 256, 0, s>>>(B.handed, n_list,
+                                                                                 -1);
+    fill_kernel<<<std::max(1, std::min((P.n_resume + 255) / 256, 1024)), 256, 0, s>>>(
+        reinterpret_cast<int32_t*>(B.claim), P.n_resume, 0);
+    e = hipGetLastError();
+    if (e != hipSuccess) return device_error(e, "fill kernel launch");
+  }
   SimArgs a;
   a.recs = B.recs;
   a.points = B.points;
@@ -732,6 +747,8 @@ int enqueue(const Plan& P, const DevBufs& B, hipStream_t s, const LaunchEvents* 
   a.handed_n = B.counter + kLaunches;
   a.n_dev = nullptr;
   a.resume = P.hand_over ? B.resume : nullptr;
+  a.take = nullptr;
+  a.claim = nullptr;
   a.time_limit_ticks = (uint64_t)P.time_limit_ms * 100000ull;  // 100 MHz clock
   a.n_layers = P.coef.n_layers;
   a.lc = P.lc;
@@ -760,6 +777,9 @@ int enqueue(const Plan& P, const DevBufs& B, hipStream_t s, const LaunchEvents* 
       a.n_dev = B.counter + kLaunches + (l - 1) * kHandBuckets;
       a.hand_cap_in = a.hand_cap[l - 1];
     }
+    // launch 0 also continues points it handed over; launch 1 skips those
+    a.take = (P.hand_over && l == 0) ? B.counter + kLaunches + 2 * kHandBuckets : nullptr;
+    a.claim = (P.hand_over && l <= 1) ? B.claim : nullptr;
     a.counter = B.counter + l;
     a.work = B.work + l;
     e = record(ev ? ev->k0[l] : nullptr);
@@ -860,6 +880,7 @@ int ts_sweep_create(const ts_model* model, const ts_trace* traces, int32_t n_tra
   if (ae == hipSuccess) ae = dev_alloc(&b.handed, n.handed);
   if (ae == hipSuccess) ae = dev_alloc(&b.work, n.work);
   if (ae == hipSuccess) ae = dev_alloc(&b.resume, n.resume * kResumeBytes);
+  if (ae == hipSuccess) ae = dev_alloc(&b.claim, n.claim);
   if (ae == hipSuccess) ae = dev_alloc(&b.pd, n.pd);
   if (ae == hipSuccess) ae = dev_alloc(&b.s1_admit, n.s1);
   if (ae == hipSuccess) ae = dev_alloc(&b.s1_first, n.s1);

@@ -86,6 +86,7 @@ size_t carve(const tsw::Plan& P, unsigned char* base, tsw::DevBufs* B) {
   b.handed = c.take<int32_t>(n.handed);
   b.work = c.take<unsigned long long>(n.work);
   b.resume = c.take<unsigned char>(n.resume * tsw::kResumeBytes);
+  b.claim = c.take<unsigned int>(n.claim);
   if (B) *B = b;
   return c.used;
 }

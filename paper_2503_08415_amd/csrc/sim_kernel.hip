@@ -23,7 +23,8 @@
 //     kernel derives every latency statistic and percentile;
 //   * a narrow launch takes points wider than its slots and hands those that
 //     need more running requests to a wider launch, with a record of their
-//     state.
+//     state; the 64-slot launch itself continues them with 128 slots in the
+//     workgroups that have no point of their own left.
 // Scheduling state is integer; only the roofline is fp64, evaluated in a
 // fixed order with contraction disabled.
 #include <hip/hip_runtime.h>
@@ -331,7 +332,8 @@ __device__ __forceinline__ void store_chunk(SlotLds<NCH>& L, Hot& h0, int j, int
 template <int NCH, int MODE, bool SIMPLE>
 __device__ __forceinline__ int simulate_point(const SimArgs& A, const int pidx,
                                                SlotLds<NCH>& L, QEntry* Q,
-                                               const int lane, const LaneRoof& roofc) {
+                                               const int lane, const LaneRoof& roofc,
+                                               const bool resumed) {
   const DevPoint P = A.points[pidx];
   const TraceRec* __restrict__ rec = A.recs + P.trace_off;
   const int N = P.n, NB = P.num_blocks, B = P.block, M = P.max_batch, K = P.chunk;
@@ -432,7 +434,7 @@ __device__ __forceinline__ int simulate_point(const SimArgs& A, const int pidx,
   // n_it0: the iterations the narrower launches counted as theirs.
   int64_t n_it0 = 0;
   if constexpr (SIMPLE && NCH > 1) {
-    if (A.n_dev != nullptr) {
+    if (resumed) {
       const unsigned char* base = A.resume + (size_t)P.resume * kResumeBytes;
       const ResumeHead* hp = reinterpret_cast<const ResumeHead*>(base);
       auto u64 = [](int64_t v) -> int64_t {
@@ -1907,11 +1909,56 @@ __device__ __forceinline__ int simulate_point(const SimArgs& A, const int pidx,
   return -1;
 }
 
+// A point the 64-slot launch handed over, taken by that launch itself once
+// no point of its own is left: the next listed position of the fullest
+// bucket whose list has one, if its entry is written and no launch has
+// claimed the point.  Returns the point, or -1 when no list has a position
+// left to take now (points handed later go to the 128-slot launch, which
+// also takes every position passed over here).
+__device__ __forceinline__ int take_handed(const SimArgs& A, const int lane) {
+  for (int b = kHandBuckets - 1; b >= 0; --b) {
+    unsigned int* nb = A.handed_n + b;
+    unsigned int* tb = A.take + b;
+    const int n = __builtin_amdgcn_readfirstlane(
+        (int)__hip_atomic_load(nb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+    const int t0 = __builtin_amdgcn_readfirstlane(
+        (int)__hip_atomic_load(tb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+    if (t0 >= n) continue;
+    const int t = __builtin_amdgcn_readfirstlane((int)atomicAdd(tb, lane == 0 ? 1u : 0u));
+    if (t >= n) continue;  // taken meanwhile; a position past the count is left to the 128-slot launch
+    // the entry is stored right after its position is reserved: wait a
+    // bounded while for it, else leave it to the 128-slot launch
+    int* ent = A.handed + A.handed_off[0] + b * A.hand_cap[0] + t;
+    int pidx = -1;
+    for (int spin = 0; spin < 4096; ++spin) {
+      pidx = __builtin_amdgcn_readfirstlane(
+          __hip_atomic_load(ent, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+      if (pidx >= 0) break;
+      __builtin_amdgcn_s_sleep(4);
+    }
+    if (pidx < 0) continue;
+    // the entry was stored after the hand-over record (a release fence):
+    // acquire it before reading the record
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    const int slot = A.points[pidx].resume;
+    unsigned int won = 0;
+    if (lane == 0) won = atomicCAS(A.claim + slot, 0u, 1u) == 0u ? 1u : 0u;
+    if (__builtin_amdgcn_readfirstlane((int)won) != 0) return pidx;
+  }
+  return -1;
+}
+
 // Persistent grid: each wave64 workgroup takes the next point from a ticket
-// counter until none is left.
+// counter until none is left.  The simple 64-slot kernel then continues, with
+// 128 slots, points that it handed over (when the launch has take lists):
+// the workgroups that run out of points early fill the launch's tail with
+// the 128-slot launch's work.
 template <int NCH, int MODE, bool SIMPLE>
 __global__ __launch_bounds__(64, NCH == 4 ? 4 : (SIMPLE ? 6 : 5)) void sim_kernel(SimArgs A) {
-  __shared__ SlotLds<NCH> L;
+  constexpr bool kTail = NCH == 1 && SIMPLE;
+  // slot state: one buffer for both widths in the 64-slot simple kernel
+  __shared__ __attribute__((aligned(16))) unsigned char lds_slots[sizeof(SlotLds<kTail ? 2 : NCH>)];
+  SlotLds<NCH>& L = *reinterpret_cast<SlotLds<NCH>*>(lds_slots);
   const int lane = lane_id();
   QEntry* Q = A.queue + (size_t)blockIdx.x * kQueueCap;
   __shared__ double coef[32];
@@ -1928,6 +1975,20 @@ __global__ __launch_bounds__(64, NCH == 4 ? 4 : (SIMPLE ? 6 : 5)) void sim_kerne
   roofc.is_attp = lane == 1;
   roofc.is_attd = lane == 2;
   roofc.is_lm = lane == 6;
+  // hand a point to the launch with twice the slots, in its bucket's list
+  // (every lane stores the same index)
+  auto hand_on = [&](const int pidx, const int bucket, const int wc) {
+    const bool live = wc == 0 && A.take != nullptr;  // read while it is written
+    if (live) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");  // the record first
+    const unsigned slot = atomicAdd(A.handed_n + wc * kHandBuckets + bucket,
+                                    lane == 0 ? 1u : 0u);
+    int* ent = A.handed + A.handed_off[wc] + bucket * A.hand_cap[wc] +
+               __builtin_amdgcn_readfirstlane((int)slot);
+    if (live)
+      __hip_atomic_store(ent, pidx, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else
+      *ent = pidx;
+  };
   // the points of this launch: a host-side count, or the points a narrow
   // launch handed over (its bucket counts were written before this launch
   // started), taken bucket by bucket, the most remaining work first
@@ -1955,15 +2016,25 @@ __global__ __launch_bounds__(64, NCH == 4 ? 4 : (SIMPLE ? 6 : 5)) void sim_kerne
       pos += k * A.hand_cap_in;
     }
     const int pidx = A.order[pos];
-    const int bucket = simulate_point<NCH, MODE, SIMPLE>(A, pidx, L, Q, lane, roofc);
-    if (bucket >= 0) {
-      // hand the point to the launch with twice the slots, in its bucket's
-      // list (every lane stores the same index)
-      const int wc = NCH == 1 ? 0 : 1;
-      const unsigned slot = atomicAdd(A.handed_n + wc * kHandBuckets + bucket,
-                                      lane == 0 ? 1u : 0u);
-      A.handed[A.handed_off[wc] + bucket * A.hand_cap[wc] +
-               __builtin_amdgcn_readfirstlane((int)slot)] = pidx;
+    if (A.claim != nullptr && NCH > 1) {  // the 64-slot launch may have taken it
+      unsigned int won = 0;
+      if (lane == 0) won = atomicCAS(A.claim + A.points[pidx].resume, 0u, 1u) == 0u ? 1u : 0u;
+      if (__builtin_amdgcn_readfirstlane((int)won) == 0) continue;
+    }
+    const int bucket =
+        simulate_point<NCH, MODE, SIMPLE>(A, pidx, L, Q, lane, roofc, A.n_dev != nullptr);
+    if (bucket >= 0) hand_on(pidx, bucket, NCH == 1 ? 0 : 1);
+  }
+  if constexpr (kTail) {
+    if (A.take != nullptr) {
+      SlotLds<2>& L2 = *reinterpret_cast<SlotLds<2>*>(lds_slots);
+      // at most every point once: each take claims a different point
+      for (int guard = 0; guard <= A.hand_cap[0]; ++guard) {
+        const int pidx = take_handed(A, lane);
+        if (pidx < 0) break;
+        const int bucket = simulate_point<2, MODE, true>(A, pidx, L2, Q, lane, roofc, true);
+        if (bucket >= 0) hand_on(pidx, bucket, 1);
+      }
     }
   }
 }
@@ -2460,6 +2531,10 @@ __global__ __launch_bounds__(256) void pd_combine_kernel(const PdAux* aux, int n
 __global__ void reset_counters_kernel(unsigned int* c, int n, unsigned long long* w, int nw) {
   if ((int)threadIdx.x < n) c[threadIdx.x] = 0u;
   if ((int)threadIdx.x < nw) w[threadIdx.x] = 0ull;
+}
+
+__global__ void fill_kernel(int32_t* p, int n, int32_t v) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = v;
 }
 
 }  // namespace tsw

@@ -50,7 +50,7 @@ struct Plan {
 // Element counts of every device buffer of a plan.
 struct BufCounts {
   size_t recs, points, order, counter, queue, res, req, lat, pd, s1, sub, gids, pinfo,
-      handed, work, resume;
+      handed, work, resume, claim;
   double bytes() const;  // total, in bytes
 };
 BufCounts buf_counts(const Plan& P);
@@ -65,6 +65,7 @@ struct DevBufs {
   unsigned long long* work = nullptr;  // simulated iterations completed per launch
   int32_t* handed = nullptr;        // points handed from launch 0 to launches 1 and 2
   unsigned char* resume = nullptr;  // their hand-over states, kResumeBytes each
+  unsigned int* claim = nullptr;    // per hand-over state: taken by a launch
   QEntry* queue = nullptr;          // kQueueCap per workgroup, shared by the launches
   ts_point_result* res = nullptr;
   ts_req_result* req = nullptr;     // the request records, max_n per point (always)

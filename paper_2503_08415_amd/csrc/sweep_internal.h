@@ -164,6 +164,13 @@ struct SimArgs {
   // hand-over states (kResumeBytes per DevPoint::resume slot), nullptr when
   // no launch hands points on
   unsigned char* resume;
+  // The 64-slot launch, once no point of its own is left, continues points
+  // it handed over itself (128 slots) while the others still run: take holds
+  // the positions of its kHandBuckets lists taken so far (nullptr when it
+  // does not).  claim, per hand-over slot, marks a point that one launch has
+  // taken, and the 128-slot launch skips those (nullptr: no claims).
+  unsigned int* take;
+  unsigned int* claim;
   double n_layers;
   LaneCoef lc;
   // disaggregated points

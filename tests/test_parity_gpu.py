@@ -627,9 +627,11 @@ def test_edge_cases(S, oracle):
 def test_hand_over_to_wider_kernels(S, oracle):
     """Simple one-worker points with room for more than 64 running requests
     first run in the 64-slot kernel; those that need more slots (bursts of
-    300 arrivals) are handed to the 128- or 256-slot kernel and simulated
-    again there.  Every request against the oracle, and the launches'
-    completed iterations add up to the oracle's."""
+    300 arrivals) are handed on with 128 slots (continued by the 64-slot
+    launch itself once none of its own points is left, or else by the
+    128-slot launch) and from there to the 256-slot launch.  Every request
+    against the oracle, and the launches' completed iterations add up to the
+    oracle's."""
     m = W.MODELS["llama2-7b"]
     rng = np.random.default_rng(3)
     burst = {"arrival_ns": np.zeros(300, np.int64),
@@ -661,5 +663,5 @@ def test_hand_over_to_wider_kernels(S, oracle):
     compare_points(out, o_out, "hand-over")
     compare_requests(req, o_req, "hand-over")
     assert per_launch[0] == k  # the 64-slot launch takes every point
-    assert work[1] > 0 and work[2] > 0  # bursts were handed to both wider kernels
+    assert work[2] > 0  # bursts were handed on twice (64 -> 128 -> 256 slots)
     assert sum(work) == int(o_out["n_iters"].sum())
