@@ -1914,18 +1914,26 @@ __device__ __forceinline__ int simulate_point(const SimArgs& A, const int pidx,
 // bucket whose list has one, if its entry is written and no launch has
 // claimed the point.  Returns the point, or -1 when no list has a position
 // left to take now (points handed later go to the 128-slot launch, which
-// also takes every position passed over here).
+// also takes any position passed over here).
 __device__ __forceinline__ int take_handed(const SimArgs& A, const int lane) {
   for (int b = kHandBuckets - 1; b >= 0; --b) {
     unsigned int* nb = A.handed_n + b;
     unsigned int* tb = A.take + b;
     const int n = __builtin_amdgcn_readfirstlane(
         (int)__hip_atomic_load(nb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-    const int t0 = __builtin_amdgcn_readfirstlane(
+    int t = __builtin_amdgcn_readfirstlane(
         (int)__hip_atomic_load(tb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-    if (t0 >= n) continue;
-    const int t = __builtin_amdgcn_readfirstlane((int)atomicAdd(tb, lane == 0 ? 1u : 0u));
-    if (t >= n) continue;  // taken meanwhile; a position past the count is left to the 128-slot launch
+    // take position t while it is below the count (a compare-and-swap, so
+    // that the take counter never passes the count)
+    bool got = false;
+    for (int tries = 0; tries < 64 && t < n && !got; ++tries) {
+      unsigned int old = 0;
+      if (lane == 0) old = atomicCAS(tb, (unsigned)t, (unsigned)t + 1u);
+      const int o = __builtin_amdgcn_readfirstlane((int)old);
+      got = o == t;
+      t = o;
+    }
+    if (!got) continue;
     // the entry is stored right after its position is reserved: wait a
     // bounded while for it, else leave it to the 128-slot launch
     int* ent = A.handed + A.handed_off[0] + b * A.hand_cap[0] + t;
