@@ -94,6 +94,10 @@ extern "C" {
 
 /* ts_options.flags */
 #define TS_F_PER_REQUEST 1u /* also return per-request records */
+/* The 64-slot launch leaves every point it hands over to the 128-slot
+ * launch instead of continuing some itself (see ts_sweep_kernel_work): the
+ * two-launch schedule, for measuring it; results are the same. */
+#define TS_F_NO_TAKEOVER 2u
 
 typedef struct ts_sweep ts_sweep; /* opaque; owns all device memory */
 

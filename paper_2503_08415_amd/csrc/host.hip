@@ -321,7 +321,7 @@ int make_plan(const ts_model* model, const ts_trace* traces, int32_t n_traces,
   int64_t iter_cap = (int64_t)1 << 40, slo_ttft = 15000000000LL, slo_tpot = 300000000LL;
   int64_t time_limit_ms = 0;
   if (opt) {
-    if (opt->flags & ~TS_F_PER_REQUEST) return TS_ERR_ARG;
+    if (opt->flags & ~(TS_F_PER_REQUEST | TS_F_NO_TAKEOVER)) return TS_ERR_ARG;
     flags = opt->flags;
     if (opt->first_point < 0 || opt->n_points < 0) return TS_ERR_ARG;
     first = opt->first_point;
@@ -778,7 +778,9 @@ int enqueue(const Plan& P, const DevBufs& B, hipStream_t s, const LaunchEvents* 
       a.hand_cap_in = a.hand_cap[l - 1];
     }
     // launch 0 also continues points it handed over; launch 1 skips those
-    a.take = (P.hand_over && l == 0) ? B.counter + kLaunches + 2 * kHandBuckets : nullptr;
+    a.take = (P.hand_over && l == 0 && !(P.flags & TS_F_NO_TAKEOVER))
+                 ? B.counter + kLaunches + 2 * kHandBuckets
+                 : nullptr;
     a.claim = (P.hand_over && l <= 1) ? B.claim : nullptr;
     a.counter = B.counter + l;
     a.work = B.work + l;

@@ -21,6 +21,7 @@ TS_OK, TS_ERR_ARG, TS_ERR_UNSUPPORTED, TS_ERR_OOM, TS_ERR_DEVICE, TS_ERR_STATE =
 POINT_OK, POINT_NO_KV, POINT_ITER_LIMIT, POINT_TIME_LIMIT = 0, 1, 2, 3
 REQ_PENDING, REQ_DONE, REQ_REJECTED = 0, 1, 2
 F_PER_REQUEST = 1
+F_NO_TAKEOVER = 2
 POLICY_MIXED, POLICY_PREFILL_FIRST, POLICY_STATIC = 0, 1, 2
 MAX_BATCH = 256
 
@@ -167,7 +168,7 @@ def _traces_array(traces):
 def run_static(model: dict, traces, points: dict, *, per_request: bool = False,
                first_point: int = 0, n_points: int = 0, iter_cap: int = 0,
                slo_ttft_ns: int = 0, slo_tpot_ns: int = 0, point_time_limit_ms: int = 0,
-               stream=None):
+               takeover: bool = True, stream=None):
     """One whole sweep through ``ts_sweep_run_static`` (no device allocation;
     buffers in the library's static scratch).  Returns (points, requests or None)."""
     L = lib()
@@ -180,7 +181,8 @@ def run_static(model: dict, traces, points: dict, *, per_request: bool = False,
     count = (n - int(first_point)) if int(n_points) == 0 else int(n_points)
     count = max(count, 0)
     max_n = max([len(t["arrival_ns"]) for t in traces] + [1])
-    opt = Options(F_PER_REQUEST if per_request else 0, int(first_point), int(n_points), 0,
+    flags = (F_PER_REQUEST if per_request else 0) | (0 if takeover else F_NO_TAKEOVER)
+    opt = Options(flags, int(first_point), int(n_points), 0,
                   int(iter_cap), int(slo_ttft_ns), int(slo_tpot_ns), int(point_time_limit_ms))
     out = np.zeros(max(count, 1), dtype=POINT_DTYPE)
     req = np.zeros((count, max_n), dtype=REQ_DTYPE) if per_request else None
@@ -197,12 +199,14 @@ class Sweep:
 
     def __init__(self, model: dict, traces, points: dict, *, per_request: bool = False,
                  first_point: int = 0, n_points: int = 0, iter_cap: int = 0,
-                 slo_ttft_ns: int = 0, slo_tpot_ns: int = 0, point_time_limit_ms: int = 0):
+                 slo_ttft_ns: int = 0, slo_tpot_ns: int = 0, point_time_limit_ms: int = 0,
+                 takeover: bool = True):
         L = lib()
         self._h = C.c_void_p()
         tr, keep = _traces_array(traces)
         pts, n = points_array(points)
-        opt = Options(F_PER_REQUEST if per_request else 0, int(first_point), int(n_points), 0,
+        flags = (F_PER_REQUEST if per_request else 0) | (0 if takeover else F_NO_TAKEOVER)
+        opt = Options(flags, int(first_point), int(n_points), 0,
                       int(iter_cap), int(slo_ttft_ns), int(slo_tpot_ns),
                       int(point_time_limit_ms))
         _check(L.ts_sweep_create(C.byref(model_struct(model)), tr, len(traces), pts, n,

@@ -157,6 +157,11 @@ def test_invalid_arguments_fail_before_device(L):
     opt = S.Options(4, 0, 0, 0, 0, 0, 0, 0)  # unknown flag
     rc, _ = _create(L, m, traces, pts, opt)
     assert rc == S.TS_ERR_ARG
+    opt = S.Options(S.F_PER_REQUEST | S.F_NO_TAKEOVER, 0, 0, 0, 0, 0, 0, 0)  # the known ones
+    rc, h = _create(L, m, traces, pts, opt)
+    assert rc in (S.TS_OK, S.TS_ERR_DEVICE)  # validation passed (no GPU here)
+    if rc == S.TS_OK:
+        L.ts_sweep_destroy(h)
     opt = S.Options(0, 0, 2, 0, 0, 0, 0, 0)  # sub-range beyond the points
     rc, _ = _create(L, m, traces, pts, opt)
     assert rc == S.TS_ERR_ARG

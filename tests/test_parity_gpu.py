@@ -497,14 +497,16 @@ def test_sweep_subsets_per_request(S, oracle, name, nreq):
     assert len(set(pts["max_batch"].tolist())) > 1 or name == "c4"
 
 
-@pytest.mark.parametrize("seed", [3, 4, 5, 6])
-def test_hand_over_records_under_memory_pressure(S, oracle, seed):
+@pytest.mark.parametrize("seed,takeover", [(3, True), (4, True), (5, True), (6, True),
+                                           (3, False), (4, False)])
+def test_hand_over_records_under_memory_pressure(S, oracle, seed, takeover):
     """Simple points of every width up to 256 slots under bursts of up to
     260 simultaneous arrivals and small KV budgets: points continue in the
     wider launches from their hand-over records with running requests,
     reserved blocks and preempted requests waiting (or start over when a
-    window had already admitted).  Every request against the oracle; the
-    launches' iteration counts add up to the oracle's."""
+    window had already admitted), with and without the 64-slot launch's
+    take-over of its own handed points.  Every request against the oracle;
+    the launches' iteration counts add up to the oracle's."""
     m = {"n_layers": 2, "d_model": 64, "n_heads": 4, "n_kv_heads": 2, "ffn_dim": 128,
          "ffn_gated": 1, "vocab": 100, "w_bytes": 2, "kv_bytes": 2, "weights_in_capacity": 0}
     rng = np.random.default_rng(seed)
@@ -532,7 +534,7 @@ def test_hand_over_records_under_memory_pressure(S, oracle, seed):
     o_all, _ = oracle.run_points(m, traces, pts)
     pts = W.subset_points(pts, np.nonzero(o_all["n_rejected"] == 0)[0])
     o_out, o_req = oracle.run_points(m, traces, pts, per_request=True)
-    sw = S.Sweep(m, traces, pts, per_request=True, iter_cap=cap_from(o_out))
+    sw = S.Sweep(m, traces, pts, per_request=True, iter_cap=cap_from(o_out), takeover=takeover)
     try:
         sw.run()
         out, req = sw.results()
@@ -541,7 +543,9 @@ def test_hand_over_records_under_memory_pressure(S, oracle, seed):
         sw.close()
     compare_points(out, o_out, "hand-over records")
     compare_requests(req, o_req, "hand-over records")
-    assert work[1] > 0 and work[2] > 0
+    assert work[2] > 0
+    if not takeover:
+        assert work[1] > 0
     assert int(o_out["n_preempt"].sum()) > 50
     assert sum(work) == int(o_out["n_iters"].sum())
 
@@ -624,12 +628,14 @@ def test_edge_cases(S, oracle):
     assert (g_cap["status"][[1, 2, 3, 6]] == 2).all()
 
 
-def test_hand_over_to_wider_kernels(S, oracle):
+@pytest.mark.parametrize("takeover", [True, False])
+def test_hand_over_to_wider_kernels(S, oracle, takeover):
     """Simple one-worker points with room for more than 64 running requests
     first run in the 64-slot kernel; those that need more slots (bursts of
     300 arrivals) are handed on with 128 slots (continued by the 64-slot
     launch itself once none of its own points is left, or else by the
-    128-slot launch) and from there to the 256-slot launch.  Every request
+    128-slot launch) and from there to the 256-slot launch; without the
+    take-over the 128-slot launch continues every one.  Every request
     against the oracle, and the launches' completed iterations add up to the
     oracle's."""
     m = W.MODELS["llama2-7b"]
@@ -652,7 +658,7 @@ def test_hand_over_to_wider_kernels(S, oracle):
            "trace_id": np.array([r[2] for r in rows], np.int32)}
     traces = [burst, spread]
     o_out, o_req = oracle.run_points(m, traces, pts, per_request=True)
-    sw = S.Sweep(m, traces, pts, per_request=True, iter_cap=cap_from(o_out))
+    sw = S.Sweep(m, traces, pts, per_request=True, iter_cap=cap_from(o_out), takeover=takeover)
     try:
         sw.run()
         out, req = sw.results()
@@ -664,4 +670,6 @@ def test_hand_over_to_wider_kernels(S, oracle):
     compare_requests(req, o_req, "hand-over")
     assert per_launch[0] == k  # the 64-slot launch takes every point
     assert work[2] > 0  # bursts were handed on twice (64 -> 128 -> 256 slots)
+    if not takeover:
+        assert work[1] > 0  # the 128-slot launch continued them
     assert sum(work) == int(o_out["n_iters"].sum())
