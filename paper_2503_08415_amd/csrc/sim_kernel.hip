@@ -759,8 +759,6 @@ __device__ __forceinline__ int simulate_point(const SimArgs& A, const int pidx,
         }
         int dG = 0, seg0 = 0, q = 0, fin_at = 0, stop = 0, cd_seg = 0;
         bool watch = false;
-        double Fw = 0.0, Bw = 0.0, dF = 0.0, dB = 0.0;
-        double k_t0 = 0.0, k_t3 = 0.0, k_t4 = 0.0, k_t5 = 0.0, k_lm = 0.0;
         const double kT52d = 4503599627370496.0;
         double thr = next < N ? __builtin_fmin((double)rdl64(w_arr, next - wbase), kT52d) : kT52d;
         // the clock (fp64, exact below 2^53), this lane's share of the
@@ -790,27 +788,26 @@ __device__ __forceinline__ int simulate_point(const SimArgs& A, const int pidx,
           cd_seg = cs + nDa * dG;
           q = npf > 0 ? K - nDa : 0;
           const int64_t AP0 = (int64_t)q * ctx_p + ((int64_t)q * (q + 1)) / 2;
+          double Fw, Bw;
           lane_work(roofc, nDa + q, q, AP0, q > 0 ? ctx_p + q : 0, nDa, cd_seg, nDa, &Fw, &Bw);
           const double dX = roofc.is_attp ? (double)((int64_t)q * q)
                                           : (roofc.is_attd ? (double)nDa : 0.0);
           const double dY = roofc.is_attp ? (double)q : (roofc.is_attd ? (double)nDa : 0.0);
-          dF = roofc.f() * dX;
-          dB = roofc.b1() * dY;
-          // the constant operators' times, moved to lane 1 where the layer sum runs
-          const double tl0 = __builtin_fmax(Fw * iF, Bw * iB);
-          k_t0 = dpp_f64<0x111>(tl0);
-          k_t3 = dpp_f64<0x102>(tl0);
-          k_t4 = dpp_f64<0x103>(tl0);
-          k_t5 = dpp_f64<0x104>(tl0);
-          k_lm = dpp_f64<0x105>(tl0);
-          if (lane == 1) {
-            L.segk[0] = Fw; L.segk[1] = Bw; L.segk[2] = dF; L.segk[3] = dB;
-            L.segk[8] = k_t0; L.segk[9] = k_t3; L.segk[10] = k_t4; L.segk[11] = k_t5;
-            L.segk[12] = k_lm;
+          // the segment's constants in LDS, where every iteration reads
+          // them: the attention operators' FLOPs and bytes at the segment
+          // start and their steps per iteration (lanes 1, 2), then the other
+          // operators' times (lanes 0, 3, 4, 5, 6)
+          if (lane == 1 || lane == 2) {
+            double* k = &L.segk[(lane - 1) * 4];
+            k[0] = Fw;
+            k[1] = Bw;
+            k[2] = roofc.f() * dX;
+            k[3] = roofc.b1() * dY;
+          } else if (lane < 7) {
+            L.segk[lane == 0 ? 8 : lane + 6] = __builtin_fmax(Fw * iF, Bw * iB);
           }
-          if (lane == 2) {
-            L.segk[4] = Fw; L.segk[5] = Bw; L.segk[6] = dF; L.segk[7] = dB;
-          }
+          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+          __builtin_amdgcn_wave_barrier();
           stop = stop_hard;
           if (q > 0) {  // the head prefill completes in iteration kc
             // floor(n / q) for 0 <= n < 2^21 and 1 <= q <= 2^20 (a target
@@ -933,9 +930,6 @@ __device__ __forceinline__ int simulate_point(const SimArgs& A, const int pidx,
               freeb -= rdl(T, last);
               t_d = rdl_f64(tend, last);
               it = rdl_f64(itv, last);
-              const double kd = (double)Kb;
-              Fw = Fw + kd * dF;
-              Bw = Bw + kd * dB;
 #pragma unroll
               for (int j = 0; j < NCH; ++j) {
                 if (j < nchd) {
@@ -950,22 +944,26 @@ __device__ __forceinline__ int simulate_point(const SimArgs& A, const int pidx,
             for (int j = 0; j < NCH; ++j)
               if (j < nchd) rr[j] += rr[j] == dG ? B : 0;
             const double used_d = (double)(NB - freeb);
-            // prefill attention (lane 1) and decode attention (lane 2, moved
-            // to lane 1), then the layer sum in the fixed operator order
-            const double tl = __builtin_fmax(Fw * iF, Bw * iB);
-            const double t2 = dpp_f64<0x101>(tl);
-            double lay = k_t0 + tl;
+            // as a block's lane prices its iteration: prefill and decode
+            // attention at this iteration, then the layer sum in the fixed
+            // operator order
+            const double mi = (double)(dG - seg0);
+            const double F1 = L.segk[0] + mi * L.segk[2];
+            const double B1 = L.segk[1] + mi * L.segk[3];
+            const double F2 = L.segk[4] + mi * L.segk[6];
+            const double B2 = L.segk[5] + mi * L.segk[7];
+            const double t1 = __builtin_fmax(F1 * iF, B1 * iB);
+            const double t2 = __builtin_fmax(F2 * iF, B2 * iB);
+            double lay = L.segk[8] + t1;
             lay = lay + t2;
-            lay = lay + k_t3;
-            lay = lay + k_t4;
-            lay = lay + k_t5;
+            lay = lay + L.segk[9];
+            lay = lay + L.segk[10];
+            lay = lay + L.segk[11];
             double tot = A.n_layers * lay;
-            tot = tot + k_lm;
+            tot = tot + L.segk[12];
             it = __builtin_fmax(ceil(tot), 1.0);
-            ubl = ubl + (lane == 1 ? used_d * it : 0.0);  // the layer sum runs in lane 1
+            ubl = ubl + (lane == 1 ? used_d * it : 0.0);  // (every lane has the same time)
             t_d = t_d + it;
-            Fw = Fw + dF;
-            Bw = Bw + dB;
             }
             if (dG == fin_at) {
               // Alive decodes emitting their last token finish at the end of
