@@ -17,7 +17,8 @@
 //   * finished requests are found by ballot and removed by a stable
 //     compaction through LDS;
 //   * steady stretches advance decodes lazily and price up to 64 iterations
-//     at once, one per lane; a head prefill's completion, the admissions
+//     at once, one per lane (while a head prefill runs, through the decodes
+//     that finish in them); a head prefill's completion, the admissions
 //     behind it and the finishes in the same iteration are handled in place;
 //   * a finish writes the request's record, from which the statistics
 //     kernel derives every latency statistic and percentile;
@@ -865,6 +866,155 @@ __device__ __forceinline__ int simulate_point(const SimArgs& A, const int pidx,
         while (more) {
           // steady iterations up to the segment's last
           while (dG != stop) {
+            if constexpr (NCH == 1 && MODE == kStageOne) {
+              if (npf == 1 && q > 0 && policy == TS_POLICY_MIXED && !swap) {
+                // A head prefill runs with the budget the decodes leave
+                // (T = K): a block of up to 64 iterations, lane i pricing
+                // iteration dG + i, runs through the decodes that finish in
+                // it.  A decode finishing at iteration e takes part in e,
+                // frees its blocks and budget from e + 1 on (the head's
+                // chunk grows by one), and writes its record with e's end.
+                // Per iteration, from prefix sums over the finishes before
+                // it: alive decodes nD_i, their key sum CD_i, the head's
+                // chunk q_i = K - nD_i and context ctx_i, the blocks freed;
+                // the four operators that depend on T only keep their
+                // segment times.  The block ends before the head prefill's
+                // completing iteration, before the first iteration short of
+                // blocks, and after the first whose end reaches an arrival
+                // that matters.
+                const int g0 = dG;
+                const int cs0 = cd_seg - nDa * seg0;  // sum of ctx0 + 1 over the alive decodes
+                close_segment();                      // the segment through g0 - 1
+                const int W = stop - g0 < 64 ? stop - g0 : 64;
+                int* hb = reinterpret_cast<int*>(&L.u);  // [4][64]: blocks taken, finishes,
+                hb[lane] = 0;                            // their keys, blocks they free
+                hb[64 + lane] = 0;
+                hb[128 + lane] = 0;
+                hb[192 + lane] = 0;
+                __syncthreads();
+                const int rr0 = rr[0];
+                const bool al = rr0 >= 0;
+                const int os = h0.rem - 1 - g0;  // the decode's finishing iteration
+                const bool fin_in = al && os >= 0 && os < W;
+                const int ob = rr0 - g0;         // its next block boundary (>= 0)
+                if (al && ob >= 0) {
+                  const int lim = fin_in ? os + 1 : W;  // boundaries through its finish
+                  for (int pz = ob; pz < lim; pz += B) atomicAdd(&hb[pz], 1);
+                }
+                if (fin_in) {
+                  const int nb = ob <= os ? divB(os - ob) + 1 : 0;  // blocks taken through it
+                  atomicAdd(&hb[64 + os], 1);
+                  atomicAdd(&hb[128 + os], h0.ctx + 1);
+                  atomicAdd(&hb[192 + os], divB(h0.ctx + rr0 + B * nb));
+                }
+                __syncthreads();
+                const bool in = lane < W;
+                const int T = scan_i32(in ? hb[lane] : 0);  // blocks taken through i
+                const int hf = in ? hb[64 + lane] : 0;
+                const int Fi = scan_i32(hf);                // finished through i
+                const int Fx = Fi - hf;                     // finished before i
+                const int hk = in ? hb[128 + lane] : 0;
+                const int KFi = scan_i32(hk);
+                const int KFx = KFi - hk;
+                const int hr = in ? hb[192 + lane] : 0;
+                const int FBi = scan_i32(hr);               // blocks freed through i
+                const int FBx = FBi - hr;
+                const int SFi = scan_i32(Fx);               // sum of Fx through i
+                const int nDi = nDa - Fx;
+                const int qi = q + Fx;
+                const int ctxi = ctx_p + lane * q + (SFi - Fx);
+                const int CDi = (cs0 - KFx) + nDi * (g0 + lane);
+                const LdsDoubles cf = roofc.tab;  // f, b0, b1, b2 per operator
+                const int64_t APi = (int64_t)qi * ctxi + ((int64_t)qi * (qi + 1)) / 2;
+                const double F1 = cf[1] * (double)APi;
+                const double B1 = (cf[9] + cf[17] * (double)(ctxi + qi)) + cf[25] * (double)qi;
+                const double F2 = cf[2] * (double)CDi;
+                const double B2 = (cf[10] + cf[18] * (double)CDi) + cf[26] * (double)nDi;
+                const double F6 = cf[6] * (double)nDi;
+                const double B6 = ((nDi == 0 ? 0.0 : cf[14]) + cf[22] * (double)nDi) + cf[30] * 0.0;
+                const double t1 = __builtin_fmax(F1 * iF, B1 * iB);
+                const double t2 = __builtin_fmax(F2 * iF, B2 * iB);
+                const double t6 = __builtin_fmax(F6 * iF, B6 * iB);
+                double lay = L.segk[8] + t1;
+                lay = lay + t2;
+                lay = lay + L.segk[9];
+                lay = lay + L.segk[10];
+                lay = lay + L.segk[11];
+                double tot = A.n_layers * lay;
+                tot = tot + t6;
+                const double itv = __builtin_fmax(ceil(tot), 1.0);
+                const double tend = rdl_f64(t_d, 1) + scan_f64(in ? itv : 0.0);
+                const uint64_t short_m = ballot(in && T > freeb + FBx);
+                const uint64_t arr_m = watch ? ballot(in && tend >= thr) : 0ull;
+                const uint64_t comp_m = ballot(in && ctxi + qi >= tgt_p);
+                int Kb = W;
+                if (short_m != 0) {
+                  const int k = (int)__builtin_ctzll(short_m);
+                  Kb = k < Kb ? k : Kb;
+                }
+                if (arr_m != 0) {
+                  const int k = (int)__builtin_ctzll(arr_m) + 1;
+                  Kb = k < Kb ? k : Kb;
+                }
+                const int kcomp = comp_m != 0 ? (int)__builtin_ctzll(comp_m) : 64;
+                Kb = kcomp < Kb ? kcomp : Kb;
+                if (Kb > 0) {
+                  const int last = Kb - 1;
+                  // used blocks during each iteration (after its reservations,
+                  // before its frees): the integral and the peak
+                  const int used = NB - freeb + T - FBx;
+                  ubl = ubl + (lane < Kb ? (double)used * itv : 0.0);
+                  const int upk = rdl(scan_max_i32(lane < Kb ? used : 0), 63);
+                  peak = upk > peak ? upk : peak;
+                  // the decodes finishing here: end of their iteration, and
+                  // the largest iteration time through it since the last fold
+                  const int64_t tl = (int64_t)tend;
+                  const int64_t pm = scan_max_i64(in ? (int64_t)itv : 0);
+                  const bool fin = fin_in && os <= last;
+                  const int src = (fin ? os : lane) << 2;
+                  const int64_t t_fin = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_ds_bpermute(
+                                                       src, (int)((uint64_t)tl >> 32)) << 32) |
+                                                   (uint32_t)__builtin_amdgcn_ds_bpermute(src, (int)tl));
+                  const int64_t pm_fin = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_ds_bpermute(
+                                                        src, (int)((uint64_t)pm >> 32)) << 32) |
+                                                    (uint32_t)__builtin_amdgcn_ds_bpermute(src, (int)pm));
+                  const int64_t em0 = (int64_t)rdl_f64(em, 1);
+                  const int64_t gx = pm_fin > em0 ? pm_fin : em0;
+                  record_done(fin, lane, t_fin, gx > h0.gap ? gx : h0.gap);
+                  if (al && !fin && ob >= 0 && ob < Kb) rr[0] = rr0 + B * (divB(last - ob) + 1);
+                  rr[0] = fin ? -0x40000000 : rr[0];
+                  const int nfin = rdl(Fi, last);
+                  const int sumF = rdl(SFi, last);  // the chunks' growth over the block
+                  pf_tok += (int64_t)Kb * q + sumF;
+                  dec_tok += (int64_t)Kb * nDa - sumF;
+                  ctx_p += Kb * q + sumF;
+                  freeb += rdl(FBi, last) - rdl(T, last);
+                  n_done += nfin;
+                  nDa -= nfin;
+                  nruna -= nfin;
+                  q = K - nDa;
+                  dG = g0 + Kb;
+                  seg0 = dG;
+                  cd_seg = (cs0 - rdl(KFi, last)) + nDa * dG;
+                  t_d = rdl_f64(tend, last);
+                  it = rdl_f64(itv, last);
+                  em = __builtin_fmax(em, (double)rdl64(pm, last));
+                }
+                if (comp_m != 0 && Kb == kcomp) stop = dG;  // the head prefill completes at dG
+                if (dG == stop) {
+                  // the completing iteration finds the decodes finishing in
+                  // it by fin_at
+                  const bool al1 = rr[0] >= 0;
+                  const int mx = rdl(scan_max_i32(al1 ? 0x7fffffff - h0.rem : 0), 63);
+                  fin_at = nDa > 0 ? 0x7fffffff - mx - 1 : 0x3fffffff;
+                }
+                if (!next_ok()) {
+                  more = false;
+                  break;
+                }
+                continue;
+              }
+            }
             // iterations that may run as one block: up to 64, through the
             // segment's last and its first finishing iteration
             int W = stop - dG;
