@@ -768,6 +768,16 @@ __device__ __forceinline__ int simulate_point(const SimArgs& A, const int pidx,
         // Segment set-up at iteration dG: the alive decodes' first finishing
         // iteration and key sum, the head prefill's chunk, every operator's
         // work and its per-iteration step, and the segment's last iteration.
+        // segk[8..11] hold the times of the operators that depend on T only
+        // at T = K (the last full set-up had a head prefill running)
+        bool tk_ok = false;
+        // the segment runs as blocks through finishes (64 slots, one worker,
+        // continuous batching with recompute preemption, a head prefill
+        // running with a token budget left)
+        auto through_fin = [&]() {
+          return NCH == 1 && MODE == kStageOne && npf == 1 && q > 0 &&
+                 policy == TS_POLICY_MIXED && !swap;
+        };
         auto setup = [&]() {
           // per lane over the chunks first, then one reduction each
           int mxl = 0, csl = 0;
@@ -788,27 +798,33 @@ __device__ __forceinline__ int simulate_point(const SimArgs& A, const int pidx,
           fin_at = nDa > 0 ? 0x7fffffff - mx - 1 : 0x3fffffff;
           cd_seg = cs + nDa * dG;
           q = npf > 0 ? K - nDa : 0;
-          const int64_t AP0 = (int64_t)q * ctx_p + ((int64_t)q * (q + 1)) / 2;
-          double Fw, Bw;
-          lane_work(roofc, nDa + q, q, AP0, q > 0 ? ctx_p + q : 0, nDa, cd_seg, nDa, &Fw, &Bw);
-          const double dX = roofc.is_attp ? (double)((int64_t)q * q)
-                                          : (roofc.is_attd ? (double)nDa : 0.0);
-          const double dY = roofc.is_attp ? (double)q : (roofc.is_attd ? (double)nDa : 0.0);
-          // the segment's constants in LDS, where every iteration reads
-          // them: the attention operators' FLOPs and bytes at the segment
-          // start and their steps per iteration (lanes 1, 2), then the other
-          // operators' times (lanes 0, 3, 4, 5, 6)
-          if (lane == 1 || lane == 2) {
-            double* k = &L.segk[(lane - 1) * 4];
-            k[0] = Fw;
-            k[1] = Bw;
-            k[2] = roofc.f() * dX;
-            k[3] = roofc.b1() * dY;
-          } else if (lane < 7) {
-            L.segk[lane == 0 ? 8 : lane + 6] = __builtin_fmax(Fw * iF, Bw * iB);
+          // A segment of blocks through finishes prices every operator but
+          // the four that depend on T only, whose times it takes from a
+          // set-up with a head prefill running (T = K in all of them).
+          if (!(through_fin() && tk_ok)) {
+            const int64_t AP0 = (int64_t)q * ctx_p + ((int64_t)q * (q + 1)) / 2;
+            double Fw, Bw;
+            lane_work(roofc, nDa + q, q, AP0, q > 0 ? ctx_p + q : 0, nDa, cd_seg, nDa, &Fw, &Bw);
+            const double dX = roofc.is_attp ? (double)((int64_t)q * q)
+                                            : (roofc.is_attd ? (double)nDa : 0.0);
+            const double dY = roofc.is_attp ? (double)q : (roofc.is_attd ? (double)nDa : 0.0);
+            // the segment's constants in LDS, where every iteration reads
+            // them: the attention operators' FLOPs and bytes at the segment
+            // start and their steps per iteration (lanes 1, 2), then the other
+            // operators' times (lanes 0, 3, 4, 5, 6)
+            if (lane == 1 || lane == 2) {
+              double* k = &L.segk[(lane - 1) * 4];
+              k[0] = Fw;
+              k[1] = Bw;
+              k[2] = roofc.f() * dX;
+              k[3] = roofc.b1() * dY;
+            } else if (lane < 7) {
+              L.segk[lane == 0 ? 8 : lane + 6] = __builtin_fmax(Fw * iF, Bw * iB);
+            }
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+            __builtin_amdgcn_wave_barrier();
+            tk_ok = npf > 0;  // T = nDa + (K - nDa)
           }
-          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-          __builtin_amdgcn_wave_barrier();
           stop = stop_hard;
           if (q > 0) {  // the head prefill completes in iteration kc
             // floor(n / q) for 0 <= n < 2^21 and 1 <= q <= 2^20 (a target
@@ -867,7 +883,7 @@ __device__ __forceinline__ int simulate_point(const SimArgs& A, const int pidx,
           // steady iterations up to the segment's last
           while (dG != stop) {
             if constexpr (NCH == 1 && MODE == kStageOne) {
-              if (npf == 1 && q > 0 && policy == TS_POLICY_MIXED && !swap) {
+              if (through_fin()) {
                 // A head prefill runs with the budget the decodes leave
                 // (T = K): a block of up to 64 iterations, lane i pricing
                 // iteration dG + i, runs through the decodes that finish in
