@@ -771,11 +771,11 @@ __device__ __forceinline__ int simulate_point(const SimArgs& A, const int pidx,
         // segk[8..11] hold the times of the operators that depend on T only
         // at T = K (the last full set-up had a head prefill running)
         bool tk_ok = false;
-        // the segment runs as blocks through finishes (64 slots, one worker,
+        // the segment runs as blocks through finishes (64 or 128 slots, one worker,
         // continuous batching with recompute preemption, a head prefill
         // running with a token budget left)
         auto through_fin = [&]() {
-          return NCH == 1 && MODE == kStageOne && npf == 1 && q > 0 &&
+          return NCH <= 2 && MODE == kStageOne && npf == 1 && q > 0 &&
                  policy == TS_POLICY_MIXED && !swap;
         };
         auto setup = [&]() {
@@ -882,7 +882,7 @@ __device__ __forceinline__ int simulate_point(const SimArgs& A, const int pidx,
         while (more) {
           // steady iterations up to the segment's last
           while (dG != stop) {
-            if constexpr (NCH == 1 && MODE == kStageOne) {
+            if constexpr (NCH <= 2 && MODE == kStageOne) {
               if (through_fin()) {
                 // A head prefill runs with the budget the decodes leave
                 // (T = K): a block of up to 64 iterations, lane i pricing
@@ -908,20 +908,32 @@ __device__ __forceinline__ int simulate_point(const SimArgs& A, const int pidx,
                 hb[128 + lane] = 0;
                 hb[192 + lane] = 0;
                 __syncthreads();
-                const int rr0 = rr[0];
-                const bool al = rr0 >= 0;
-                const int os = h0.rem - 1 - g0;  // the decode's finishing iteration
-                const bool fin_in = al && os >= 0 && os < W;
-                const int ob = rr0 - g0;         // its next block boundary (>= 0)
-                if (al && ob >= 0) {
-                  const int lim = fin_in ? os + 1 : W;  // boundaries through its finish
-                  for (int pz = ob; pz < lim; pz += B) atomicAdd(&hb[pz], 1);
-                }
-                if (fin_in) {
-                  const int nb = ob <= os ? divB(os - ob) + 1 : 0;  // blocks taken through it
-                  atomicAdd(&hb[64 + os], 1);
-                  atomicAdd(&hb[128 + os], h0.ctx + 1);
-                  atomicAdd(&hb[192 + os], divB(h0.ctx + rr0 + B * nb));
+                // per slot: its finishing iteration in the block (W: none)
+                int osj[NCH];
+#pragma unroll
+                for (int j = 0; j < NCH; ++j) {
+                  osj[j] = W;
+                  if (j < nchd) {
+                    const int e = (j - 1) * 64 + lane;
+                    const int rem0 = j == 0 ? h0.rem : L.x_rem[e];
+                    const int ctx0 = j == 0 ? h0.ctx : L.x_ctx[e];
+                    const int rrj = rr[j];
+                    const bool al = rrj >= 0;
+                    const int os = rem0 - 1 - g0;  // the decode's finishing iteration
+                    const bool fin_in = al && os >= 0 && os < W;
+                    const int ob = rrj - g0;       // its next block boundary (>= 0)
+                    if (al && ob >= 0) {
+                      const int lim = fin_in ? os + 1 : W;  // boundaries through its finish
+                      for (int pz = ob; pz < lim; pz += B) atomicAdd(&hb[pz], 1);
+                    }
+                    if (fin_in) {
+                      const int nb = ob <= os ? divB(os - ob) + 1 : 0;  // blocks taken through it
+                      atomicAdd(&hb[64 + os], 1);
+                      atomicAdd(&hb[128 + os], ctx0 + 1);
+                      atomicAdd(&hb[192 + os], divB(ctx0 + rrj + B * nb));
+                      osj[j] = os;
+                    }
+                  }
                 }
                 __syncthreads();
                 const bool in = lane < W;
@@ -986,19 +998,32 @@ __device__ __forceinline__ int simulate_point(const SimArgs& A, const int pidx,
                   // the largest iteration time through it since the last fold
                   const int64_t tl = (int64_t)tend;
                   const int64_t pm = scan_max_i64(in ? (int64_t)itv : 0);
-                  const bool fin = fin_in && os <= last;
-                  const int src = (fin ? os : lane) << 2;
-                  const int64_t t_fin = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_ds_bpermute(
-                                                       src, (int)((uint64_t)tl >> 32)) << 32) |
-                                                   (uint32_t)__builtin_amdgcn_ds_bpermute(src, (int)tl));
-                  const int64_t pm_fin = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_ds_bpermute(
-                                                        src, (int)((uint64_t)pm >> 32)) << 32) |
-                                                    (uint32_t)__builtin_amdgcn_ds_bpermute(src, (int)pm));
                   const int64_t em0 = (int64_t)rdl_f64(em, 1);
-                  const int64_t gx = pm_fin > em0 ? pm_fin : em0;
-                  record_done(fin, lane, t_fin, gx > h0.gap ? gx : h0.gap);
-                  if (al && !fin && ob >= 0 && ob < Kb) rr[0] = rr0 + B * (divB(last - ob) + 1);
-                  rr[0] = fin ? -0x40000000 : rr[0];
+                  auto lane64 = [](int src, int64_t v) {  // v of lane src / 4
+                    return (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_ds_bpermute(
+                                          src, (int)((uint64_t)v >> 32)) << 32) |
+                                     (uint32_t)__builtin_amdgcn_ds_bpermute(src, (int)v));
+                  };
+#pragma unroll
+                  for (int j = 0; j < NCH; ++j) {
+                    if (j < nchd) {
+                      const int e = (j - 1) * 64 + lane;
+                      const int os = osj[j];
+                      const bool fin = os <= last;
+                      if (ballot(fin) != 0) {
+                        const int src = (fin ? os : lane) << 2;
+                        const int64_t t_fin = lane64(src, tl);
+                        const int64_t pm_fin = lane64(src, pm);
+                        const int64_t gx = pm_fin > em0 ? pm_fin : em0;
+                        const int64_t gap0 = j == 0 ? h0.gap : L.x_gap[e];
+                        record_done(fin, j * 64 + lane, t_fin, gx > gap0 ? gx : gap0);
+                      }
+                      const int rrj = rr[j];
+                      const int ob = rrj - g0;
+                      if (rrj >= 0 && !fin && ob >= 0 && ob < Kb) rr[j] = rrj + B * (divB(last - ob) + 1);
+                      rr[j] = fin ? -0x40000000 : rr[j];
+                    }
+                  }
                   const int nfin = rdl(Fi, last);
                   const int sumF = rdl(SFi, last);  // the chunks' growth over the block
                   pf_tok += (int64_t)Kb * q + sumF;
@@ -1020,8 +1045,16 @@ __device__ __forceinline__ int simulate_point(const SimArgs& A, const int pidx,
                 if (dG == stop) {
                   // the completing iteration finds the decodes finishing in
                   // it by fin_at
-                  const bool al1 = rr[0] >= 0;
-                  const int mx = rdl(scan_max_i32(al1 ? 0x7fffffff - h0.rem : 0), 63);
+                  int mxl = 0;
+#pragma unroll
+                  for (int j = 0; j < NCH; ++j) {
+                    if (j < nchd) {
+                      const int rem0 = j == 0 ? h0.rem : L.x_rem[(j - 1) * 64 + lane];
+                      const int m = rr[j] >= 0 ? 0x7fffffff - rem0 : 0;
+                      mxl = m > mxl ? m : mxl;
+                    }
+                  }
+                  const int mx = rdl(scan_max_i32(mxl), 63);
                   fin_at = nDa > 0 ? 0x7fffffff - mx - 1 : 0x3fffffff;
                 }
                 if (!next_ok()) {
