@@ -793,15 +793,21 @@ __device__ __forceinline__ int simulate_point(const SimArgs& A, const int pidx,
               csl += al ? ctx0 + 1 : 0;
             }
           }
-          const int mx = rdl(scan_max_i32(mxl), 63);
           const int cs = wsum(csl);
-          fin_at = nDa > 0 ? 0x7fffffff - mx - 1 : 0x3fffffff;
           cd_seg = cs + nDa * dG;
           q = npf > 0 ? K - nDa : 0;
+          // the first finishing iteration; blocks through finishes need it
+          // only for a head prefill completing at once
+          auto first_finish = [&]() {
+            const int mx = rdl(scan_max_i32(mxl), 63);
+            fin_at = nDa > 0 ? 0x7fffffff - mx - 1 : 0x3fffffff;
+          };
+          const bool tf = through_fin();
+          if (!tf) first_finish();
           // A segment of blocks through finishes prices every operator but
           // the four that depend on T only, whose times it takes from a
           // set-up with a head prefill running (T = K in all of them).
-          if (!(through_fin() && tk_ok)) {
+          if (!(tf && tk_ok)) {
             const int64_t AP0 = (int64_t)q * ctx_p + ((int64_t)q * (q + 1)) / 2;
             double Fw, Bw;
             lane_work(roofc, nDa + q, q, AP0, q > 0 ? ctx_p + q : 0, nDa, cd_seg, nDa, &Fw, &Bw);
@@ -839,6 +845,7 @@ __device__ __forceinline__ int simulate_point(const SimArgs& A, const int pidx,
             const int kc = dG + kq;
             stop = kc < stop ? kc : stop;
           }
+          if (tf && stop == dG) first_finish();
           // arrivals matter within the segment only if one could be admitted
           watch = adm_open() && npre == 0 && nwait == 0;
           seg0 = dG;
@@ -992,12 +999,16 @@ __device__ __forceinline__ int simulate_point(const SimArgs& A, const int pidx,
                   // before its frees): the integral and the peak
                   const int used = NB - freeb + T - FBx;
                   ubl = ubl + (lane < Kb ? (double)used * itv : 0.0);
-                  const int upk = rdl(scan_max_i32(lane < Kb ? used : 0), 63);
+                  // (with no finish in the block the used blocks and the
+                  // iteration times only grow: the last ones are the largest)
+                  const int nfin = rdl(Fi, last);
+                  const int upk = nfin > 0 ? rdl(scan_max_i32(lane < Kb ? used : 0), 63)
+                                           : rdl(used, last);
                   peak = upk > peak ? upk : peak;
                   // the decodes finishing here: end of their iteration, and
                   // the largest iteration time through it since the last fold
                   const int64_t tl = (int64_t)tend;
-                  const int64_t pm = scan_max_i64(in ? (int64_t)itv : 0);
+                  const int64_t pm = nfin > 0 ? scan_max_i64(in ? (int64_t)itv : 0) : 0;
                   const int64_t em0 = (int64_t)rdl_f64(em, 1);
                   auto lane64 = [](int src, int64_t v) {  // v of lane src / 4
                     return (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_ds_bpermute(
@@ -1024,7 +1035,6 @@ __device__ __forceinline__ int simulate_point(const SimArgs& A, const int pidx,
                       rr[j] = fin ? -0x40000000 : rr[j];
                     }
                   }
-                  const int nfin = rdl(Fi, last);
                   const int sumF = rdl(SFi, last);  // the chunks' growth over the block
                   pf_tok += (int64_t)Kb * q + sumF;
                   dec_tok += (int64_t)Kb * nDa - sumF;
@@ -1039,7 +1049,7 @@ __device__ __forceinline__ int simulate_point(const SimArgs& A, const int pidx,
                   cd_seg = (cs0 - rdl(KFi, last)) + nDa * dG;
                   t_d = rdl_f64(tend, last);
                   it = rdl_f64(itv, last);
-                  em = __builtin_fmax(em, (double)rdl64(pm, last));
+                  em = __builtin_fmax(em, nfin > 0 ? (double)rdl64(pm, last) : it);
                 }
                 if (comp_m != 0 && Kb == kcomp) stop = dG;  // the head prefill completes at dG
                 if (dG == stop) {
