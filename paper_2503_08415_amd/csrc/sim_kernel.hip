@@ -771,12 +771,11 @@ __device__ __forceinline__ int simulate_point(const SimArgs& A, const int pidx,
         // segk[8..11] hold the times of the operators that depend on T only
         // at T = K (the last full set-up had a head prefill running)
         bool tk_ok = false;
-        // the segment runs as blocks through finishes (64 or 128 slots, one worker,
-        // continuous batching with recompute preemption, a head prefill
-        // running with a token budget left)
+        // the segment runs as blocks through finishes (64 or 128 slots,
+        // simple points: one worker, continuous batching with recompute
+        // preemption; a head prefill running with a token budget left)
         auto through_fin = [&]() {
-          return NCH <= 2 && MODE == kStageOne && npf == 1 && q > 0 &&
-                 policy == TS_POLICY_MIXED && !swap;
+          return SIMPLE && NCH <= 2 && npf == 1 && q > 0;
         };
         auto setup = [&]() {
           // per lane over the chunks first, then one reduction each
@@ -889,7 +888,7 @@ __device__ __forceinline__ int simulate_point(const SimArgs& A, const int pidx,
         while (more) {
           // steady iterations up to the segment's last
           while (dG != stop) {
-            if constexpr (NCH <= 2 && MODE == kStageOne) {
+            if constexpr (SIMPLE && NCH <= 2) {
               if (through_fin()) {
                 // A head prefill runs with the budget the decodes leave
                 // (T = K): a block of up to 64 iterations, lane i pricing
