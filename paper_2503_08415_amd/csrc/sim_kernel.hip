@@ -713,7 +713,11 @@ __device__ __forceinline__ int simulate_point(const SimArgs& A, const int pidx,
           tgt_p = __builtin_amdgcn_readfirstlane(L.x_tgt[(jp - 1) * 64 + lp]);
           fl_p = __builtin_amdgcn_readfirstlane(L.x_fl[(jp - 1) * 64 + lp]);
         }
-        if (tgt_p - ctx_p <= K - nD) go = false;  // the head prefill completes now
+        // the head prefill completes now: the general path, except for a
+        // simple point's fresh head, which the stretch's first (completing)
+        // iteration handles in place
+        if (tgt_p - ctx_p <= K - nD && (!SIMPLE || (fl_p & (FL_FIRST | FL_STALE)) != 0))
+          go = false;
       }
       constexpr int64_t kT52 = (int64_t)1 << 52;
       if (n_iters >= A.iter_cap || t >= kT52) go = false;
