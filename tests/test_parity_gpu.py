@@ -550,6 +550,43 @@ def test_hand_over_records_under_memory_pressure(S, oracle, seed, takeover):
     assert sum(work) == int(o_out["n_iters"].sum())
 
 
+@pytest.mark.parametrize("seed", [11, 12])
+def test_blocks_through_simultaneous_finishes(S, oracle, seed):
+    """Simple points whose decodes finish while a long head prefill runs:
+    groups of requests with equal outputs admitted together finish in the
+    same iteration, short prompts ride behind long chunked ones, and tight
+    KV budgets with block sizes 1 to 16 make iterations run short of blocks
+    inside a block of iterations.  Every request against the oracle."""
+    m = {"n_layers": 2, "d_model": 64, "n_heads": 4, "n_kv_heads": 2, "ffn_dim": 128,
+         "ffn_gated": 1, "vocab": 100, "w_bytes": 2, "kv_bytes": 2, "weights_in_capacity": 0}
+    rng = np.random.default_rng(seed)
+    traces = []
+    for _ in range(4):
+        n = int(rng.integers(150, 300))
+        arr = np.sort(rng.integers(0, 400_000_000, n)).astype(np.int64)
+        arr[: n // 3] = arr[0]  # a burst admitted together
+        prompt = np.where(rng.random(n) < 0.3, rng.integers(600, 3000, n),
+                          rng.integers(1, 60, n)).astype(np.int32)
+        output = rng.choice([8, 16, 17, 40], n).astype(np.int32)  # equal outputs finish together
+        traces.append({"arrival_ns": arr, "prompt_len": prompt, "output_len": output})
+    k = 48
+    kv_tok = 2 * 2 * (64 // 4 * 2) * 2
+    pts = {"peak_flops": rng.choice([1e12, 5e12], k), "mem_bw": rng.choice([1e11, 1e12], k),
+           "capacity_bytes": (rng.integers(3200, 20000, k) * kv_tok).astype(np.int64),
+           "mem_util_permille": np.full(k, 1000, np.int32),
+           "block_size": rng.choice([1, 2, 4, 16], k).astype(np.int32),
+           "max_batch": rng.choice([16, 64, 100, 128], k).astype(np.int32),
+           "trace_id": rng.integers(0, len(traces), k).astype(np.int32)}
+    pts["chunk_size"] = np.maximum(rng.choice([64, 128, 256], k), pts["max_batch"]).astype(np.int32)
+    o_all, _ = oracle.run_points(m, traces, pts)
+    pts = W.subset_points(pts, np.nonzero(o_all["n_rejected"] == 0)[0])  # simple points only
+    o_out, o_req = oracle.run_points(m, traces, pts, per_request=True)
+    out, req = gpu_run(S, m, traces, pts, per_request=True, iter_cap=cap_from(o_out))
+    compare_points(out, o_out, "simultaneous finishes")
+    compare_requests(req, o_req, "simultaneous finishes")
+    assert int(o_out["n_done"].sum()) > 5000
+
+
 def test_percentiles_when_many_latencies_are_equal(S, oracle):
     """Requests served one at a time with equal lengths have equal latencies:
     far more of them share a latency bucket than the statistics kernel keeps
